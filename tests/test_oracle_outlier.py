@@ -1,0 +1,115 @@
+"""Pins for the oracle's outlier-aware path (Sec. 5).
+
+* P_s against an independent selection (numpy lexsort on (-|v|, index));
+* Lemma 3: the IHT step never increases g (H sparse, ||H||_0 <= s);
+* s = 0 reduces to the plain CD of Sec. 4;
+* Sigma = c I: V = H - E/c = W - What in closed form, so H+ = P_s(W - What);
+* lambda_max on a matrix with known eigenvalues (Householder-rotated diagonal);
+* the initialisation H = P_s(W), What = W - H keeps What + H = W exactly.
+"""
+import numpy as np
+import pytest
+
+import synth
+
+
+def lexsort_topk(v, s):
+    v = np.asarray(v, np.float64).reshape(-1)
+    order = np.lexsort((np.arange(v.size), -np.abs(v)))
+    sel = [e for e in order[:s] if v[e] != 0.0]
+    return np.sort(np.array(sel, np.int64))
+
+
+@pytest.mark.parametrize("s", [0, 1, 7, 50, 400, 1000])
+def test_topk_matches_lexsort(oracle, s):
+    V = synth.gaussian((20, 30), seed=1)
+    # inject exact ties in |v| and exact zeros
+    V.reshape(-1)[::17] = 0.5
+    V.reshape(-1)[5::23] = -0.5
+    V.reshape(-1)[3::7] = 0.0
+    sup, Hp = oracle.topk_abs(V, s)
+    assert np.array_equal(sup, lexsort_topk(V, s))
+    flat = Hp.reshape(-1)
+    assert np.array_equal(flat[sup], V.reshape(-1)[sup])
+    mask = np.ones(V.size, bool)
+    mask[sup] = False
+    assert np.all(flat[mask] == 0)
+
+
+def test_topk_threshold_property(oracle):
+    V = synth.gaussian((64, 64), seed=2)
+    s = 300
+    sup, _ = oracle.topk_abs(V, s)
+    a = np.abs(V.reshape(-1))
+    kept = a[sup]
+    rest = np.delete(a, sup)
+    assert len(sup) == s and kept.min() >= rest.max()
+
+
+def _layer(q, p, n, seed, corr=0.9):
+    W = synth.gaussian((q, p), seed=seed, std=0.05)
+    W.reshape(-1)[::37] *= 8.0
+    X = synth.correlated_activations(p, n, corr, seed)
+    return W, X
+
+
+def test_init_sums_to_w(oracle):
+    W, _ = _layer(16, 20, 10, 3)
+    sup, H, Wh = oracle.outlier_init(W, 12)
+    assert len(sup) == 12
+    assert np.array_equal(Wh + H, W.astype(np.float64))
+
+
+def test_zero_budget_is_plain_cd(oracle):
+    W, X = _layer(24, 30, 90, 4)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    sc, ze = oracle.grid_minmax(W, 3)
+    lam = oracle.lambda_max(S)
+    r0 = oracle.outlier(W, S, 3, sc, ze, 0, lam, 4)
+    rc = oracle.cd(W, S, 3, sc, ze, 4)
+    assert np.array_equal(r0.codes, rc.codes)
+    assert np.array_equal(r0.What, rc.What)
+    assert np.allclose(r0.g, rc.obj, rtol=1e-12)
+    assert not np.any(r0.H)
+
+
+@pytest.mark.parametrize("seed", [5, 6])
+def test_iht_step_descends(oracle, seed):
+    W, X = _layer(30, 36, 100, seed)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    s = int(0.02 * W.size)
+    sup0, H0, _ = oracle.outlier_init(W, s)
+    sc, ze = oracle.grid_minmax(W, 3, H0)
+    lam = oracle.lambda_max(S)
+    r = oracle.outlier(W, S, 3, sc, ze, s, lam, 6)
+    for k in range(6):
+        assert r.g[k] <= r.g_cd[k] * (1 + 1e-12), k          # Lemma 3
+        if k > 0:
+            assert r.g_cd[k] <= r.g[k - 1] * (1 + 1e-12), k  # CD step, H fixed
+        assert len(r.support_hist[k]) <= s
+
+
+def test_identity_sigma_closed_form(oracle):
+    W, _ = _layer(12, 16, 10, 7)
+    c = 2.5
+    S = c * np.eye(16)
+    s = 20
+    sup0, H0, _ = oracle.outlier_init(W, s)
+    sc, ze = oracle.grid_minmax(W, 3, H0)
+    r = oracle.outlier(W, S, 3, sc, ze, s, c, 1)
+    # with Sigma = c I the CD step is round-to-nearest of W - H0 ...
+    t = (W.astype(np.float64) - H0) / sc[:, None].astype(np.float64) + ze[:, None]
+    assert np.array_equal(r.codes, np.clip(np.rint(t), 0, 7))
+    # ... and V = H - (What + H - W) c / c = W - What
+    _, Hp = oracle.topk_abs(W.astype(np.float64) - r.What, s)
+    assert np.array_equal(r.H, Hp)
+
+
+def test_lambda_max_known_spectrum(oracle):
+    p = 40
+    lam = np.linspace(0.5, 7.25, p)
+    v = synth.gaussian((p,), seed=8).astype(np.float64)
+    v /= np.linalg.norm(v)
+    Q = np.eye(p) - 2.0 * np.outer(v, v)        # Householder reflection: orthogonal
+    S = Q @ np.diag(lam) @ Q.T
+    assert oracle.lambda_max(S) == pytest.approx(7.25, rel=1e-13)
