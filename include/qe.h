@@ -1,0 +1,195 @@
+/*
+ * qe.h -- C ABI of the MI355X (gfx950) QuantEase hot-path library, libqe.so.
+ *
+ * QuantEase (arXiv 2309.01885) quantizes one linear layer at a time by
+ * minimising f(What) = ||W X - What X||_F^2 over a per-output-channel uniform
+ * b-bit grid (Sec. 3, problem (1)), with cyclic coordinate descent (Sec. 4)
+ * and, optionally, a sparse full-precision outlier matrix H chosen by
+ * iterative hard thresholding (Sec. 5).
+ *
+ * Conventions shared by every entry point:
+ *  - Matrices are dense, row-major, contiguous fp32 in DEVICE memory (HBM)
+ *    unless stated otherwise: W, What, R/E, H are q x p (q output channels,
+ *    p input channels); Sigma is p x p and symmetric; X is p x n or n x p.
+ *  - The library never allocates or frees caller memory.  Scratch space comes
+ *    from the caller as a device workspace `ws` of at least the size returned
+ *    by the matching *_workspace_size query; the first 256 bytes of every
+ *    workspace hold a device status word.
+ *  - All work is enqueued on `stream` (a hipStream_t; NULL = the default
+ *    stream) and is asynchronous.  Host-detectable argument errors return
+ *    immediately with nothing enqueued.  Data-dependent errors (a
+ *    non-positive diagonal entry of Sigma, a non-finite or non-positive grid
+ *    scale) are written to the workspace status word, the remaining kernels
+ *    of that call become no-ops, and qe_sync_status() reports them.
+ *  - Results are bitwise deterministic for a fixed shape, block width and
+ *    flag set (no floating-point atomics anywhere).
+ *  - Concurrent calls on different streams need disjoint workspaces and
+ *    outputs.
+ */
+#ifndef QE_H
+#define QE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int qe_status;
+
+#define QE_OK              0
+#define QE_ERR_ARG         1  /* null pointer, bad size, bits outside [1, 8], ... */
+#define QE_ERR_DIAG        2  /* some Sigma_jj <= 0 or not finite (Lemma 1 assumes Sigma_jj > 0) */
+#define QE_ERR_SCALE       3  /* some grid scale <= 0 or not finite */
+#define QE_ERR_WORKSPACE   4  /* workspace null or smaller than the size query */
+#define QE_ERR_HIP         5  /* a HIP runtime call failed */
+#define QE_ERR_UNSUPPORTED 6  /* a valid request this build does not implement */
+
+/* Layouts of X for qe_gram. */
+#define QE_LAYOUT_PN 0        /* X is p x n: each channel's n tokens contiguous */
+#define QE_LAYOUT_NP 1        /* X is n x p: each token's p channels contiguous */
+
+/* Flags for qe_cd_sweep / qe_cd_outlier_sweep. */
+#define QE_INIT_FROM_W 0x1u   /* start from What = W (Sec. 4.1) or What = W - H (Sec. 5.3);
+                                 R (or E) is set to 0; codes are not yet valid */
+#define QE_R_VALID     0x2u   /* R (or E) already holds (What [+ H] - W) Sigma: resume */
+#define QE_CODES_VALID 0x4u   /* codes hold What's grid codes: the keep-current tie rule of the
+                                 modified CD (Sec. 4.3) applies from the first sweep */
+
+/* Human-readable name of a status code (static string). */
+const char* qe_status_string(qe_status s);
+
+/* Library ABI version (increases on any signature change). */
+int qe_version(void);
+
+/* Synchronises `stream`, then returns the status word of workspace `ws`
+ * (QE_OK if no kernel reported a data error).  Also clears the word. */
+qe_status qe_sync_status(void* ws, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Gram matrix.  Lemma 1 (Sec. 4.2) works with Sigma = X X^T, whose size is
+ * independent of the token count n (Sec. 4.2, "Memory Footprint").
+ *   Sigma (+)= X X^T; then, if damp > 0, Sigma_jj += damp * mean_j(Sigma_jj).
+ * X: p x n (QE_LAYOUT_PN) or n x p (QE_LAYOUT_NP), fp32, device.
+ * Sigma: p x p fp32, device; overwritten (accumulate = 0) or added to
+ * (accumulate = 1, for token chunks streamed through several calls; pass
+ * damp = 0 on all but the last).  The result is exactly symmetric.
+ * Accumulation: fp32 matrix-core products over short token chunks, chunk
+ * sums added in fp32, split partial sums reduced in fp64.
+ * ------------------------------------------------------------------------ */
+size_t qe_gram_workspace_size(int64_t p, int64_t n);
+qe_status qe_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma,
+                  int accumulate, float damp, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Per-row uniform grid Q_i = { scale_i (k - zero_i) : k = 0 .. 2^bits - 1 }
+ * (Sec. 3: uniformly spaced levels per output channel).  Asymmetric min/max
+ * reading: lo = min(0, min_j W_ij), hi = max(0, max_j W_ij), an all-zero row
+ * uses [-1, 1]; scale = (hi - lo) / (2^bits - 1), zero = rint(-lo / scale),
+ * all in fp32.  Entries with H_ij != 0 are excluded (outlier-aware grid,
+ * Sec. 5.3); H may be NULL.
+ * W, H: q x p device.  scale, zero: q floats each, device, written.
+ * ------------------------------------------------------------------------ */
+qe_status qe_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, int bits,
+                         float* scale, float* zero, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Blocked cyclic coordinate descent (Sec. 4; Lemma 1; the rank-1 identity of
+ * Sec. 4.2; Algorithm "QuantEase").
+ * Residual form: R = (What - W) Sigma.  For each column j in order, for all
+ * rows i at once:  beta = What_ij - R_ij / Sigma_jj;  What_ij <- q_i(beta)
+ * (nearest grid level, half to even, a valid equally-near current level is
+ * kept, Sec. 4.3);  R += (What_new - What_old)_{:,j} Sigma_{j,:}.
+ * Columns are processed in blocks of `block` (0 = 128; one of 16, 32, 64,
+ * 128): inside a block the rank-1 updates touch only the block's columns;
+ * the accumulated block update is then applied to every column as one
+ * matrix-core GEMM.  The result equals the column-by-column algorithm up to
+ * floating-point rounding.
+ *
+ * W:      q x p, device, read (only for R initialisation and the objective).
+ * Sigma:  p x p, device, symmetric with Sigma_jj > 0 (else QE_ERR_DIAG).
+ * scale, zero: q floats, device (e.g. from qe_grid_minmax); bits in [1, 8].
+ * W_hat:  q x p, device, in/out.  codes: q x p uint8, device, in/out.
+ * R:      q x p, device, in/out: (What - W) Sigma on exit.
+ * sweeps: >= 0 full passes over the columns.
+ * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID.  Without
+ *         QE_INIT_FROM_W and without QE_R_VALID, R is first computed as
+ *         (What - W) Sigma (warm start from any What, Sec. 4.1).
+ * obj:    NULL, or device array of `sweeps` doubles receiving
+ *         f_k = <What - W, R> = ||(W - What) X||_F^2 after sweep k.
+ * ------------------------------------------------------------------------ */
+size_t qe_cd_workspace_size(int64_t q, int64_t p, int block);
+qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
+                      const float* scale, const float* zero, float* W_hat, uint8_t* codes,
+                      float* R, int sweeps, int block, uint32_t flags, double* obj,
+                      void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Outlier-aware QuantEase (Sec. 5, Algorithm "Outlier-Aware QuantEase").
+ * Per iteration: one CD sweep on What with H fixed (linear term from
+ * W - H, residual E = (What + H - W) Sigma), then one iterative-hard-
+ * thresholding step  H <- P_s(H - eta grad_H g),  grad_H g = 2E,
+ * eta = 1 / (2 lambda_max), i.e. V = H - E / lambda_max (fp32); P_s keeps
+ * the s entries of largest |V| (ties: lower linear index i*p + j; zeros are
+ * never kept); then E += (H_new - H_old) Sigma.
+ *
+ * H:        q x p dense, device, in/out.
+ * E:        q x p, device, in/out (the residual).
+ * support:  device int64 array of capacity s, in/out: ascending linear
+ *           indices of H's nonzeros.  support_nnz: device int64, in/out.
+ * s:        outlier budget, 0 <= s <= q*p.  lambda_max > 0 (qe_lambda_max).
+ * flags:    QE_INIT_FROM_W: What = W - H (H and support as given, e.g. from
+ *           qe_topk_abs on W, Sec. 5.3 initialisation), E = 0.
+ *           QE_R_VALID: E already valid.  QE_CODES_VALID as above.
+ *           Without QE_INIT_FROM_W / QE_R_VALID, E = (What + H - W) Sigma.
+ * obj:      NULL or device array of 2*sweeps doubles: obj[2k] = g after the
+ *           CD sweep of iteration k, obj[2k+1] = g after its IHT step.
+ * scale/zero: the outlier-aware grid (qe_grid_minmax with H excluded).
+ * ------------------------------------------------------------------------ */
+size_t qe_outlier_workspace_size(int64_t q, int64_t p, int block, int64_t s);
+qe_status qe_cd_outlier_sweep(const float* W, const float* Sigma, int64_t q, int64_t p,
+                              int bits, const float* scale, const float* zero, float* W_hat,
+                              uint8_t* codes, float* H, float* E, int64_t s, float lambda_max,
+                              int64_t* support, int64_t* support_nnz, int sweeps, int block,
+                              uint32_t flags, double* obj, void* ws, size_t ws_bytes,
+                              void* stream);
+
+/* ------------------------------------------------------------------------
+ * P_s of Sec. 5.3 on a dense array: keep the s entries largest in absolute
+ * value (ties: lower index first; exact zeros never kept).
+ * V: `count` floats, device.  out: `count` floats, device: P_s(V).
+ * support: device int64[s]: kept indices, ascending.  nnz: device int64.
+ * ------------------------------------------------------------------------ */
+size_t qe_topk_workspace_size(int64_t count, int64_t s);
+qe_status qe_topk_abs(const float* V, int64_t count, int64_t s, float* out, int64_t* support,
+                      int64_t* nnz, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Exact objective and its normaliser (Sec. 3 problem (1); Sec. 4.4 relative
+ * calibration error), recomputed from scratch, independent of R:
+ *   out[0] = <D, D Sigma> = ||(What + H - W) X||_F^2,  D = What + H - W,
+ *   out[1] = <W, W Sigma> = ||W X||_F^2.
+ * H may be NULL.  out: device, 2 doubles.
+ * ------------------------------------------------------------------------ */
+size_t qe_objective_workspace_size(int64_t q, int64_t p);
+qe_status qe_objective(const float* W, const float* W_hat, const float* H, const float* Sigma,
+                       int64_t q, int64_t p, double* out, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/* ------------------------------------------------------------------------
+ * lambda_max(Sigma) by the power method (Sec. 5.3: matrix-vector products
+ * only, O(p^2) per iteration).  Start vector 1/sqrt(p); the estimate is the
+ * Rayleigh quotient; stops when it changes by less than tol (relative)
+ * between checks, or after max_iters iterations.  Synchronises `stream`.
+ * lambda_out: HOST float.
+ * ------------------------------------------------------------------------ */
+size_t qe_lambda_workspace_size(int64_t p);
+qe_status qe_lambda_max(const float* Sigma, int64_t p, int max_iters, float tol,
+                        float* lambda_out, void* ws, size_t ws_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QE_H */

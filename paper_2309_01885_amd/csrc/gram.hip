@@ -1,0 +1,205 @@
+// Gram matrix Sigma = X X^T on fp32 matrix cores (gfx950).
+//
+// Lemma 1 (Sec. 4.2) needs X only through Sigma, a p x p statistic whose size
+// does not grow with the token count n.  Work split: 128 x 128 tiles of the
+// upper triangle (ti <= tj) x token splits.  Inside a workgroup the products
+// of `kInnerChunks` K-chunks are summed in the matrix-core accumulators, then
+// added into a second fp32 accumulator, which keeps each running sum short
+// (~512 terms) at n = 262144.  With several splits, partial tiles go to the
+// workspace and a finalize kernel adds them in a fixed order in fp64.  The
+// lower triangle is written as an exact mirror through an LDS transpose.
+#include "qe_internal.h"
+
+namespace qe {
+
+constexpr int kInnerChunks = 16;          // 16 x 32 = 512 tokens per inner sum
+constexpr int kTileFloats = kTile * kTile;
+constexpr int kTStride = kTile + 1;       // LDS transpose tile row stride
+
+__device__ inline void tri_index(int64_t t, int64_t nt, int64_t& ti, int64_t& tj)
+{
+    // row ti of the upper triangle starts at ti * nt - ti * (ti - 1) / 2
+    const double b = 2.0 * nt + 1.0;
+    int64_t r = (int64_t)((b - sqrt(b * b - 8.0 * (double)t)) * 0.5);
+    if (r < 0) r = 0;
+    auto start = [nt](int64_t i) { return i * nt - i * (i - 1) / 2; };
+    while (r > 0 && start(r) > t) --r;
+    while (r + 1 < nt && start(r + 1) <= t) ++r;
+    ti = r;
+    tj = r + (t - start(r));
+}
+
+// Writes the 128 x 128 tile held in LDS (row stride kTStride) to Sigma's
+// upper block (ti, tj) and its mirror (tj, ti).  On a diagonal tile only the
+// entries with row <= col are taken and the rest mirrored, so Sigma is
+// exactly symmetric.  With `accumulate`, the old upper value is added first.
+__device__ void write_symmetric(float* tileLds, int64_t ti, int64_t tj, float* Sigma, int64_t p,
+                                int accumulate)
+{
+    const int64_t a0 = ti * kTile, b0 = tj * kTile;
+    const bool diag = ti == tj;
+    for (int e = threadIdx.x; e < kTileFloats; e += blockDim.x) {
+        const int r = e / kTile, c = e % kTile;
+        const int64_t a = a0 + r, b = b0 + c;
+        if (a < p && b < p && (!diag || r <= c)) {
+            float v = tileLds[r * kTStride + c];
+            if (accumulate) v += Sigma[a * p + b];
+            Sigma[a * p + b] = v;
+            tileLds[r * kTStride + c] = v;
+        }
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < kTileFloats; e += blockDim.x) {
+        const int c = e / kTile, r = e % kTile;      // consecutive threads: consecutive a
+        const int64_t a = a0 + r, b = b0 + c;
+        if (a < p && b < p && (!diag || r < c)) Sigma[b * p + a] = tileLds[r * kTStride + c];
+    }
+}
+
+template <bool TRANS>
+__global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ X, int64_t p,
+                                                   int64_t n, int64_t nt, int64_t split_len,
+                                                   float* __restrict__ out, int direct,
+                                                   int accumulate, int x_vec4, const int* status)
+{
+    if (failed(status)) return;
+    __shared__ __attribute__((aligned(16))) float lds[kNTLdsFloats];
+    int64_t ti, tj;
+    tri_index(blockIdx.x, nt, ti, tj);
+    const int64_t k0 = (int64_t)blockIdx.y * split_len;
+    const int64_t k1 = min(n, k0 + split_len);
+
+    f32x16 acc[2][2], outer[2][2];
+    zero_acc(outer);
+    const int64_t inner = (int64_t)kInnerChunks * kKC;
+    for (int64_t kb = k0; kb < k1; kb += inner) {
+        const int64_t ke = min(k1, kb + inner);
+        zero_acc(acc);
+        if (TRANS) {
+            // X is n x p: element (channel r, token k) at X[k * p + r]
+            const ColOp op{X + kb * p, p, p, ke - kb, x_vec4 != 0};
+            nt_tile(op, ti * kTile, op, tj * kTile, ke - kb, lds, acc);
+        } else {
+            const RowOp op{X + kb, n, p, ke - kb, x_vec4 != 0};
+            nt_tile(op, ti * kTile, op, tj * kTile, ke - kb, lds, acc);
+        }
+#pragma unroll
+        for (int a = 0; a < 2; ++a)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) outer[a][b] += acc[a][b];
+    }
+
+    if (direct) {
+        float* tl = lds;   // reuse the pipeline LDS (nt_tile ended with a barrier)
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    tl[acc_row(mi, v) * kTStride + acc_col(ni)] = outer[mi][ni][v];
+        __syncthreads();
+        write_symmetric(tl, ti, tj, out, p, accumulate);
+    } else {
+        float* dst = out + ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * kTileFloats;
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    dst[acc_row(mi, v) * kTile + acc_col(ni)] = outer[mi][ni][v];
+    }
+}
+
+// Adds the split partial tiles in fixed split order (fp64) and writes Sigma.
+__global__ __launch_bounds__(256) void gram_finalize_kernel(const float* __restrict__ parts,
+                                                            int64_t ntiles, int splits,
+                                                            int64_t nt, float* Sigma, int64_t p,
+                                                            int accumulate, const int* status)
+{
+    if (failed(status)) return;
+    __shared__ float tl[kTile * kTStride];
+    int64_t ti, tj;
+    tri_index(blockIdx.x, nt, ti, tj);
+    for (int e = threadIdx.x; e < kTileFloats; e += blockDim.x) {
+        double s = 0.0;
+        for (int sp = 0; sp < splits; ++sp)
+            s += (double)parts[((int64_t)sp * ntiles + blockIdx.x) * kTileFloats + e];
+        tl[(e / kTile) * kTStride + (e % kTile)] = (float)s;
+    }
+    __syncthreads();
+    write_symmetric(tl, ti, tj, Sigma, p, accumulate);
+}
+
+// Sigma_jj += damp * mean_j(Sigma_jj): one workgroup, fp64 mean.
+__global__ __launch_bounds__(256) void damp_kernel(float* Sigma, int64_t p, float damp,
+                                                   const int* status)
+{
+    if (failed(status)) return;
+    __shared__ double sh[256];
+    double s = 0.0;
+    for (int64_t j = threadIdx.x; j < p; j += blockDim.x) s += (double)Sigma[j * p + j];
+    const double total = block_sum_f64(s, sh);
+    const float add = (float)((double)damp * (total / (double)p));
+    for (int64_t j = threadIdx.x; j < p; j += blockDim.x) Sigma[j * p + j] += add;
+}
+
+static int gram_splits(int64_t p, int64_t n)
+{
+    const int64_t nt = cdiv(p, kTile);
+    const int64_t tiles = nt * (nt + 1) / 2;
+    int64_t s = cdiv(1024, tiles);
+    const int64_t max_by_n = cdiv(n, (int64_t)kInnerChunks * kKC);
+    if (s > max_by_n) s = max_by_n;
+    if (s > 32) s = 32;
+    if (s < 1) s = 1;
+    return (int)s;
+}
+
+size_t gram_ws_bytes(int64_t p, int64_t n)
+{
+    const int64_t nt = cdiv(p, kTile);
+    const int64_t tiles = nt * (nt + 1) / 2;
+    const int splits = gram_splits(p, n);
+    size_t b = kStatusBytes;
+    if (splits > 1) b += align256((size_t)splits * tiles * kTileFloats * sizeof(float));
+    return b;
+}
+
+qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma,
+                      int accumulate, float damp, void* ws, hipStream_t s)
+{
+    int* status = static_cast<int*>(ws);
+    const int64_t nt = cdiv(p, kTile);
+    const int64_t tiles = nt * (nt + 1) / 2;
+    const int splits = gram_splits(p, n);
+    // split length: a multiple of the inner sum length
+    const int64_t inner = (int64_t)kInnerChunks * kKC;
+    const int64_t split_len = cdiv(cdiv(n, splits), inner) * inner;
+    const int used_splits = (int)cdiv(n, split_len);
+    dim3 grid((unsigned)tiles, (unsigned)used_splits);
+    const bool direct = used_splits == 1;
+    float* parts = direct ? Sigma : reinterpret_cast<float*>(static_cast<char*>(ws) + kStatusBytes);
+    // 16-byte loads need an aligned base and a row stride that keeps them aligned
+    const int x_vec4 = aligned16(X) && ((layout == QE_LAYOUT_PN ? n : p) % 4 == 0);
+    if (layout == QE_LAYOUT_PN)
+        hipLaunchKernelGGL(gram_kernel<false>, grid, dim3(256), 0, s, X, p, n, nt, split_len,
+                           parts, direct ? 1 : 0, accumulate, x_vec4, status);
+    else
+        hipLaunchKernelGGL(gram_kernel<true>, grid, dim3(256), 0, s, X, p, n, nt, split_len,
+                           parts, direct ? 1 : 0, accumulate, x_vec4, status);
+    if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+    if (!direct) {
+        hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)tiles), dim3(256), 0, s, parts,
+                           tiles, used_splits, nt, Sigma, p, accumulate, status);
+        if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+    }
+    if (damp > 0.f) {
+        hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, Sigma, p, damp, status);
+        if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+    }
+    return QE_OK;
+}
+
+}  // namespace qe

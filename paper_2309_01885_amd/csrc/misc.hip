@@ -1,0 +1,214 @@
+// Grid, exact objective and lambda_max kernels (gfx950).
+#include "qe_internal.h"
+
+namespace qe {
+
+// ---------------------------------------------------------------- grid
+// Per-row asymmetric min/max grid (Sec. 3: uniformly spaced levels per output
+// channel; the paper does not print the formula, see qe.h): one workgroup per
+// row, min/max reductions (exact in any order), then the scale and zero point
+// in fp32.  Entries with H != 0 are excluded (outlier-aware grid, Sec. 5.3).
+__global__ __launch_bounds__(256) void grid_minmax_kernel(const float* __restrict__ W,
+                                                          const float* __restrict__ H, int64_t p,
+                                                          float maxq, float* scale, float* zero)
+{
+    __shared__ float slo[256], shi[256];
+    const int64_t i = blockIdx.x;
+    float lo = 0.f, hi = 0.f;
+    for (int64_t j = threadIdx.x; j < p; j += blockDim.x) {
+        if (H && H[i * p + j] != 0.f) continue;
+        const float w = W[i * p + j];
+        lo = fminf(lo, w);
+        hi = fmaxf(hi, w);
+    }
+    slo[threadIdx.x] = lo;
+    shi[threadIdx.x] = hi;
+    __syncthreads();
+    for (int s = 128; s > 0; s >>= 1) {
+        if ((int)threadIdx.x < s) {
+            slo[threadIdx.x] = fminf(slo[threadIdx.x], slo[threadIdx.x + s]);
+            shi[threadIdx.x] = fmaxf(shi[threadIdx.x], shi[threadIdx.x + s]);
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        lo = slo[0];
+        hi = shi[0];
+        if (lo == 0.f && hi == 0.f) {
+            lo = -1.f;
+            hi = 1.f;
+        }
+        const float s = (hi - lo) / maxq;
+        scale[i] = s;
+        zero[i] = rintf(-lo / s);
+    }
+}
+
+qe_status launch_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, int bits,
+                             float* scale, float* zero, hipStream_t s)
+{
+    if (q == 0) return QE_OK;
+    hipLaunchKernelGGL(grid_minmax_kernel, dim3((unsigned)q), dim3(256), 0, s, W, H, p,
+                       (float)((1 << bits) - 1), scale, zero);
+    return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+// ---------------------------------------------------------------- exact objective
+// <A, A Sigma> for A = P1 + P2 - P3 (P2, P3 nullable), fused: each 128 x 128
+// tile of A Sigma is formed on matrix cores and immediately dotted with the
+// matching tile of A in fp64; per-tile partials are summed in a fixed order.
+__global__ __launch_bounds__(256) void quad_form_kernel(const float* p1, const float* p2,
+                                                        const float* p3, const float* Sigma,
+                                                        int64_t q, int64_t p, double* partial,
+                                                        int vec4, const int* status)
+{
+    if (failed(status)) return;
+    __shared__ __attribute__((aligned(16))) float lds[kNTLdsFloats];
+    __shared__ double sh[256];
+    const int64_t tn_count = cdiv(p, kTile);
+    const int64_t row0 = (blockIdx.x / tn_count) * kTile, col0 = (blockIdx.x % tn_count) * kTile;
+    f32x16 acc[2][2];
+    zero_acc(acc);
+    const CompOp A{p1, p2, p3, p, q, p, vec4 != 0};
+    const RowOp B{Sigma, p, p, p, vec4 != 0};
+    nt_tile(A, row0, B, col0, p, lds, acc);
+    double d = 0.0;
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t r = row0 + acc_row(mi, v), c = col0 + acc_col(ni);
+                if (r < q && c < p) {
+                    const int64_t e = r * p + c;
+                    float a = p2 ? p1[e] + p2[e] : p1[e];
+                    if (p3) a = a - p3[e];
+                    d += (double)a * (double)acc[mi][ni][v];
+                }
+            }
+    const double s = block_sum_f64(d, sh);
+    if (threadIdx.x == 0) partial[blockIdx.x] = s;
+}
+
+__global__ __launch_bounds__(256) void sum_tiles_kernel(const double* partial, int64_t n,
+                                                        double* out, const int* status)
+{
+    if (failed(status)) return;
+    __shared__ double sh[256];
+    double acc = 0.0;
+    for (int64_t e = threadIdx.x; e < n; e += blockDim.x) acc += partial[e];
+    const double s = block_sum_f64(acc, sh);
+    if (threadIdx.x == 0) *out = s;
+}
+
+size_t objective_ws_bytes(int64_t q, int64_t p)
+{
+    const int64_t tiles = cdiv(q, kTile) * cdiv(p, kTile);
+    return kStatusBytes + 2 * align256(sizeof(double) * tiles);
+}
+
+qe_status launch_objective(const float* W, const float* Wh, const float* H, const float* Sigma,
+                           int64_t q, int64_t p, double* out, void* ws, hipStream_t s)
+{
+    int* status = static_cast<int*>(ws);
+    Ws w(ws);
+    const int64_t tiles = cdiv(q, kTile) * cdiv(p, kTile);
+    double* part0 = w.take<double>(tiles);
+    double* part1 = w.take<double>(tiles);
+    const bool vec4 = aligned16(W) && aligned16(Wh) && aligned16(Sigma) && (!H || aligned16(H)) &&
+                      p % 4 == 0;
+    // D = What + H - W
+    hipLaunchKernelGGL(quad_form_kernel, dim3((unsigned)tiles), dim3(256), 0, s, Wh, H, W, Sigma,
+                       q, p, part0, vec4 ? 1 : 0, status);
+    hipLaunchKernelGGL(sum_tiles_kernel, dim3(1), dim3(256), 0, s, part0, tiles, out, status);
+    // W itself
+    hipLaunchKernelGGL(quad_form_kernel, dim3((unsigned)tiles), dim3(256), 0, s, W,
+                       (const float*)nullptr, (const float*)nullptr, Sigma, q, p, part1,
+                       vec4 ? 1 : 0, status);
+    hipLaunchKernelGGL(sum_tiles_kernel, dim3(1), dim3(256), 0, s, part1, tiles, out + 1, status);
+    return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+// ---------------------------------------------------------------- lambda_max
+// Power method (Sec. 5.3): y = Sigma v (one wavefront per row), then
+// v <- y / ||y||, lambda = v^T Sigma v (Rayleigh quotient of the unit v).
+__global__ __launch_bounds__(256) void fill_kernel(float* v, int64_t n, float val)
+{
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e < n) v[e] = val;
+}
+
+__global__ __launch_bounds__(256) void symv_kernel(const float* __restrict__ Sigma, int64_t p,
+                                                   const float* __restrict__ v, float* y)
+{
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= p) return;
+    const float* srow = Sigma + row * p;
+    double acc = 0.0;
+    for (int64_t j = lane; j < p; j += 64) acc += (double)srow[j] * (double)v[j];
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+    if (lane == 0) y[row] = (float)acc;
+}
+
+__global__ __launch_bounds__(256) void power_normalize_kernel(const float* y, const float* v,
+                                                              int64_t p, float* vout,
+                                                              double* lam_hist, int it)
+{
+    __shared__ double sh[256];
+    double yy = 0.0, vy = 0.0;
+    for (int64_t j = threadIdx.x; j < p; j += blockDim.x) {
+        yy += (double)y[j] * (double)y[j];
+        vy += (double)v[j] * (double)y[j];
+    }
+    const double nrm2 = block_sum_f64(yy, sh);
+    const double rq = block_sum_f64(vy, sh);
+    const double inv = nrm2 > 0.0 ? 1.0 / sqrt(nrm2) : 0.0;
+    for (int64_t j = threadIdx.x; j < p; j += blockDim.x) vout[j] = (float)((double)y[j] * inv);
+    if (threadIdx.x == 0) lam_hist[it] = rq;
+}
+
+constexpr int kLambdaCheck = 8;
+
+size_t lambda_ws_bytes(int64_t p)
+{
+    return kStatusBytes + 3 * align256(sizeof(float) * p) + align256(sizeof(double) * kLambdaCheck);
+}
+
+qe_status launch_lambda(const float* Sigma, int64_t p, int max_iters, float tol, float* out,
+                        void* ws, hipStream_t s)
+{
+    Ws w(ws);
+    float* v = w.take<float>(p);
+    float* y = w.take<float>(p);
+    float* v2 = w.take<float>(p);
+    double* hist = w.take<double>(kLambdaCheck);
+    hipLaunchKernelGGL(fill_kernel, dim3((unsigned)cdiv(p, 256)), dim3(256), 0, s, v, p,
+                       (float)(1.0 / sqrt((double)p)));
+    double last = 0.0, prev = 0.0;
+    int it = 0;
+    while (it < max_iters) {
+        const int batch = std::min(kLambdaCheck, max_iters - it);
+        for (int b = 0; b < batch; ++b) {
+            hipLaunchKernelGGL(symv_kernel, dim3((unsigned)cdiv(p, 4)), dim3(256), 0, s, Sigma, p,
+                               v, y);
+            hipLaunchKernelGGL(power_normalize_kernel, dim3(1), dim3(256), 0, s, y, v, p, v2, hist,
+                               b);
+            std::swap(v, v2);
+        }
+        it += batch;
+        if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+        double h[kLambdaCheck];
+        if (hipMemcpyAsync(h, hist, sizeof(double) * batch, hipMemcpyDeviceToHost, s) != hipSuccess)
+            return QE_ERR_HIP;
+        if (hipStreamSynchronize(s) != hipSuccess) return QE_ERR_HIP;
+        prev = batch > 1 ? h[batch - 2] : last;
+        last = h[batch - 1];
+        if (last > 0.0 && fabs(last - prev) <= (double)tol * last) break;
+    }
+    *out = (float)last;
+    return QE_OK;
+}
+
+}  // namespace qe

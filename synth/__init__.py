@@ -104,7 +104,8 @@ def outlier_channels(spec: LayerSpec, p: Optional[int] = None) -> np.ndarray:
     if spec.x_out_count <= 0:
         return np.zeros(0, np.int64)
     cfg = spec.cfg if spec.x_cfg is None else spec.x_cfg
-    return np.sort(rng(cfg, 2).choice(p, size=spec.x_out_count, replace=False)).astype(np.int64)
+    count = min(spec.x_out_count, p)
+    return np.sort(rng(cfg, 2).choice(p, size=count, replace=False)).astype(np.int64)
 
 
 def activation_chunk(spec: LayerSpec, chunk: int, p: Optional[int] = None,

@@ -17,3 +17,13 @@ def pytest_configure(config):
 def oracle():
     import oracle as _oracle
     return _oracle
+
+
+@pytest.fixture(scope="session")
+def qe():
+    """The HIP library binding; GPU tests fail (not skip) if it cannot run."""
+    import torch
+    assert torch.cuda.is_available(), "GPU test run without a visible GPU"
+    import paper_2309_01885_amd as P
+    P.load()
+    return P

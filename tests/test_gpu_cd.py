@@ -1,0 +1,235 @@
+"""GPU parity of qe_cd_sweep (Sec. 4: Lemma 1, the rank-1 identity, blocked)
+against the fp64 oracle, on the same seeded fp32 inputs.
+
+Bar (per sweep): objective within 1e-4 relative; at most 0.1% of codes
+differ, and in every row the first differing code is a near tie (the
+oracle's t lies within 1e-4 grid units of a rounding boundary: before that
+point both rows hold identical codes, so only rounding separates the two
+t values).  Exact cases (weights on the grid, diagonal Sigma, constructed
+ties) must match bit for bit."""
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from parity import dev, first_divergence, host
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+OBJ_RTOL = 1e-4
+CODE_FRAC = 1e-3
+TIE_MARGIN = 1e-4
+
+
+def gpu_cd(qe, W, S32, bits, scale, zero, sweeps, block=0, per_sweep=True, W0=None, codes0=None):
+    q, p = W.shape
+    Wd, Sd = dev(W), dev(S32)
+    sc, ze = dev(scale), dev(zero)
+    Wh = torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    R = torch.empty_like(Wd)
+    flags = qe.QE_INIT_FROM_W
+    if W0 is not None:
+        Wh.copy_(dev(W0))
+        flags = 0
+        if codes0 is not None:
+            codes.copy_(dev(codes0.astype(np.uint8)))
+            flags = qe.QE_CODES_VALID
+    hist, objs = [], []
+    if per_sweep:
+        for k in range(sweeps):
+            obj = torch.zeros(1, dtype=torch.float64, device="cuda")
+            qe.cd_sweep(Wd, Sd, bits, sc, ze, Wh, codes, R, 1, block=block, flags=flags, obj=obj)
+            flags = qe.QE_R_VALID | qe.QE_CODES_VALID
+            hist.append(host(codes).astype(np.int32))
+            objs.append(float(host(obj)[0]))
+    else:
+        obj = torch.zeros(sweeps, dtype=torch.float64, device="cuda")
+        qe.cd_sweep(Wd, Sd, bits, sc, ze, Wh, codes, R, sweeps, block=block, flags=flags, obj=obj)
+        objs = list(host(obj))
+        hist.append(host(codes).astype(np.int32))
+    return dict(What=host(Wh), codes=host(codes).astype(np.int32), R=host(R), hist=hist,
+                obj=objs)
+
+
+def layer(q, p, n, seed, corr=0.0, bits=4, damp=0.01, spec="c1"):
+    if corr > 0:
+        X = synth.correlated_activations(p, n, corr, seed, out_channels=max(1, p // 50),
+                                         out_mult=20.0)
+        W = synth.gaussian((q, p), seed=seed, std=0.02)
+    else:
+        sp = synth.CONFIGS[spec]
+        X = synth.activations(sp, n=n, p=p)
+        W = synth.weights(sp, q=q, p=p)
+    return W, X
+
+
+def check_parity(oracle, W, S32, bits, scale, zero, g, sweeps):
+    ref = oracle.cd(W, S32.astype(np.float64), bits, scale, zero, sweeps)
+    q, p = W.shape
+    for k in range(sweeps):
+        assert g["obj"][k] == pytest.approx(ref.obj[k], rel=OBJ_RTOL), f"objective, sweep {k + 1}"
+        frac = np.mean(g["hist"][k] != ref.codes_hist[k])
+        assert frac <= CODE_FRAC, f"sweep {k + 1}: {frac:.2e} of codes differ"
+    fd = first_divergence(g["hist"], ref.codes_hist)
+    for i, d in enumerate(fd):
+        if d is None:
+            continue
+        k, j = d
+        assert ref.margin_hist[k][i, j] <= TIE_MARGIN, \
+            f"row {i}: first divergence at sweep {k + 1}, column {j} is not a near tie " \
+            f"(margin {ref.margin_hist[k][i, j]:.3e})"
+    return ref
+
+
+@pytest.mark.parametrize("q,p,corr,bits", [
+    (512, 512, 0.0, 4),       # the small single-layer workload
+    (512, 512, 0.9, 4),       # correlated channels: CD really moves
+    (77, 200, 0.9, 3),        # ragged rows and a ragged last block
+    (130, 301, 0.5, 2),
+    (1, 33, 0.9, 4),
+])
+def test_cd_matches_oracle(qe, oracle, q, p, corr, bits):
+    W, X = layer(q, p, 2048, 11, corr=corr, bits=bits)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, bits)
+    sweeps = 5
+    g = gpu_cd(qe, W, S32, bits, scale, zero, sweeps)
+    check_parity(oracle, W, S32, bits, scale, zero, g, sweeps)
+
+
+@pytest.mark.parametrize("block", [16, 32, 64, 128])
+def test_block_width_invariance(qe, oracle, block):
+    W, X = layer(96, 250, 1024, 12, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    g = gpu_cd(qe, W, S32, 4, scale, zero, 4, block=block)
+    check_parity(oracle, W, S32, 4, scale, zero, g, 4)
+
+
+def test_multi_sweep_call_equals_resumed_calls(qe, oracle):
+    W, X = layer(200, 260, 1024, 13, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 3)
+    a = gpu_cd(qe, W, S32, 3, scale, zero, 4, per_sweep=True)
+    b = gpu_cd(qe, W, S32, 3, scale, zero, 4, per_sweep=False)
+    assert np.array_equal(a["What"], b["What"])
+    assert np.array_equal(a["codes"], b["codes"])
+    assert np.array_equal(a["R"], b["R"])
+    assert a["obj"] == b["obj"]
+
+
+def test_deterministic(qe, oracle):
+    W, X = layer(256, 384, 1024, 14, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    a = gpu_cd(qe, W, S32, 4, scale, zero, 3, per_sweep=False)
+    b = gpu_cd(qe, W, S32, 4, scale, zero, 3, per_sweep=False)
+    assert np.array_equal(a["What"], b["What"]) and np.array_equal(a["R"], b["R"])
+
+
+def test_residual_is_exact_after_sweeps(qe, oracle):
+    W, X = layer(150, 270, 1024, 15, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    g = gpu_cd(qe, W, S32, 4, scale, zero, 3)
+    R_ref = (g["What"].astype(np.float64) - W) @ S32.astype(np.float64)
+    scale_R = np.abs(g["What"].astype(np.float64) - W) @ np.abs(S32.astype(np.float64))
+    assert np.all(np.abs(g["R"] - R_ref) <= 1e-5 * scale_R + 1e-30)
+
+
+def test_on_grid_weights_bitwise(qe, oracle):
+    q, p = 100, 230
+    k = synth.integers((q, p), seed=20, lo=0, hi=16)
+    scale = np.full(q, 2.0 ** -6, np.float32)
+    zero = synth.integers((q,), seed=21, lo=0, hi=16).astype(np.float32)
+    W = (scale[:, None] * (k - zero[:, None])).astype(np.float32)
+    X = synth.correlated_activations(p, 512, 0.9, 22)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    g = gpu_cd(qe, W, S32, 4, scale, zero, 3)
+    assert np.array_equal(g["codes"], k)
+    assert np.array_equal(g["What"], W)
+    assert not np.any(g["R"])
+    assert all(o == 0.0 for o in g["obj"])
+
+
+def test_diagonal_sigma_is_round_to_nearest(qe, oracle):
+    q, p = 64, 300
+    W = synth.gaussian((q, p), seed=23, std=0.03)
+    d = synth.uniform((p,), seed=24, lo=0.5, hi=3.0)
+    S32 = np.diag(d).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 3)
+    g = gpu_cd(qe, W, S32, 3, scale, zero, 3)
+    ref = oracle.cd(W, S32, 3, scale, zero, 3)
+    for k in range(3):
+        assert np.array_equal(g["hist"][k], ref.codes_hist[k])
+
+
+def test_tie_rule_fixture(qe, oracle):
+    gd = json.load(open(os.path.join(GOLDEN, "cd_tie_rule.json")))
+    W = np.array(gd["W"], np.float32)
+    S32 = np.array(gd["Sigma"], np.float32)
+    sc = np.array(gd["scale"], np.float32)
+    ze = np.array(gd["zero"], np.float32)
+    for case in gd["cases"]:
+        if case["codes0"] is None:
+            g = gpu_cd(qe, W, S32, gd["bits"], sc, ze, 1)
+        else:
+            c0 = np.array(case["codes0"], np.int32)
+            W0 = oracle.dequant(c0, sc, ze).astype(np.float32)
+            g = gpu_cd(qe, W, S32, gd["bits"], sc, ze, 1, W0=W0, codes0=c0)
+        assert np.array_equal(g["codes"], case["expect"]), case
+
+
+def test_hand_fixture(qe):
+    gd = json.load(open(os.path.join(GOLDEN, "cd_two_by_two.json")))
+    W = np.array(gd["W"], np.float32)
+    S32 = np.array(gd["Sigma"], np.float32)
+    g = gpu_cd(qe, W, S32, gd["bits"], np.array(gd["scale"], np.float32),
+               np.array(gd["zero"], np.float32), gd["sweeps"])
+    for k in range(gd["sweeps"]):
+        assert np.array_equal(g["hist"][k], gd["codes_after_sweep"][k])
+        assert g["obj"][k] == gd["f_after_sweep"][k]
+
+
+def test_warm_start_from_arbitrary_what(qe, oracle):
+    # Sec. 4.1: CD may start from any What (e.g. another quantizer's output)
+    W, X = layer(120, 200, 1024, 25, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    codes0 = np.clip(np.rint(W / scale[:, None] + zero[:, None]), 0, 15).astype(np.int32)
+    W0 = oracle.dequant(codes0, scale, zero).astype(np.float32)
+    g = gpu_cd(qe, W, S32, 4, scale, zero, 3, W0=W0, codes0=codes0)
+    ref = oracle.cd(W, S32.astype(np.float64), 4, scale, zero, 3, W0=W0, codes0=codes0,
+                    codes_valid=True)
+    for k in range(3):
+        assert g["obj"][k] == pytest.approx(ref.obj[k], rel=OBJ_RTOL)
+        assert np.mean(g["hist"][k] != ref.codes_hist[k]) <= CODE_FRAC
+
+
+def test_zero_diagonal_reports_error(qe):
+    q, p = 8, 40
+    W = synth.gaussian((q, p), seed=26)
+    S = np.eye(p, dtype=np.float32)
+    S[7, 7] = 0.0
+    with pytest.raises(qe.QEError) as e:
+        gpu_cd(qe, W, S, 4, np.ones(q, np.float32), np.zeros(q, np.float32), 1)
+    assert e.value.code == 2
+
+
+def test_objective_entry_point(qe, oracle):
+    W, X = layer(140, 260, 1024, 27, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    g = gpu_cd(qe, W, S32, 4, scale, zero, 2)
+    H = np.zeros_like(W)
+    H.reshape(-1)[::97] = 0.01
+    out = host(qe.objective(dev(W), dev(g["What"]), dev(S32), dev(H)))
+    assert out[0] == pytest.approx(oracle.objective(W, g["What"], S32, H), rel=1e-5)
+    assert out[1] == pytest.approx(oracle.objective(np.zeros_like(W), W, S32), rel=1e-5)
+    out0 = host(qe.objective(dev(W), dev(g["What"]), dev(S32)))
+    assert out0[0] == pytest.approx(g["obj"][-1], rel=1e-4)

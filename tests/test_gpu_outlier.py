@@ -1,0 +1,105 @@
+"""GPU parity of the outlier-aware path (Sec. 5): P_s, lambda_max and the
+full CD + IHT iteration, against the fp64 oracle.
+
+P_s on the same fp32 V is an integer decision taken in the same precision by
+both sides, so the support must be identical, ties and zeros included.
+End to end, E is fp32 on the GPU and fp64 in the oracle; the supports must
+still be identical on these seeds, and g must agree within 1e-4."""
+import numpy as np
+import pytest
+import torch
+
+import synth
+from parity import dev, host
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("shape,s", [((512, 512), 2621), ((77, 301), 100), ((10, 10), 0),
+                                     ((10, 10), 100), ((33, 7), 5), ((4096, 64), 20000)])
+def test_topk_identical_support(qe, oracle, shape, s):
+    V = synth.gaussian(shape, seed=1)
+    V.reshape(-1)[::13] = 0.25          # exact ties in |v|
+    V.reshape(-1)[7::29] = -0.25
+    V.reshape(-1)[3::11] = 0.0          # exact zeros
+    out, sup, nnz = qe.topk_abs(dev(V), s)
+    n = int(host(nnz)[0])
+    ref_sup, ref_dense = oracle.topk_abs(V, s)
+    assert n == len(ref_sup)
+    assert np.array_equal(host(sup)[:n], ref_sup)
+    assert np.array_equal(host(out), ref_dense)
+
+
+def test_lambda_max(qe, oracle):
+    X = synth.correlated_activations(300, 2000, 0.9, 3, out_channels=6, out_mult=20.0)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    lam = qe.lambda_max(dev(S.astype(np.float32)))
+    assert lam == pytest.approx(oracle.lambda_max(S), rel=1e-5)
+
+
+def run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0, block=0):
+    q, p = W.shape
+    Wd, Sd = dev(W), dev(S32)
+    Wh = torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    H = H0.clone()
+    E = torch.empty_like(Wd)
+    sup = sup0.clone()
+    nnz = n0.clone()
+    obj = torch.zeros(2 * sweeps, dtype=torch.float64, device="cuda")
+    qe.cd_outlier_sweep(Wd, Sd, bits, dev(scale), dev(zero), Wh, codes, H, E, s, lam, sup, nnz,
+                        sweeps, block=block, flags=qe.QE_INIT_FROM_W, obj=obj)
+    n = int(host(nnz)[0])
+    return dict(What=host(Wh), codes=host(codes).astype(np.int32), H=host(H), E=host(E),
+                support=host(sup)[:n], obj=host(obj))
+
+
+@pytest.mark.parametrize("q,p,bits,frac,corr", [(512, 512, 3, 0.01, 0.9), (96, 200, 3, 0.02, 0.5),
+                                                 (130, 257, 2, 0.005, 0.9)])
+def test_outlier_matches_oracle(qe, oracle, q, p, bits, frac, corr):
+    W = synth.gaussian((q, p), seed=5, std=0.02)
+    W.reshape(-1)[::487] *= 10.0
+    X = synth.correlated_activations(p, 2048, corr, 6, out_channels=max(1, p // 100),
+                                     out_mult=30.0)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    S32 = S.astype(np.float32)
+    s = int(frac * q * p)
+    lam = float(np.float32(oracle.lambda_max(S32)))
+    # initial outliers H = P_s(W) and the outlier-aware grid, both on the GPU
+    H0, sup0, n0 = qe.topk_abs(dev(W), s)
+    scale_d, zero_d = qe.grid_minmax(dev(W), bits, H0)
+    ref_sup0, ref_H0 = oracle.topk_abs(W, s)
+    assert np.array_equal(host(sup0)[:int(host(n0)[0])], ref_sup0)
+    scale, zero = oracle.grid_minmax(W, bits, ref_H0)
+    assert np.array_equal(host(scale_d), scale) and np.array_equal(host(zero_d), zero)
+
+    sweeps = 4
+    g = run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0)
+    ref = oracle.outlier(W, S32, bits, scale, zero, s, lam, sweeps)
+    for k in range(sweeps):
+        assert g["obj"][2 * k] == pytest.approx(ref.g_cd[k], rel=1e-4), f"g after CD, it {k + 1}"
+        assert g["obj"][2 * k + 1] == pytest.approx(ref.g[k], rel=1e-4), f"g after IHT, it {k + 1}"
+        assert g["obj"][2 * k + 1] <= g["obj"][2 * k] * (1 + 1e-6)       # Lemma 3
+    assert np.array_equal(g["support"], ref.support)
+    assert np.mean(g["codes"] != ref.codes) <= 1e-3
+    assert np.allclose(g["H"], ref.H, rtol=1e-3, atol=1e-7)
+
+
+def test_zero_budget_equals_plain_cd(qe, oracle):
+    q, p = 64, 130
+    W = synth.gaussian((q, p), seed=7, std=0.02)
+    X = synth.correlated_activations(p, 1024, 0.9, 8)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 3)
+    Hz = torch.zeros((q, p), dtype=torch.float32, device="cuda")
+    sup = torch.zeros(1, dtype=torch.int64, device="cuda")
+    n0 = torch.zeros(1, dtype=torch.int64, device="cuda")
+    g = run_outlier_gpu(qe, W, S32, 3, scale, zero, 0, 1.0, 3, Hz, sup, n0)
+    Wd = dev(W)
+    Wh = torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    R = torch.empty_like(Wd)
+    qe.cd_sweep(Wd, dev(S32), 3, dev(scale), dev(zero), Wh, codes, R, 3)
+    assert np.array_equal(g["What"], host(Wh))
+    assert np.array_equal(g["codes"], host(codes).astype(np.int32))
+    assert not np.any(g["H"])
