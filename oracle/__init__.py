@@ -62,8 +62,39 @@ def _load():
     lib.qeo_cd_sweep_alg2.restype = None
     lib.qeo_topk_abs.argtypes = [_f64p, _i64, _i64, _i64p]
     lib.qeo_topk_abs.restype = _i64
+    lib.qeo_num_threads.argtypes = []
+    lib.qeo_num_threads.restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def num_threads() -> int:
+    """OpenMP threads the oracle's loops use."""
+    return int(_load().qeo_num_threads())
+
+
+def cd_sweep_timed(W, Sigma, bits, scale, zero) -> float:
+    """Wall seconds of one Lemma-1 sweep from What = W, clocked around the C
+    call only (T = W Sigma is formed before the clock starts)."""
+    import time
+    lib = _load()
+    W = np.asarray(W)
+    q, p = W.shape
+    S = _c(Sigma, np.float64)
+    T = _c(np.asarray(W, np.float64) @ S, np.float64)
+    Wh = _c(W, np.float64).copy()
+    codes = np.zeros((q, p), np.int32)
+    valid = np.zeros((q, p), np.uint8)
+    sc = _c(scale, np.float32).astype(np.float64)
+    ze = _c(zero, np.float32).astype(np.float64)
+    t0 = time.perf_counter()
+    rc = lib.qeo_cd_sweep_lemma1(_p(T, _f64p), _p(S, _f64p), q, p, bits, _p(sc, _f64p),
+                                 _p(ze, _f64p), _p(Wh, _f64p), _p(codes, _i32p),
+                                 _p(valid, _u8p), None, 0)
+    dt = time.perf_counter() - t0
+    if rc != 0:
+        raise ValueError("Sigma has a non-positive diagonal entry")
+    return dt
 
 
 def _p(a: np.ndarray, ptype):

@@ -277,3 +277,7 @@ int64_t qeo_topk_abs(const double* V, int64_t count, int64_t s, int64_t* support
     qsort(support, (size_t)nnz, sizeof(int64_t), idx_cmp);
     return nnz;
 }
+
+/* Number of OpenMP threads the loops above run with (for reporting). */
+#include <omp.h>
+int qeo_num_threads(void) { return omp_get_max_threads(); }
