@@ -149,7 +149,8 @@ def main():
     # ---- dominant kernels, measured live on this stream
     # block-update step kernel: sweeps resumed from a valid R, no objective,
     # so the region holds only the step launches (+2 tiny setup kernels)
-    nb = (p + block - 1) // block
+    super_w = max(256, block)                     # columns per step launch (super-block)
+    nb = (p + super_w - 1) // super_w
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     P.cd_sweep(W, Sigma, bits, scale, zero, Wh, codes, R, sweeps, block=block,
@@ -158,7 +159,7 @@ def main():
     torch.cuda.synchronize()
     t_steps = e0.elapsed_time(e1) * 1e-3
     launches = sweeps * (nb + 1)
-    cd_flops_per_launch = 2.0 * q * p * p / (nb + 1)      # 2qp^2 per sweep over nb+1 launches
+    cd_flops_per_launch = 2.0 * q * p * p / (nb + 1)      # 2qp^2 per sweep over nb + 1 launches
     cd_avg = t_steps / launches
     cd_tflops = cd_flops_per_launch / cd_avg / 1e12
     gram_t = float(np.median(phase["gram"]))

@@ -6,20 +6,23 @@
 // and the rank-1 identity of Sec. 4.2 (both halves fused, as the paper's
 // acceleration note suggests) keeps R exact:  R += delta_{:,j} Sigma_{j,:}.
 //
-// Columns are taken in blocks J of width B.  One launch ("step") of
-// cd_step_kernel does two independent jobs on disjoint data:
-//  * panel workgroups (16 rows each) run the B column updates of block J in
+// Columns are taken in blocks J of width B (the panel width), grouped into
+// super-blocks of S = m * B columns.  One launch ("step") of cd_step_kernel
+// does two independent jobs on disjoint data:
+//  * panel workgroups (16 rows each) run the m blocks of super-block t in
 //    order.  Each row is spread over 16 lanes (one DPP row); lane g holds the
 //    block columns g, g + 16, ... in registers.  The owner lane of column j
 //    computes the new code, broadcasts delta with DPP row_newbcast, and every
 //    lane applies delta * Sigma_{j, its columns} from an LDS copy of
-//    Sigma_{J,J}.  Before that, the panel adds the previous block's update to
-//    its own columns (R_{:,J} += Delta_prev Sigma_{Jprev,J}) and writes R_{:,J}.
-//  * GEMM workgroups apply the previous block's update to every other
-//    column: R_{:,~J} += Delta_prev Sigma_{Jprev,~J}, an fp32 matrix-core GEMM
-//    with K = B (Sigma symmetric, so Sigma_{Jprev,c} is row c of Sigma).
-// The panel of block J therefore overlaps the wide GEMM of the block before
-// it.  After the last block, a GEMM-only step leaves R = (What - W) Sigma exact.
+//    Sigma_{J,J}.  Before a block starts, the panel adds to its columns the
+//    deltas of super-block t-1 (written back to R) and of the earlier blocks
+//    of super-block t (kept local).
+//  * GEMM workgroups apply the deltas of super-block t-1 to every column
+//    outside super-block t: R_{:,c} += Delta_{t-1} Sigma_{SB(t-1), c}, an fp32
+//    matrix-core GEMM with K = S (Sigma symmetric, so Sigma_{SB(t-1), c} is a
+//    stretch of row c).
+// The panels of super-block t therefore overlap the wide GEMM of super-block
+// t-1; after the last one a GEMM-only step leaves R = (What - W) Sigma exact.
 #include <utility>
 
 #include "qe_internal.h"
@@ -68,7 +71,7 @@ __global__ void init_from_w_kernel(const float* __restrict__ W, const float* __r
 }
 
 // R = (What + H - W) Sigma over all 128 x 128 tiles (warm start from any What).
-__global__ __launch_bounds__(256) void residual_init_kernel(const float* Wh, const float* H,
+__global__ __launch_bounds__(256, 2) void residual_init_kernel(const float* Wh, const float* H,
                                                             const float* W, const float* Sigma,
                                                             int64_t q, int64_t p, float* R,
                                                             int vec4, const int* status)
@@ -137,17 +140,19 @@ struct StepArgs {
     const float* scale;
     const float* zero;
     const float* inv_s;
-    float* dcur;          // q x B: this block's column deltas (panel output)
-    const float* dprev;   // q x B: previous block's deltas (applied in this step)
+    float* dcur;          // q x S: deltas of the current super-block (panel output)
+    const float* dprev;   // q x S: deltas of the previous super-block (applied here)
     int64_t q, p;
-    int64_t blk;          // first column of the panel block, or -1 (GEMM-only step)
-    int64_t prev_blk;     // first column of the previous block, or -1 (panel-only step)
-    int cur_w, prev_w;    // widths of the two blocks (<= B)
+    int64_t sb;           // first column of the current super-block, or -1 (GEMM-only step)
+    int64_t psb;          // first column of the previous super-block, or -1 (panel-only step)
+    int sbw, psbw;        // their widths (<= S)
+    int S;                // super-block width = row stride of dcur / dprev
     float maxq;
     int codes_valid;      // current codes may be kept on an exact tie (Sec. 4.3)
     int n_panel;          // workgroups [0, n_panel) run the panel
     int64_t tiles_n;      // GEMM column tiles
     int sig_vec4;
+    int r_vec4;           // R allows aligned 16-byte row access
     const int* status;
 };
 
@@ -155,174 +160,260 @@ template <int SLOTS>
 struct PanelState {
     float L[SLOTS];     // residual of the lane's block columns (local copy of R_{i,J})
     float w[SLOTS];     // What_{i,J}
-    float cd[SLOTS];    // codes as floats
     float dl[SLOTS];    // delta of the columns this lane owns
     float invd[SLOTS];  // 1 / Sigma_jj
+    float srow[3][SLOTS];   // Sigma rows J, J+1, J+2 (lane's columns), fetched ahead
 };
 
 // Broadcast lane O of every 16-lane DPP row to the whole row.
 template <int O>
 __device__ __forceinline__ float row_bcast(float v)
 {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), 0x150 + O, 0xF, 0xF,
-                                                      false));
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x150 + O, 0xF, 0xF, false));
+}
+
+template <int SLOTS>
+__device__ __forceinline__ void load_srow(float (&dst)[SLOTS], const float* sS, int row, int g)
+{
+    const float* src = sS + row * (16 * SLOTS) + g * SLOTS;
+    if constexpr (SLOTS % 4 == 0) {
+#pragma unroll
+        for (int q4 = 0; q4 < SLOTS / 4; ++q4) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(src + 4 * q4);
+#pragma unroll
+            for (int u = 0; u < 4; ++u) dst[4 * q4 + u] = v[u];
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < SLOTS; ++m) dst[m] = src[m];
+    }
 }
 
 // One column update (column J of the block) for all 16 rows of the workgroup.
-template <int SLOTS, int J>
+// FULL blocks (width == B) carry no per-column test.  The Sigma row of column
+// J + 2 is fetched from LDS while column J's dependent chain runs.
+template <int SLOTS, int J, bool FULL>
 __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* sS, int g,
                                            int width, float s, float z, float inv_s,
                                            float maxq, bool cvalid)
 {
     constexpr int B = 16 * SLOTS;
     constexpr int M = J / 16, O = J % 16;
-    if (J >= width) return;                          // uniform across the workgroup
+    if (!FULL && J >= width) return;                 // uniform across the workgroup
+    if constexpr (J + 2 < B) load_srow<SLOTS>(st.srow[(J + 2) % 3], sS, J + 2, g);
+    // keep the fetch here: the scheduler would otherwise sink it next to its use
+    __builtin_amdgcn_sched_barrier(0);
+    const float w = st.w[M];
     // Lemma 1: unconstrained minimiser, then its position t on the grid
-    const float beta = fmaf(-st.L[M], st.invd[M], st.w[M]);
+    const float beta = fmaf(-st.L[M], st.invd[M], w);
     const float t = fmaf(beta, inv_s, z);
     // nearest level (half to even), clamped to the finite grid
-    float k = fminf(fmaxf(rintf(t), 0.f), maxq);
-    // modified CD: an equally near current level is kept
-    if (cvalid && fabsf(t - st.cd[M]) <= fabsf(t - k)) k = st.cd[M];
+    const float kn = __builtin_amdgcn_fmed3f(rintf(t), 0.f, maxq);
+    // modified CD: a valid, equally near current level is kept (its code is
+    // recovered exactly from What: |k - z| <= 255 keeps the error far below 1/2)
+    const float kc = rintf(fmaf(w, inv_s, z));
+    const bool keep = cvalid && fabsf(t - kc) <= fabsf(t - kn);
+    const float k = keep ? kc : kn;
     const float wn = s * (k - z);
-    const float delta = wn - st.w[M];
+    const float delta = wn - w;
     const float db = row_bcast<O>(delta);
-    if (g == O) {
-        st.w[M] = wn;
-        st.cd[M] = k;
-        st.dl[M] = delta;
-    }
+    const bool own = g == O;
+    st.w[M] = own ? wn : w;
+    st.dl[M] = own ? delta : st.dl[M];
     // rank-1 update restricted to the block: L_{i,c} += delta_i Sigma_{j,c}
-    const float* srow = sS + J * B + g * SLOTS;
-    if constexpr (SLOTS % 4 == 0) {
 #pragma unroll
-        for (int q4 = 0; q4 < SLOTS / 4; ++q4) {
-            const f32x4 sv = *reinterpret_cast<const f32x4*>(srow + 4 * q4);
-#pragma unroll
-            for (int u = 0; u < 4; ++u) st.L[4 * q4 + u] = fmaf(db, sv[u], st.L[4 * q4 + u]);
-        }
-    } else {
-#pragma unroll
-        for (int mm = 0; mm < SLOTS; ++mm) st.L[mm] = fmaf(db, srow[mm], st.L[mm]);
-    }
+    for (int mm = 0; mm < SLOTS; ++mm) st.L[mm] = fmaf(db, st.srow[J % 3][mm], st.L[mm]);
 }
 
-template <int SLOTS, int... Js>
+template <int SLOTS, bool FULL, int... Js>
 __device__ __forceinline__ void panel_run(std::integer_sequence<int, Js...>,
                                           PanelState<SLOTS>& st, const float* sS, int g,
                                           int width, float s, float z, float inv_s, float maxq,
                                           bool cvalid)
 {
-    (panel_step<SLOTS, Js>(st, sS, g, width, s, z, inv_s, maxq, cvalid), ...);
+    load_srow<SLOTS>(st.srow[0], sS, 0, g);
+    if constexpr (16 * SLOTS > 1) load_srow<SLOTS>(st.srow[1], sS, 1, g);
+    (panel_step<SLOTS, Js, FULL>(st, sS, g, width, s, z, inv_s, maxq, cvalid), ...);
 }
 
 // Stages Sigma[r0 + k][c0 + c] (k < kw, c < cw; else 0) into LDS with the
 // column permutation used by the panel: column c = 16 m + g sits at g * SLOTS + m.
+// Full blocks issue all their 16-byte loads before the first LDS store, so the
+// global latency is paid once per block.
 template <int SLOTS>
-__device__ inline void stage_sigma_block(const float* __restrict__ Sigma, int64_t p, int64_t r0,
-                                         int kw, int64_t c0, int cw, float* sS)
+__device__ __forceinline__ void stage_sigma_block(const float* __restrict__ Sigma, int64_t p,
+                                                  int64_t r0, int kw, int64_t c0, int cw,
+                                                  bool vec4, float* sS)
 {
     constexpr int B = 16 * SLOTS;
+    constexpr int Q = B / 4;                     // float4 per row
+    constexpr int PER = (B * Q + 255) / 256;     // float4 per thread
+    if (vec4 && kw == B && cw == B) {
+        f32x4 v[PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int f = threadIdx.x + 256 * u;
+            if (f < B * Q)
+                v[u] = *reinterpret_cast<const f32x4*>(Sigma + (r0 + f / Q) * p + c0 + 4 * (f % Q));
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int f = threadIdx.x + 256 * u;
+            if (f >= B * Q) continue;
+            const int k = f / Q, cb = 4 * (f % Q);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int cc = cb + e;
+                sS[k * B + (cc & 15) * SLOTS + (cc >> 4)] = v[u][e];
+            }
+        }
+        return;
+    }
     for (int e = threadIdx.x; e < B * B; e += blockDim.x) {
-        const int k = e / B, c = e % B;
-        float v = 0.f;
-        if (k < kw && c < cw) v = Sigma[(r0 + k) * p + c0 + c];
-        sS[k * B + (c & 15) * SLOTS + (c >> 4)] = v;
+        const int k = e / B, cc = e % B;
+        float x = 0.f;
+        if (k < kw && cc < cw) x = Sigma[(r0 + k) * p + c0 + cc];
+        sS[k * B + (cc & 15) * SLOTS + (cc >> 4)] = x;
+    }
+}
+
+// L_{i,J} += D_{i, k0..k0+kw} Sigma_{r0..r0+kw, J} for the workgroup's 16 rows,
+// with D a q x S row-major delta buffer.  Uses sS / sD as staging.
+template <int SLOTS>
+__device__ __forceinline__ void add_block_update(PanelState<SLOTS>& st, const StepArgs& a,
+                                                 const float* D, int64_t k0, int kw, int64_t r0,
+                                                 int64_t j0, int width, int64_t i0, int lrow,
+                                                 int g, float* sS, float* sD)
+{
+    constexpr int B = 16 * SLOTS;
+    __syncthreads();                                 // staging buffers free
+    stage_sigma_block<SLOTS>(a.Sigma, a.p, r0, kw, j0, width, a.sig_vec4 != 0, sS);
+    if (kw == B && i0 + 16 <= a.q) {
+        constexpr int PER = (16 * B / 4 + 255) / 256;
+        f32x4 v[PER];
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int f = threadIdx.x + 256 * u;
+            if (f < 16 * B / 4)
+                v[u] = *reinterpret_cast<const f32x4*>(D + (i0 + f / (B / 4)) * a.S + k0 +
+                                                       4 * (f % (B / 4)));
+        }
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int f = threadIdx.x + 256 * u;
+            if (f < 16 * B / 4) *reinterpret_cast<f32x4*>(sD + 4 * f) = v[u];
+        }
+    } else {
+        for (int e = threadIdx.x; e < 16 * B; e += blockDim.x) {
+            const int r = e / B, k = e % B;
+            const int64_t ii = i0 + r;
+            sD[e] = (ii < a.q && k < kw) ? D[ii * a.S + k0 + k] : 0.f;
+        }
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int k = 0; k < kw; ++k) {
+        const float dk = sD[lrow * B + k];
+#pragma unroll
+        for (int m = 0; m < SLOTS; ++m) st.L[m] = fmaf(dk, sS[k * B + g * SLOTS + m], st.L[m]);
     }
 }
 
 template <int SLOTS>
-__device__ void panel_role(const StepArgs& a, float* lds)
+__device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
 {
     constexpr int B = 16 * SLOTS;
     float* sS = lds;            // B x B
-    float* sD = lds + B * B;    // 16 x B: previous deltas of this workgroup's rows
+    float* sD = lds + B * B;    // 16 x B
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane & 15;
     const int lrow = wave * 4 + (lane >> 4);
     const int64_t i0 = (int64_t)blockIdx.x * 16;
     const int64_t i = i0 + lrow;
     const bool rowok = i < a.q;
-    const int width = a.cur_w;
     const int64_t p = a.p;
-
-    PanelState<SLOTS> st;
-#pragma unroll
-    for (int m = 0; m < SLOTS; ++m) {
-        const int c = 16 * m + g;
-        const bool ok = rowok && c < width;
-        const int64_t idx = i * p + a.blk + c;
-        st.L[m] = ok ? a.R[idx] : 0.f;
-        st.w[m] = ok ? a.Wh[idx] : 0.f;
-        st.cd[m] = ok ? (float)a.codes[idx] : 0.f;
-        st.invd[m] = c < width ? a.inv_d[a.blk + c] : 0.f;
-        st.dl[m] = 0.f;
-    }
     const float s = rowok ? a.scale[i] : 1.f;
     const float z = rowok ? a.zero[i] : 0.f;
     const float inv_s = rowok ? a.inv_s[i] : 1.f;
+    const int nsub = (int)cdiv(a.sbw, B);
 
-    if (a.prev_blk >= 0) {
-        // look-ahead: R_{i,J} += Delta_prev_{i,:} Sigma_{Jprev, J}
-        const int pw = a.prev_w;
-        stage_sigma_block<SLOTS>(a.Sigma, p, a.prev_blk, pw, a.blk, width, sS);
-        for (int e = threadIdx.x; e < 16 * B; e += blockDim.x) {
-            const int64_t ii = i0 + e / B;
-            sD[e] = ii < a.q ? a.dprev[ii * B + (e % B)] : 0.f;
-        }
-        __syncthreads();
-        for (int k = 0; k < pw; ++k) {
-            const float dk = sD[lrow * B + k];
-#pragma unroll
-            for (int m = 0; m < SLOTS; ++m) st.L[m] = fmaf(dk, sS[k * B + g * SLOTS + m], st.L[m]);
-        }
+    for (int sub = 0; sub < nsub; ++sub) {
+        const int64_t j0 = a.sb + (int64_t)sub * B;
+        const int width = (int)min((int64_t)B, a.sb + a.sbw - j0);
+        PanelState<SLOTS> st;
 #pragma unroll
         for (int m = 0; m < SLOTS; ++m) {
             const int c = 16 * m + g;
-            if (rowok && c < width) a.R[i * p + a.blk + c] = st.L[m];
+            const bool ok = rowok && c < width;
+            const int64_t idx = i * p + j0 + c;
+            st.L[m] = ok ? a.R[idx] : 0.f;
+            st.w[m] = ok ? a.Wh[idx] : 0.f;
+            st.invd[m] = c < width ? a.inv_d[j0 + c] : 0.f;
+            st.dl[m] = 0.f;
         }
-        __syncthreads();
-    }
-
-    stage_sigma_block<SLOTS>(a.Sigma, p, a.blk, width, a.blk, width, sS);
-    __syncthreads();
-    panel_run<SLOTS>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s, z, inv_s,
-                     a.maxq, a.codes_valid != 0);
-
+        // (1) look-ahead: deltas of the previous super-block, R_{i,J} written back
+        if (a.psb >= 0) {
+            for (int kc = 0; kc < a.psbw; kc += B) {
+                const int kw = min(B, a.psbw - kc);
+                add_block_update<SLOTS>(st, a, a.dprev, kc, kw, a.psb + kc, j0, width, i0, lrow, g,
+                                        sS, sD);
+            }
 #pragma unroll
-    for (int m = 0; m < SLOTS; ++m) {
-        const int c = 16 * m + g;
-        if (rowok && c < width) {
-            a.Wh[i * p + a.blk + c] = st.w[m];
-            a.codes[i * p + a.blk + c] = (uint8_t)st.cd[m];
+            for (int m = 0; m < SLOTS; ++m) {
+                const int c = 16 * m + g;
+                if (rowok && c < width) a.R[i * p + j0 + c] = st.L[m];
+            }
         }
-        if (rowok) a.dcur[i * B + c] = st.dl[m];
+        // (2) earlier blocks of this super-block (this workgroup's own rows; not
+        //     written to R: the next launch's GEMM applies the whole super-block)
+        for (int sp = 0; sp < sub; ++sp)
+            add_block_update<SLOTS>(st, a, a.dcur, (int64_t)sp * B, B, a.sb + (int64_t)sp * B, j0,
+                                    width, i0, lrow, g, sS, sD);
+        // (3) the B column updates in order
+        __syncthreads();
+        stage_sigma_block<SLOTS>(a.Sigma, p, j0, width, j0, width, a.sig_vec4 != 0, sS);
+        __syncthreads();
+        if (width == B)
+            panel_run<SLOTS, true>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s, z,
+                                   inv_s, a.maxq, a.codes_valid != 0);
+        else
+            panel_run<SLOTS, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s, z,
+                                    inv_s, a.maxq, a.codes_valid != 0);
+#pragma unroll
+        for (int m = 0; m < SLOTS; ++m) {
+            const int c = 16 * m + g;
+            if (rowok && c < width) {
+                a.Wh[i * p + j0 + c] = st.w[m];
+                a.codes[i * p + j0 + c] = (uint8_t)rintf(fmaf(st.w[m], inv_s, z));
+            }
+            if (rowok) a.dcur[i * a.S + (int64_t)sub * B + c] = st.dl[m];
+        }
+        // This block's deltas are read back only by this workgroup (its next
+        // blocks), after the __syncthreads() that opens add_block_update: a
+        // workgroup-scope release/acquire.  A device-scope fence here would
+        // write back and invalidate L2 under the concurrent GEMM tiles.
     }
 }
 
-template <int SLOTS>
-__device__ void gemm_role(const StepArgs& a, float* lds, int64_t t)
+// R's tile is read only after the K loop (through an LDS-staged, float4-wide
+// read-modify-write): holding it across the loop would cost 64 registers and
+// the second workgroup per CU, which matters more than hiding its latency.
+__device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t t)
 {
-    constexpr int B = 16 * SLOTS;
     const int64_t tm = t / a.tiles_n, tn = t % a.tiles_n;
     const int64_t row0 = tm * kTile, col0 = tn * kTile;
-    const int64_t ex0 = a.blk, ex1 = a.blk >= 0 ? a.blk + a.cur_w : -1;
-    if (a.blk >= 0 && col0 >= ex0 && min(col0 + kTile, a.p) <= ex1) return;   // all in J
+    const int64_t ex0 = a.sb >= 0 ? a.sb : 0, ex1 = a.sb >= 0 ? a.sb + a.sbw : 0;
+    if (a.sb >= 0 && col0 >= ex0 && min(col0 + kTile, a.p) <= ex1) return;   // all excluded
     f32x16 acc[2][2];
     zero_acc(acc);
-    const RowOp A{a.dprev, B, a.q, a.prev_w, true};
-    const RowOp Bo{a.Sigma + a.prev_blk, a.p, a.p, a.prev_w, a.sig_vec4 != 0};
-    nt_tile(A, row0, Bo, col0, a.prev_w, lds, acc);
-#pragma unroll
-    for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t r = row0 + acc_row(mi, v), c = col0 + acc_col(ni);
-                if (r < a.q && c < a.p && !(c >= ex0 && c < ex1))
-                    a.R[r * a.p + c] += acc[mi][ni][v];
-            }
+    const RowOp A{a.dprev, a.S, a.q, a.psbw, true};
+    const RowOp Bo{a.Sigma + a.psb, a.p, a.p, a.psbw, a.sig_vec4 != 0};
+    nt_tile(A, row0, Bo, col0, a.psbw, lds, acc);
+    acc_to_lds(acc, lds);                                // nt_tile ended with a barrier
+    __syncthreads();
+    TileRM rv;
+    tile_load_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv);
+    tile_add_store_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv, lds, ex0, ex1);
 }
 
 template <int SLOTS>
@@ -334,26 +425,29 @@ constexpr int step_lds_floats()
 }
 
 template <int SLOTS>
-__global__ __launch_bounds__(256) void cd_step_kernel(StepArgs a)
+__global__ __launch_bounds__(256, 2) void cd_step_kernel(StepArgs a)
 {
     if (failed(a.status)) return;
     __shared__ __attribute__((aligned(16))) float lds[step_lds_floats<SLOTS>()];
     if ((int)blockIdx.x < a.n_panel)
         panel_role<SLOTS>(a, lds);
     else
-        gemm_role<SLOTS>(a, lds, (int64_t)blockIdx.x - a.n_panel);
+        gemm_role(a, lds, (int64_t)blockIdx.x - a.n_panel);
 }
 
 // ---------------------------------------------------------------- host side
 static int block_width(int block) { return block == 0 ? 128 : block; }
 
+// Super-block width = the GEMM's K per launch (a multiple of the panel width).
+static int super_width(int B) { return B >= 256 ? B : 256; }
+
 size_t cd_ws_bytes(int64_t q, int64_t p, int block)
 {
-    const int B = block_width(block);
+    const int S = super_width(block_width(block));
     size_t b = kStatusBytes;
     b += align256(sizeof(float) * p);               // inv_d
     b += align256(sizeof(float) * q);               // inv_s
-    b += 2 * align256(sizeof(float) * q * B);       // delta double buffer
+    b += 2 * align256(sizeof(float) * q * S);       // delta double buffer
     b += align256(sizeof(double) * kObjBlocks);     // objective partials
     return b;
 }
@@ -371,23 +465,24 @@ qe_status launch_residual_dot(const float* W, const float* Wh, const float* H, c
 }
 
 template <int SLOTS>
-static qe_status launch_steps(StepArgs base, float* d0, float* d1, int64_t nb, int64_t q,
-                              int64_t p, hipStream_t s)
+static qe_status launch_steps(StepArgs base, float* d0, float* d1, int64_t q, int64_t p,
+                              hipStream_t s)
 {
-    constexpr int B = 16 * SLOTS;
+    const int S = base.S;
+    const int64_t nsb = cdiv(p, S);
     const int64_t panel_wgs = cdiv(q, 16);
     const int64_t tiles_m = cdiv(q, kTile), tiles_n = cdiv(p, kTile);
-    for (int64_t k = 0; k <= nb; ++k) {
+    for (int64_t t = 0; t <= nsb; ++t) {
         StepArgs a = base;
-        a.blk = k < nb ? k * B : -1;
-        a.cur_w = k < nb ? (int)std::min<int64_t>(B, p - k * B) : 0;
-        a.prev_blk = k > 0 ? (k - 1) * B : -1;
-        a.prev_w = k > 0 ? (int)std::min<int64_t>(B, p - (k - 1) * B) : 0;
-        a.dcur = (k & 1) ? d1 : d0;
-        a.dprev = (k & 1) ? d0 : d1;
-        a.n_panel = k < nb ? (int)panel_wgs : 0;
+        a.sb = t < nsb ? t * S : -1;
+        a.sbw = t < nsb ? (int)std::min<int64_t>(S, p - t * S) : 0;
+        a.psb = t > 0 ? (t - 1) * S : -1;
+        a.psbw = t > 0 ? (int)std::min<int64_t>(S, p - (t - 1) * S) : 0;
+        a.dcur = (t & 1) ? d1 : d0;
+        a.dprev = (t & 1) ? d0 : d1;
+        a.n_panel = t < nsb ? (int)panel_wgs : 0;
         a.tiles_n = tiles_n;
-        const int64_t gemm_wgs = k > 0 ? tiles_m * tiles_n : 0;
+        const int64_t gemm_wgs = t > 0 ? tiles_m * tiles_n : 0;
         const int64_t grid = a.n_panel + gemm_wgs;
         hipLaunchKernelGGL(cd_step_kernel<SLOTS>, dim3((unsigned)grid), dim3(256), 0, s, a);
         if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
@@ -401,12 +496,13 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
                     int obj_stride, void* ws, hipStream_t s)
 {
     const int B = block_width(block);
+    const int S = super_width(B);
     int* status = static_cast<int*>(ws);
     Ws w(ws);
     float* inv_d = w.take<float>(p);
     float* inv_s = w.take<float>(q);
-    float* d0 = w.take<float>((size_t)q * B);
-    float* d1 = w.take<float>((size_t)q * B);
+    float* d0 = w.take<float>((size_t)q * S);
+    float* d1 = w.take<float>((size_t)q * S);
     double* part = w.take<double>(kObjBlocks);
 
     hipLaunchKernelGGL(diag_prep_kernel, dim3((unsigned)cdiv(p, 256)), dim3(256), 0, s, Sigma, p,
@@ -436,19 +532,20 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     base.inv_s = inv_s;
     base.q = q;
     base.p = p;
+    base.S = S;
     base.maxq = (float)((1 << bits) - 1);
     base.sig_vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
+    base.r_vec4 = (aligned16(R) && p % 4 == 0) ? 1 : 0;
     base.status = status;
     const bool codes_valid0 = (flags & QE_CODES_VALID) && !(flags & QE_INIT_FROM_W);
-    const int64_t nb = cdiv(p, B);
     for (int sw = 0; sw < sweeps; ++sw) {
         base.codes_valid = (sw > 0 || codes_valid0) ? 1 : 0;
         qe_status st;
         switch (B) {
-            case 16: st = launch_steps<1>(base, d0, d1, nb, q, p, s); break;
-            case 32: st = launch_steps<2>(base, d0, d1, nb, q, p, s); break;
-            case 64: st = launch_steps<4>(base, d0, d1, nb, q, p, s); break;
-            default: st = launch_steps<8>(base, d0, d1, nb, q, p, s); break;
+            case 16: st = launch_steps<1>(base, d0, d1, q, p, s); break;
+            case 32: st = launch_steps<2>(base, d0, d1, q, p, s); break;
+            case 64: st = launch_steps<4>(base, d0, d1, q, p, s); break;
+            default: st = launch_steps<8>(base, d0, d1, q, p, s); break;
         }
         if (st != QE_OK) return st;
         if (obj) {

@@ -2,17 +2,23 @@
 //
 // Lemma 1 (Sec. 4.2) needs X only through Sigma, a p x p statistic whose size
 // does not grow with the token count n.  Work split: 128 x 128 tiles of the
-// upper triangle (ti <= tj) x token splits.  Inside a workgroup the products
-// of `kInnerChunks` K-chunks are summed in the matrix-core accumulators, then
-// added into a second fp32 accumulator, which keeps each running sum short
-// (~512 terms) at n = 262144.  With several splits, partial tiles go to the
-// workspace and a finalize kernel adds them in a fixed order in fp64.  The
-// lower triangle is written as an exact mirror through an LDS transpose.
+// upper triangle (ti <= tj) x token splits of at most kSplitTokens tokens.
+// Each workgroup sums its split in the fp32 matrix-core accumulators (a
+// running sum of <= 16384 products: ~3e-7 relative error at this workload's
+// statistics), writes the partial tile to the workspace, and a finalize kernel
+// adds the splits in a fixed order in fp64.  When the split partials would
+// not fit the workspace budget (very large p), one workgroup per tile sums all
+// tokens with a two-level accumulator (inner sums of 512 tokens added into a
+// second fp32 accumulator) and writes Sigma directly.  The lower triangle is
+// written as an exact mirror through an LDS transpose.
 #include "qe_internal.h"
 
 namespace qe {
 
-constexpr int kInnerChunks = 16;          // 16 x 32 = 512 tokens per inner sum
+constexpr int kInnerChunks = 16;          // two-level mode: 16 x 32 = 512 tokens per inner sum
+constexpr int64_t kSplitTokens = 16384;   // split mode: preferred tokens per workgroup
+constexpr int64_t kSplitTokensMax = 32768;  // longest single fp32 running sum allowed
+constexpr size_t kSplitBudget = size_t(2) << 30;   // bytes of split partials allowed
 constexpr int kTileFloats = kTile * kTile;
 constexpr int kTStride = kTile + 1;       // LDS transpose tile row stride
 
@@ -56,11 +62,10 @@ __device__ void write_symmetric(float* tileLds, int64_t ti, int64_t tj, float* S
     }
 }
 
-template <bool TRANS>
-__global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ X, int64_t p,
-                                                   int64_t n, int64_t nt, int64_t split_len,
-                                                   float* __restrict__ out, int direct,
-                                                   int accumulate, int x_vec4, const int* status)
+template <bool TRANS, bool TWO_LEVEL>
+__global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_kernel(
+    const float* __restrict__ X, int64_t p, int64_t n, int64_t nt, int64_t split_len,
+    float* __restrict__ out, int accumulate, int x_vec4, const int* status)
 {
     if (failed(status)) return;
     __shared__ __attribute__((aligned(16))) float lds[kNTLdsFloats];
@@ -69,12 +74,8 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ X, 
     const int64_t k0 = (int64_t)blockIdx.y * split_len;
     const int64_t k1 = min(n, k0 + split_len);
 
-    f32x16 acc[2][2], outer[2][2];
-    zero_acc(outer);
-    const int64_t inner = (int64_t)kInnerChunks * kKC;
-    for (int64_t kb = k0; kb < k1; kb += inner) {
-        const int64_t ke = min(k1, kb + inner);
-        zero_acc(acc);
+    f32x16 acc[2][2];
+    auto run = [&](int64_t kb, int64_t ke) {
         if (TRANS) {
             // X is n x p: element (channel r, token k) at X[k * p + r]
             const ColOp op{X + kb * p, p, p, ke - kb, x_vec4 != 0};
@@ -83,13 +84,19 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ X, 
             const RowOp op{X + kb, n, p, ke - kb, x_vec4 != 0};
             nt_tile(op, ti * kTile, op, tj * kTile, ke - kb, lds, acc);
         }
+    };
+    if constexpr (TWO_LEVEL) {
+        f32x16 outer[2][2];
+        zero_acc(outer);
+        const int64_t inner = (int64_t)kInnerChunks * kKC;
+        for (int64_t kb = k0; kb < k1; kb += inner) {
+            zero_acc(acc);
+            run(kb, min(k1, kb + inner));
 #pragma unroll
-        for (int a = 0; a < 2; ++a)
+            for (int a = 0; a < 2; ++a)
 #pragma unroll
-            for (int b = 0; b < 2; ++b) outer[a][b] += acc[a][b];
-    }
-
-    if (direct) {
+                for (int b = 0; b < 2; ++b) outer[a][b] += acc[a][b];
+        }
         float* tl = lds;   // reuse the pipeline LDS (nt_tile ended with a barrier)
 #pragma unroll
         for (int mi = 0; mi < 2; ++mi)
@@ -101,6 +108,8 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ X, 
         __syncthreads();
         write_symmetric(tl, ti, tj, out, p, accumulate);
     } else {
+        zero_acc(acc);
+        run(k0, k1);
         float* dst = out + ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * kTileFloats;
 #pragma unroll
         for (int mi = 0; mi < 2; ++mi)
@@ -108,7 +117,7 @@ __global__ __launch_bounds__(256) void gram_kernel(const float* __restrict__ X, 
             for (int ni = 0; ni < 2; ++ni)
 #pragma unroll
                 for (int v = 0; v < 16; ++v)
-                    dst[acc_row(mi, v) * kTile + acc_col(ni)] = outer[mi][ni][v];
+                    dst[acc_row(mi, v) * kTile + acc_col(ni)] = acc[mi][ni][v];
     }
 }
 
@@ -145,26 +154,24 @@ __global__ __launch_bounds__(256) void damp_kernel(float* Sigma, int64_t p, floa
     for (int64_t j = threadIdx.x; j < p; j += blockDim.x) Sigma[j * p + j] += add;
 }
 
-static int gram_splits(int64_t p, int64_t n)
+// Number of token splits (each <= kSplitTokens), or 0 for the two-level direct mode.
+static int64_t gram_splits(int64_t p, int64_t n)
 {
     const int64_t nt = cdiv(p, kTile);
     const int64_t tiles = nt * (nt + 1) / 2;
-    int64_t s = cdiv(1024, tiles);
-    const int64_t max_by_n = cdiv(n, (int64_t)kInnerChunks * kKC);
-    if (s > max_by_n) s = max_by_n;
-    if (s > 32) s = 32;
-    if (s < 1) s = 1;
-    return (int)s;
+    for (int64_t len = kSplitTokens; len <= kSplitTokensMax; len *= 2) {
+        const int64_t s = cdiv(n, len);
+        if ((size_t)s * tiles * kTileFloats * sizeof(float) <= kSplitBudget) return s;
+    }
+    return 0;
 }
 
 size_t gram_ws_bytes(int64_t p, int64_t n)
 {
     const int64_t nt = cdiv(p, kTile);
     const int64_t tiles = nt * (nt + 1) / 2;
-    const int splits = gram_splits(p, n);
-    size_t b = kStatusBytes;
-    if (splits > 1) b += align256((size_t)splits * tiles * kTileFloats * sizeof(float));
-    return b;
+    const int64_t splits = gram_splits(p, n);
+    return kStatusBytes + align256((size_t)splits * tiles * kTileFloats * sizeof(float));
 }
 
 qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma,
@@ -173,28 +180,35 @@ qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* S
     int* status = static_cast<int*>(ws);
     const int64_t nt = cdiv(p, kTile);
     const int64_t tiles = nt * (nt + 1) / 2;
-    const int splits = gram_splits(p, n);
-    // split length: a multiple of the inner sum length
-    const int64_t inner = (int64_t)kInnerChunks * kKC;
-    const int64_t split_len = cdiv(cdiv(n, splits), inner) * inner;
-    const int used_splits = (int)cdiv(n, split_len);
-    dim3 grid((unsigned)tiles, (unsigned)used_splits);
-    const bool direct = used_splits == 1;
-    float* parts = direct ? Sigma : reinterpret_cast<float*>(static_cast<char*>(ws) + kStatusBytes);
+    const int64_t splits = gram_splits(p, n);
     // 16-byte loads need an aligned base and a row stride that keeps them aligned
     const int x_vec4 = aligned16(X) && ((layout == QE_LAYOUT_PN ? n : p) % 4 == 0);
-    if (layout == QE_LAYOUT_PN)
-        hipLaunchKernelGGL(gram_kernel<false>, grid, dim3(256), 0, s, X, p, n, nt, split_len,
-                           parts, direct ? 1 : 0, accumulate, x_vec4, status);
-    else
-        hipLaunchKernelGGL(gram_kernel<true>, grid, dim3(256), 0, s, X, p, n, nt, split_len,
-                           parts, direct ? 1 : 0, accumulate, x_vec4, status);
-    if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
-    if (!direct) {
-        hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)tiles), dim3(256), 0, s, parts,
-                           tiles, used_splits, nt, Sigma, p, accumulate, status);
+    const bool trans = layout == QE_LAYOUT_NP;
+    if (splits == 0) {
+        dim3 grid((unsigned)tiles, 1);
+        if (trans)
+            hipLaunchKernelGGL((gram_kernel<true, true>), grid, dim3(256), 0, s, X, p, n, nt, n,
+                               Sigma, accumulate, x_vec4, status);
+        else
+            hipLaunchKernelGGL((gram_kernel<false, true>), grid, dim3(256), 0, s, X, p, n, nt, n,
+                               Sigma, accumulate, x_vec4, status);
+    } else {
+        // split length: a multiple of the K chunk, at most kSplitTokensMax
+        const int64_t split_len = cdiv(cdiv(n, splits), kKC) * kKC;
+        const int64_t used = cdiv(n, split_len);
+        float* parts = reinterpret_cast<float*>(static_cast<char*>(ws) + kStatusBytes);
+        dim3 grid((unsigned)tiles, (unsigned)used);
+        if (trans)
+            hipLaunchKernelGGL((gram_kernel<true, false>), grid, dim3(256), 0, s, X, p, n, nt,
+                               split_len, parts, accumulate, x_vec4, status);
+        else
+            hipLaunchKernelGGL((gram_kernel<false, false>), grid, dim3(256), 0, s, X, p, n, nt,
+                               split_len, parts, accumulate, x_vec4, status);
         if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+        hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)tiles), dim3(256), 0, s, parts,
+                           tiles, (int)used, nt, Sigma, p, accumulate, status);
     }
+    if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
     if (damp > 0.f) {
         hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, Sigma, p, damp, status);
         if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;

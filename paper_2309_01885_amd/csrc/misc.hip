@@ -57,7 +57,7 @@ qe_status launch_grid_minmax(const float* W, const float* H, int64_t q, int64_t 
 // <A, A Sigma> for A = P1 + P2 - P3 (P2, P3 nullable), fused: each 128 x 128
 // tile of A Sigma is formed on matrix cores and immediately dotted with the
 // matching tile of A in fp64; per-tile partials are summed in a fixed order.
-__global__ __launch_bounds__(256) void quad_form_kernel(const float* p1, const float* p2,
+__global__ __launch_bounds__(256, 2) void quad_form_kernel(const float* p1, const float* p2,
                                                         const float* p3, const float* Sigma,
                                                         int64_t q, int64_t p, double* partial,
                                                         int vec4, const int* status)

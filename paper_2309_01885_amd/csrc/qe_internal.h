@@ -56,6 +56,8 @@ __device__ inline void store_rowmajor(float* lds, const Stage& st)
 }
 
 // Row-major operand: element (r, k) at base[r * ld + k].
+// Chunks fully inside the matrix take a branch-free path (the test is uniform
+// across the workgroup); edge chunks fall back to guarded element loads.
 struct RowOp {
     const float* base;
     int64_t ld, rows, kvalid;
@@ -64,6 +66,13 @@ struct RowOp {
     {
         const int t = threadIdx.x;
         const int kq = (t & 7) * 4;
+        if (vec4 && row0 + kTile <= rows && k0 + kKC <= kvalid) {
+            const float* src = base + (row0 + (t >> 3)) * ld + k0 + kq;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                st.v[m] = *reinterpret_cast<const f32x4*>(src + (int64_t)(32 * m) * ld);
+            return;
+        }
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int64_t gr = row0 + (t >> 3) + 32 * m;
@@ -71,13 +80,9 @@ struct RowOp {
             f32x4 v = {0.f, 0.f, 0.f, 0.f};
             if (gr < rows) {
                 const float* src = base + gr * ld + gk;
-                if (vec4 && gk + 3 < kvalid) {
-                    v = *reinterpret_cast<const f32x4*>(src);
-                } else {
 #pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (gk + u < kvalid) v[u] = src[u];
-                }
+                for (int u = 0; u < 4; ++u)
+                    if (gk + u < kvalid) v[u] = src[u];
             }
             st.v[m] = v;
         }
@@ -94,6 +99,18 @@ struct CompOp {
     {
         const int t = threadIdx.x;
         const int kq = (t & 7) * 4;
+        if (vec4 && row0 + kTile <= rows && k0 + kKC <= kvalid) {
+            const int64_t off0 = (row0 + (t >> 3)) * ld + k0 + kq;
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const int64_t off = off0 + (int64_t)(32 * m) * ld;
+                f32x4 v = *reinterpret_cast<const f32x4*>(p1 + off);
+                if (p2) v = v + *reinterpret_cast<const f32x4*>(p2 + off);
+                if (p3) v = v - *reinterpret_cast<const f32x4*>(p3 + off);
+                st.v[m] = v;
+            }
+            return;
+        }
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int64_t gr = row0 + (t >> 3) + 32 * m;
@@ -101,20 +118,14 @@ struct CompOp {
             f32x4 v = {0.f, 0.f, 0.f, 0.f};
             if (gr < rows) {
                 const int64_t off = gr * ld + gk;
-                if (vec4 && gk + 3 < kvalid) {
-                    v = *reinterpret_cast<const f32x4*>(p1 + off);
-                    if (p2) v = v + *reinterpret_cast<const f32x4*>(p2 + off);
-                    if (p3) v = v - *reinterpret_cast<const f32x4*>(p3 + off);
-                } else {
 #pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (gk + u < kvalid) {
-                            float x = p1[off + u];
-                            if (p2) x = x + p2[off + u];
-                            if (p3) x = x - p3[off + u];
-                            v[u] = x;
-                        }
-                }
+                for (int u = 0; u < 4; ++u)
+                    if (gk + u < kvalid) {
+                        float x = p1[off + u];
+                        if (p2) x = x + p2[off + u];
+                        if (p3) x = x - p3[off + u];
+                        v[u] = x;
+                    }
             }
             st.v[m] = v;
         }
@@ -133,6 +144,13 @@ struct ColOp {
     {
         const int t = threadIdx.x;
         const int rq = (t & 31) * 4;
+        if (vec4 && row0 + kTile <= rows && k0 + kKC <= kvalid) {
+            const float* src = base + (k0 + (t >> 5)) * ld + row0 + rq;
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+                st.v[m] = *reinterpret_cast<const f32x4*>(src + (int64_t)(8 * m) * ld);
+            return;
+        }
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int64_t gk = k0 + (t >> 5) + 8 * m;
@@ -140,13 +158,9 @@ struct ColOp {
             f32x4 v = {0.f, 0.f, 0.f, 0.f};
             if (gk < kvalid) {
                 const float* src = base + gk * ld + gr;
-                if (vec4 && gr + 3 < rows) {
-                    v = *reinterpret_cast<const f32x4*>(src);
-                } else {
 #pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        if (gr + u < rows) v[u] = src[u];
-                }
+                for (int u = 0; u < 4; ++u)
+                    if (gr + u < rows) v[u] = src[u];
             }
             st.v[m] = v;
         }
@@ -205,32 +219,171 @@ __device__ inline int acc_col(int ni)
     return wn * 64 + ni * 32 + (lane & 31);
 }
 
+// Loads the 128 x 128 tile at (row0, col0) of a row-major matrix (ld floats
+// per row) in accumulator layout; elements outside rows x cols read as 0.
+__device__ inline void tile_load(const float* M, int64_t ld, int64_t rows, int64_t cols,
+                                 int64_t row0, int64_t col0, f32x16 (&v)[2][2])
+{
+    if (row0 + kTile <= rows && col0 + kTile <= cols) {
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    v[mi][ni][e] = M[(row0 + acc_row(mi, e)) * ld + col0 + acc_col(ni)];
+        return;
+    }
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int64_t r = row0 + acc_row(mi, e), c = col0 + acc_col(ni);
+                v[mi][ni][e] = (r < rows && c < cols) ? M[r * ld + c] : 0.f;
+            }
+}
+
+// Stores v to the tile at (row0, col0), skipping elements outside rows x cols
+// and columns in [ex0, ex1).
+__device__ inline void tile_store(float* M, int64_t ld, int64_t rows, int64_t cols, int64_t row0,
+                                  int64_t col0, const f32x16 (&v)[2][2], int64_t ex0 = 0,
+                                  int64_t ex1 = 0)
+{
+    if (row0 + kTile <= rows && col0 + kTile <= cols && (ex1 <= col0 || ex0 >= col0 + kTile)) {
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+                for (int e = 0; e < 16; ++e)
+                    M[(row0 + acc_row(mi, e)) * ld + col0 + acc_col(ni)] = v[mi][ni][e];
+        return;
+    }
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int64_t r = row0 + acc_row(mi, e), c = col0 + acc_col(ni);
+                if (r < rows && c < cols && !(c >= ex0 && c < ex1)) M[r * ld + c] = v[mi][ni][e];
+            }
+}
+
+// Row-major view of a 128 x 128 tile for a 256-thread workgroup: thread t owns
+// the float4 at row (t >> 5) + 8 j, columns 4 (t & 31) .. +3, for j = 0..15.
+// One base address per thread keeps a prefetched tile cheap in registers.
+struct TileRM { f32x4 v[16]; };
+
+__device__ inline void tile_load_rm(const float* M, int64_t ld, int64_t rows, int64_t cols,
+                                    int64_t row0, int64_t col0, bool vec4, TileRM& T)
+{
+    const int t = threadIdx.x;
+    const int64_t r0 = row0 + (t >> 5), c0 = col0 + 4 * (t & 31);
+    if (vec4 && row0 + kTile <= rows && col0 + kTile <= cols) {
+        const float* base = M + r0 * ld + c0;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) T.v[j] = *reinterpret_cast<const f32x4*>(base + 8 * j * ld);
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const int64_t r = r0 + 8 * j;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) T.v[j][u] = (r < rows && c0 + u < cols) ? M[r * ld + c0 + u] : 0.f;
+    }
+}
+
+// Writes T + (the accumulator tile staged in LDS by acc_to_lds) to M, skipping
+// elements outside rows x cols and columns in [ex0, ex1).
+constexpr int kAccStride = kTile + 4;
+__device__ inline void tile_add_store_rm(float* M, int64_t ld, int64_t rows, int64_t cols,
+                                         int64_t row0, int64_t col0, bool vec4, const TileRM& T,
+                                         const float* accLds, int64_t ex0 = 0, int64_t ex1 = 0)
+{
+    const int t = threadIdx.x;
+    const int lr = t >> 5, lc = 4 * (t & 31);
+    const int64_t r0 = row0 + lr, c0 = col0 + lc;
+    if (vec4 && row0 + kTile <= rows && col0 + kTile <= cols &&
+        (ex1 <= col0 || ex0 >= col0 + kTile)) {
+        float* base = M + r0 * ld + c0;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const f32x4 a = *reinterpret_cast<const f32x4*>(accLds + (lr + 8 * j) * kAccStride + lc);
+            *reinterpret_cast<f32x4*>(base + 8 * j * ld) = T.v[j] + a;
+        }
+        return;
+    }
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+        const int64_t r = r0 + 8 * j;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int64_t c = c0 + u;
+            if (r < rows && c < cols && !(c >= ex0 && c < ex1))
+                M[r * ld + c] = T.v[j][u] + accLds[(lr + 8 * j) * kAccStride + lc + u];
+        }
+    }
+}
+
+// Stages the accumulators into LDS as a row-major 128 x 128 tile (row stride
+// kAccStride); needs kTile * kAccStride floats.  Caller synchronises after.
+__device__ inline void acc_to_lds(const f32x16 (&acc)[2][2], float* lds)
+{
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) lds[acc_row(mi, e) * kAccStride + acc_col(ni)] = acc[mi][ni][e];
+}
+
 // Double-buffered K loop: acc += A[row0a.., 0..K) * B[row0b.., 0..K)^T.
-// `lds` must hold kNTLdsFloats floats.  Ends with a barrier.
+// `lds` must hold kNTLdsFloats floats.  Ends with a barrier.  The loop is
+// unrolled by two so that both buffer addresses are compile-time offsets of
+// the LDS array (a runtime-selected buffer pointer degrades to flat accesses,
+// which wait on the outstanding global prefetch).
 template <class OA, class OB>
 __device__ inline void nt_tile(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                int64_t K, float* lds, f32x16 (&acc)[2][2])
 {
-    float* la[2] = {lds, lds + kTile * kLdsStride};
-    float* lb[2] = {lds + 2 * kTile * kLdsStride, lds + 3 * kTile * kLdsStride};
+    float* const la0 = lds;
+    float* const la1 = lds + kTile * kLdsStride;
+    float* const lb0 = lds + 2 * kTile * kLdsStride;
+    float* const lb1 = lds + 3 * kTile * kLdsStride;
     const int64_t nch = cdiv(K, kKC);
     Stage sa, sb;
     A.load(row0a, 0, sa);
     B.load(row0b, 0, sb);
-    A.store(la[0], sa);
-    B.store(lb[0], sb);
+    A.store(la0, sa);
+    B.store(lb0, sb);
     __syncthreads();
-    for (int64_t c = 0; c < nch; ++c) {
-        const int cur = (int)(c & 1);
-        const bool more = c + 1 < nch;
+    for (int64_t c = 0; c < nch; c += 2) {
+        // chunk c in buffer 0, prefetch c + 1 into buffer 1
+        bool more = c + 1 < nch;
         if (more) {
             A.load(row0a, (c + 1) * kKC, sa);
             B.load(row0b, (c + 1) * kKC, sb);
         }
-        mfma_chunk(la[cur], lb[cur], acc);
+        mfma_chunk(la0, lb0, acc);
         if (more) {
-            A.store(la[cur ^ 1], sa);
-            B.store(lb[cur ^ 1], sb);
+            A.store(la1, sa);
+            B.store(lb1, sb);
+        }
+        __syncthreads();
+        if (!more) break;
+        // chunk c + 1 in buffer 1, prefetch c + 2 into buffer 0
+        more = c + 2 < nch;
+        if (more) {
+            A.load(row0a, (c + 2) * kKC, sa);
+            B.load(row0b, (c + 2) * kKC, sb);
+        }
+        mfma_chunk(la1, lb1, acc);
+        if (more) {
+            A.store(la0, sa);
+            B.store(lb0, sb);
         }
         __syncthreads();
     }
