@@ -172,13 +172,15 @@ __device__ __forceinline__ float row_bcast(float v)
     return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x150 + O, 0xF, 0xF, false));
 }
 
-template <int SLOTS>
+// Fetches this lane's entries of Sigma row `row` of the block, from slot FIRST
+// on (float4 granules; earlier slots are no longer needed).
+template <int SLOTS, int FIRST = 0>
 __device__ __forceinline__ void load_srow(float (&dst)[SLOTS], const float* sS, int row, int g)
 {
     const float* src = sS + row * (16 * SLOTS) + g * SLOTS;
     if constexpr (SLOTS % 4 == 0) {
 #pragma unroll
-        for (int q4 = 0; q4 < SLOTS / 4; ++q4) {
+        for (int q4 = FIRST / 4; q4 < SLOTS / 4; ++q4) {
             const f32x4 v = *reinterpret_cast<const f32x4*>(src + 4 * q4);
 #pragma unroll
             for (int u = 0; u < 4; ++u) dst[4 * q4 + u] = v[u];
@@ -200,7 +202,7 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
     constexpr int B = 16 * SLOTS;
     constexpr int M = J / 16, O = J % 16;
     if (!FULL && J >= width) return;                 // uniform across the workgroup
-    if constexpr (J + 2 < B) load_srow<SLOTS>(st.srow[(J + 2) % 3], sS, J + 2, g);
+    if constexpr (J + 2 < B) load_srow<SLOTS, (J + 2) / 16>(st.srow[(J + 2) % 3], sS, J + 2, g);
     // keep the fetch here: the scheduler would otherwise sink it next to its use
     __builtin_amdgcn_sched_barrier(0);
     const float w = st.w[M];
@@ -220,9 +222,10 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
     const bool own = g == O;
     st.w[M] = own ? wn : w;
     st.dl[M] = own ? delta : st.dl[M];
-    // rank-1 update restricted to the block: L_{i,c} += delta_i Sigma_{j,c}
+    // rank-1 update restricted to the block: L_{i,c} += delta_i Sigma_{j,c}.
+    // Slot mm holds columns 16 mm + g; slots below M are finished this block.
 #pragma unroll
-    for (int mm = 0; mm < SLOTS; ++mm) st.L[mm] = fmaf(db, st.srow[J % 3][mm], st.L[mm]);
+    for (int mm = M; mm < SLOTS; ++mm) st.L[mm] = fmaf(db, st.srow[J % 3][mm], st.L[mm]);
 }
 
 template <int SLOTS, bool FULL, int... Js>
@@ -277,45 +280,118 @@ __device__ __forceinline__ void stage_sigma_block(const float* __restrict__ Sigm
     }
 }
 
-// L_{i,J} += D_{i, k0..k0+kw} Sigma_{r0..r0+kw, J} for the workgroup's 16 rows,
-// with D a q x S row-major delta buffer.  Uses sS / sD as staging.
+// L_{i,J} += D_{i, k0..k0+kw} Sigma_{r0..r0+kw, J} for the workgroup's 16 rows
+// (kw <= B), with D a q x S row-major delta buffer.
+//
+// B >= 64: on matrix cores (v_mfma_f32_16x16x4f32, 16 x 16 output tiles; wave
+// w owns block columns [B/4 w, B/4 (w+1))).  A = the 16 delta rows, fetched as
+// float4 straight into registers; B = Sigma_{r0+k, j0+c}, staged in LDS
+// transposed (k contiguous) from rows j0+c of Sigma, which are the same
+// numbers by symmetry.  Both operands use the same k order inside each group
+// of 16 (lane half h covers k = 4h .. 4h+3), which leaves the sum unchanged.
+// The 16 x B result passes through LDS into the panel's register layout.
+// B < 64: a VALU loop over k with Sigma staged in the panel layout.
+constexpr int kTStride = 128 + 4;   // transposed-Sigma LDS row stride (floats)
+
 template <int SLOTS>
 __device__ __forceinline__ void add_block_update(PanelState<SLOTS>& st, const StepArgs& a,
                                                  const float* D, int64_t k0, int kw, int64_t r0,
                                                  int64_t j0, int width, int64_t i0, int lrow,
-                                                 int g, float* sS, float* sD)
+                                                 int g, float* lds)
 {
     constexpr int B = 16 * SLOTS;
-    __syncthreads();                                 // staging buffers free
-    stage_sigma_block<SLOTS>(a.Sigma, a.p, r0, kw, j0, width, a.sig_vec4 != 0, sS);
-    if (kw == B && i0 + 16 <= a.q) {
-        constexpr int PER = (16 * B / 4 + 255) / 256;
-        f32x4 v[PER];
+    if constexpr (SLOTS >= 4) {
+        constexpr int CPW = B / 4;               // block columns per wave
+        constexpr int T = CPW / 16;              // 16-column MFMA tiles per wave
+        constexpr int KG = B / 16;               // k groups of 16
+        const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+        const int r = lane & 15, h = lane >> 4;
+        float* sT = lds;                         // B columns x kTStride
+        __syncthreads();                         // LDS free
+        // Sigma staged transposed: sT[c][k] = Sigma[j0 + c][r0 + k]
+        constexpr int PER = B * (B / 4) / 256;  // float4 per thread
+        constexpr int HALF = PER >= 8 ? PER / 2 : PER;   // in flight at once (register budget)
+        if (kw == B && width == B && a.sig_vec4) {
 #pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const int f = threadIdx.x + 256 * u;
-            if (f < 16 * B / 4)
-                v[u] = *reinterpret_cast<const f32x4*>(D + (i0 + f / (B / 4)) * a.S + k0 +
-                                                       4 * (f % (B / 4)));
-        }
+            for (int u0 = 0; u0 < PER; u0 += HALF) {
+                f32x4 v[HALF];
 #pragma unroll
-        for (int u = 0; u < PER; ++u) {
-            const int f = threadIdx.x + 256 * u;
-            if (f < 16 * B / 4) *reinterpret_cast<f32x4*>(sD + 4 * f) = v[u];
+                for (int u = 0; u < HALF; ++u) {
+                    const int f = threadIdx.x + 256 * (u0 + u);
+                    v[u] = *reinterpret_cast<const f32x4*>(a.Sigma + (j0 + f / (B / 4)) * a.p +
+                                                           r0 + 4 * (f % (B / 4)));
+                }
+#pragma unroll
+                for (int u = 0; u < HALF; ++u) {
+                    const int f = threadIdx.x + 256 * (u0 + u);
+                    *reinterpret_cast<f32x4*>(sT + (f / (B / 4)) * kTStride + 4 * (f % (B / 4))) =
+                        v[u];
+                }
+            }
+        } else {
+            for (int e = threadIdx.x; e < B * B; e += blockDim.x) {
+                const int cc = e / B, k = e % B;
+                sT[cc * kTStride + k] =
+                    (cc < width && k < kw) ? a.Sigma[(j0 + cc) * a.p + r0 + k] : 0.f;
+            }
         }
+        // A fragments: row i0 + r, k = 16 kg + 4h .. +3 (fetched after the Sigma
+        // loads retire, to keep both sets from being live at once)
+        f32x4 av[KG];
+        const int64_t ia = i0 + r;
+        const bool full = kw == B && i0 + 16 <= a.q;
+#pragma unroll
+        for (int kg = 0; kg < KG; ++kg) {
+            const int kk = 16 * kg + 4 * h;
+            if (full) {
+                av[kg] = *reinterpret_cast<const f32x4*>(D + ia * a.S + k0 + kk);
+            } else {
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    av[kg][u] = (ia < a.q && kk + u < kw) ? D[ia * a.S + k0 + kk + u] : 0.f;
+            }
+        }
+        __syncthreads();
+        f32x4 acc[T];
+#pragma unroll
+        for (int t = 0; t < T; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kg = 0; kg < KG; ++kg) {
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+                const f32x4 bv = *reinterpret_cast<const f32x4*>(
+                    sT + (CPW * wave + 16 * t + r) * kTStride + 16 * kg + 4 * h);
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[kg][u], bv[u], acc[t], 0, 0, 0);
+            }
+        }
+        __syncthreads();                         // sT consumed; reuse as the result tile
+        float* sC = lds;                         // 16 x B
+        // 16 x 16 output: lane holds rows 4 (lane / 16) + v, column lane % 16
+#pragma unroll
+        for (int t = 0; t < T; ++t)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) sC[(4 * h + v) * B + CPW * wave + 16 * t + r] = acc[t][v];
+        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < SLOTS; ++m) st.L[m] += sC[lrow * B + 16 * m + g];
     } else {
+        float* sS = lds;            // B x B
+        float* sD = lds + B * B;    // 16 x B
+        __syncthreads();            // staging buffers free
+        stage_sigma_block<SLOTS>(a.Sigma, a.p, r0, kw, j0, width, a.sig_vec4 != 0, sS);
         for (int e = threadIdx.x; e < 16 * B; e += blockDim.x) {
-            const int r = e / B, k = e % B;
-            const int64_t ii = i0 + r;
+            const int rr = e / B, k = e % B;
+            const int64_t ii = i0 + rr;
             sD[e] = (ii < a.q && k < kw) ? D[ii * a.S + k0 + k] : 0.f;
         }
-    }
-    __syncthreads();
-#pragma unroll 8
-    for (int k = 0; k < kw; ++k) {
-        const float dk = sD[lrow * B + k];
+        __syncthreads();
+        for (int k = 0; k < kw; ++k) {
+            const float dk = sD[lrow * B + k];
 #pragma unroll
-        for (int m = 0; m < SLOTS; ++m) st.L[m] = fmaf(dk, sS[k * B + g * SLOTS + m], st.L[m]);
+            for (int m = 0; m < SLOTS; ++m) st.L[m] = fmaf(dk, sS[k * B + g * SLOTS + m], st.L[m]);
+        }
     }
 }
 
@@ -323,8 +399,7 @@ template <int SLOTS>
 __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
 {
     constexpr int B = 16 * SLOTS;
-    float* sS = lds;            // B x B
-    float* sD = lds + B * B;    // 16 x B
+    float* sS = lds;            // B x B: Sigma_{J,J} in the panel layout
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int g = lane & 15;
     const int lrow = wave * 4 + (lane >> 4);
@@ -356,7 +431,7 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
             for (int kc = 0; kc < a.psbw; kc += B) {
                 const int kw = min(B, a.psbw - kc);
                 add_block_update<SLOTS>(st, a, a.dprev, kc, kw, a.psb + kc, j0, width, i0, lrow, g,
-                                        sS, sD);
+                                        lds);
             }
 #pragma unroll
             for (int m = 0; m < SLOTS; ++m) {
@@ -368,7 +443,7 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
         //     written to R: the next launch's GEMM applies the whole super-block)
         for (int sp = 0; sp < sub; ++sp)
             add_block_update<SLOTS>(st, a, a.dcur, (int64_t)sp * B, B, a.sb + (int64_t)sp * B, j0,
-                                    width, i0, lrow, g, sS, sD);
+                                    width, i0, lrow, g, lds);
         // (3) the B column updates in order
         __syncthreads();
         stage_sigma_block<SLOTS>(a.Sigma, p, j0, width, j0, width, a.sig_vec4 != 0, sS);
