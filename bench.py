@@ -14,6 +14,7 @@ reported under "outlier"; the CPU oracle is timed on a bounded sample under
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -25,6 +26,39 @@ sys.path.insert(0, ROOT)
 METRIC = "CD sweep time per layer (s) and column-updates/s at 4096×4096 4-bit"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_c2_4096x4096.md")
+CALIB_COPY_BYTES = 256 << 20
+
+
+def kernel_source_hash():
+    """sha256 over the HIP sources the library is built from (sorted by name)."""
+    import hashlib
+    d = os.path.join(ROOT, "paper_2309_01885_amd", "csrc")
+    h = hashlib.sha256()
+    for name in sorted(os.listdir(d)):
+        if name.endswith((".hip", ".h")):
+            h.update(name.encode())
+            with open(os.path.join(d, name), "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary
+    (copy-calibrated), keyed by kernel; empty when the summary is missing or
+    was taken on other kernel sources."""
+    try:
+        with open(TRAFFIC_PROFILE) as f:
+            text = f.read()
+    except OSError:
+        return {}
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    if not m:
+        return {}
+    data = json.loads(m.group(1))
+    if data.get("source_sha256") != kernel_source_hash():
+        return {}
+    return {k: v["hbm_bytes_per_launch"] for k, v in data["kernels"].items()}
 
 
 def log(msg):
@@ -63,6 +97,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-outlier", action="store_true", help="skip the outlier-aware timing")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="end with a plain 256 MiB device copy (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: --gpus {args.gpus} is not supported "
@@ -166,13 +202,16 @@ def main():
     gram_flops = float(p) * (p + 1) * n
     gram_tflops = gram_flops / gram_t / 1e12
     sweep_t = float(np.median(phase["cd"])) / sweeps
+    traffic = measured_traffic()
     roof_cd = {"kernel": "cd_step_kernel<8>", "bound": "mfma", "achieved": cd_tflops,
                "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-               "frac": cd_tflops / FP32_MFMA_PEAK_TFLOPS, "traffic": None,
+               "frac": cd_tflops / FP32_MFMA_PEAK_TFLOPS,
+               "traffic": traffic.get("cd_step_kernel"),
                "avg_launch_s": cd_avg, "flops_per_launch": cd_flops_per_launch}
-    roof_gram = {"kernel": "gram_kernel<false>", "bound": "mfma", "achieved": gram_tflops,
+    roof_gram = {"kernel": "gram_kernel", "bound": "mfma", "achieved": gram_tflops,
                  "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                 "frac": gram_tflops / FP32_MFMA_PEAK_TFLOPS, "traffic": None,
+                 "frac": gram_tflops / FP32_MFMA_PEAK_TFLOPS,
+                 "traffic": traffic.get("gram_kernel"),
                  "call_s": gram_t, "flops_per_call": gram_flops}
     dominant = roof_gram if gram_t > sweeps * sweep_t else roof_cd
 
@@ -211,6 +250,11 @@ def main():
         log("CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(spec, X_head, W_h, scale.cpu().numpy(),
                                               zero.cpu().numpy(), sweeps)
+    if args.calib_copy:
+        a = torch.ones(CALIB_COPY_BYTES // 4, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
     print(json.dumps(result), flush=True)
 
 
