@@ -30,23 +30,30 @@ TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_c2_4096x4096.md")
 CALIB_COPY_BYTES = 256 << 20
 
 
-def kernel_source_hash():
-    """sha256 over the HIP sources the library is built from (sorted by name)."""
+# HIP sources each measured kernel is compiled from
+KERNEL_SOURCES = {
+    "gram_kernel": ["gram.hip", "qe_internal.h"],
+    "cd_step_kernel": ["cd.hip", "qe_internal.h"],
+}
+
+
+def kernel_source_hash(kernel):
+    """sha256 over the HIP sources `kernel` is compiled from (and the ABI header)."""
     import hashlib
-    d = os.path.join(ROOT, "paper_2309_01885_amd", "csrc")
     h = hashlib.sha256()
-    for name in sorted(os.listdir(d)):
-        if name.endswith((".hip", ".h")):
-            h.update(name.encode())
-            with open(os.path.join(d, name), "rb") as f:
-                h.update(f.read())
+    files = [os.path.join(ROOT, "paper_2309_01885_amd", "csrc", f) for f in KERNEL_SOURCES[kernel]]
+    files.append(os.path.join(ROOT, "include", "qe.h"))
+    for path in files:
+        h.update(os.path.basename(path).encode())
+        with open(path, "rb") as f:
+            h.update(f.read())
     return h.hexdigest()
 
 
 def measured_traffic():
     """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary
-    (copy-calibrated), keyed by kernel; empty when the summary is missing or
-    was taken on other kernel sources."""
+    (copy-calibrated), keyed by kernel; a kernel is left out when its sources
+    changed since the counters were taken."""
     try:
         with open(TRAFFIC_PROFILE) as f:
             text = f.read()
@@ -56,38 +63,8 @@ def measured_traffic():
     if not m:
         return {}
     data = json.loads(m.group(1))
-    if data.get("source_sha256") != kernel_source_hash():
-        return {}
-    return {k: v["hbm_bytes_per_launch"] for k, v in data["kernels"].items()}
-
-
-def log(msg):
-    print(f"[bench] {msg}", file=sys.stderr, flush=True)
-
-
-def cpu_baseline(spec, X_head, W, scale, zero, sweeps):
-    """The oracle as it stands on the host cores, on a bounded sample of the
-    same step: Gram on the first n' tokens (scaled by n/n'), one CD sweep on r
-    seeded rows (scaled by q/r rows and by the sweep count)."""
-    import oracle
-    q, p, n = spec.q, spec.p, spec.n
-    n_s = X_head.shape[1]
-    t0 = time.perf_counter()
-    S = oracle.damp(oracle.gram(X_head), spec.damp)
-    t_gram = time.perf_counter() - t0
-    rows = __import__("synth").row_sample(q, 256, spec.cfg)
-    t_sweep = oracle.cd_sweep_timed(W[rows], S, spec.bits, scale[rows], zero[rows])
-    t_step = t_gram * (n / n_s) + t_sweep * (q / len(rows)) * sweeps
-    return {
-        "value": p * sweeps / t_step,
-        "unit": "column-updates/s",
-        "cores": oracle.num_threads(),
-        "kind": "oracle",
-        "sample": (f"Gram over {n_s} of {n} tokens (x{n / n_s:.0f}), one Lemma-1 sweep over "
-                   f"{len(rows)} of {q} rows (x{q / len(rows):.0f} rows, x{sweeps} sweeps); "
-                   f"measured {t_gram:.2f} s + {t_sweep:.2f} s"),
-        "step_s_extrapolated": t_step,
-    }
+    return {k: v["hbm_bytes_per_launch"] for k, v in data["kernels"].items()
+            if k in KERNEL_SOURCES and v.get("source_sha256") == kernel_source_hash(k)}
 
 
 def main():

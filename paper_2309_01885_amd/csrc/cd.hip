@@ -103,14 +103,32 @@ __global__ __launch_bounds__(256) void obj_partial_kernel(const float* __restric
                                                           const float* __restrict__ Wh,
                                                           const float* __restrict__ H,
                                                           const float* __restrict__ R,
-                                                          int64_t count, double* partial,
+                                                          int64_t count, int vec4, double* partial,
                                                           const int* status)
 {
     if (failed(status)) return;
     __shared__ double sh[256];
     double acc = 0.0;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < count;
-         e += (int64_t)gridDim.x * blockDim.x) {
+    const int64_t G = (int64_t)gridDim.x * blockDim.x;
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t tail = 0;
+    if (vec4) {
+        const int64_t n4 = count / 4;
+        const f32x4* W4 = reinterpret_cast<const f32x4*>(W);
+        const f32x4* Wh4 = reinterpret_cast<const f32x4*>(Wh);
+        const f32x4* H4 = reinterpret_cast<const f32x4*>(H);
+        const f32x4* R4 = reinterpret_cast<const f32x4*>(R);
+#pragma unroll 2
+        for (int64_t e = tid; e < n4; e += G) {
+            const f32x4 w = W4[e], wh = Wh4[e], r = R4[e];
+            f32x4 d = wh - w;
+            if (H) d = (wh + H4[e]) - w;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc += (double)d[u] * (double)r[u];
+        }
+        tail = n4 * 4;
+    }
+    for (int64_t e = tail + tid; e < count; e += G) {
         float d = Wh[e] - W[e];
         if (H) d = (Wh[e] + H[e]) - W[e];
         acc += (double)d * (double)R[e];
@@ -532,8 +550,9 @@ qe_status launch_residual_dot(const float* W, const float* Wh, const float* H, c
                               int64_t count, double* out, double* part, const int* status,
                               hipStream_t s)
 {
+    const int vec4 = aligned16(W) && aligned16(Wh) && aligned16(R) && (!H || aligned16(H));
     hipLaunchKernelGGL(obj_partial_kernel, dim3(kObjBlocks), dim3(256), 0, s, W, Wh, H, R, count,
-                       part, status);
+                       vec4, part, status);
     hipLaunchKernelGGL(sum_partials_kernel, dim3(1), dim3(256), 0, s, part, kObjBlocks, out,
                        status);
     return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;

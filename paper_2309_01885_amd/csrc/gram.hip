@@ -35,19 +35,20 @@ __device__ inline void tri_index(int64_t t, int64_t nt, int64_t& ti, int64_t& tj
     tj = r + (t - start(r));
 }
 
-// Writes the 128 x 128 tile held in LDS (row stride kTStride) to Sigma's
-// upper block (ti, tj) and its mirror (tj, ti).  On a diagonal tile only the
-// entries with row <= col are taken and the rest mirrored, so Sigma is
-// exactly symmetric.  With `accumulate`, the old upper value is added first.
+// Writes rows [r0, r0 + nr) of the 128 x 128 tile (held in LDS as rows
+// 0 .. nr-1, row stride kTStride) to Sigma's upper block (ti, tj) and their
+// mirror in block (tj, ti).  On a diagonal tile only the entries with
+// row <= col are taken and the rest mirrored, so Sigma is exactly symmetric.
+// With `accumulate`, the old upper value is added first.
 __device__ void write_symmetric(float* tileLds, int64_t ti, int64_t tj, float* Sigma, int64_t p,
-                                int accumulate)
+                                int accumulate, int r0, int nr)
 {
-    const int64_t a0 = ti * kTile, b0 = tj * kTile;
+    const int64_t a0 = ti * kTile + r0, b0 = tj * kTile;
     const bool diag = ti == tj;
-    for (int e = threadIdx.x; e < kTileFloats; e += blockDim.x) {
+    for (int e = threadIdx.x; e < nr * kTile; e += blockDim.x) {
         const int r = e / kTile, c = e % kTile;
         const int64_t a = a0 + r, b = b0 + c;
-        if (a < p && b < p && (!diag || r <= c)) {
+        if (a < p && b < p && (!diag || r0 + r <= c)) {
             float v = tileLds[r * kTStride + c];
             if (accumulate) v += Sigma[a * p + b];
             Sigma[a * p + b] = v;
@@ -55,10 +56,10 @@ __device__ void write_symmetric(float* tileLds, int64_t ti, int64_t tj, float* S
         }
     }
     __syncthreads();
-    for (int e = threadIdx.x; e < kTileFloats; e += blockDim.x) {
-        const int c = e / kTile, r = e % kTile;      // consecutive threads: consecutive a
+    for (int e = threadIdx.x; e < nr * kTile; e += blockDim.x) {
+        const int c = e / nr, r = e % nr;            // consecutive threads: consecutive a
         const int64_t a = a0 + r, b = b0 + c;
-        if (a < p && b < p && (!diag || r < c)) Sigma[b * p + a] = tileLds[r * kTStride + c];
+        if (a < p && b < p && (!diag || r0 + r < c)) Sigma[b * p + a] = tileLds[r * kTStride + c];
     }
 }
 
@@ -106,7 +107,7 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_kernel(
                 for (int v = 0; v < 16; ++v)
                     tl[acc_row(mi, v) * kTStride + acc_col(ni)] = outer[mi][ni][v];
         __syncthreads();
-        write_symmetric(tl, ti, tj, out, p, accumulate);
+        write_symmetric(tl, ti, tj, out, p, accumulate, 0, kTile);
     } else {
         zero_acc(acc);
         run(k0, k1);
@@ -122,23 +123,44 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_kernel(
 }
 
 // Adds the split partial tiles in fixed split order (fp64) and writes Sigma.
+// Workgroup (tile, quarter): rows [32 quarter, 32 quarter + 32) of the tile,
+// one float4 column group per thread and pass, all splits in flight.
+constexpr int kFinRows = 32;
+
 __global__ __launch_bounds__(256) void gram_finalize_kernel(const float* __restrict__ parts,
                                                             int64_t ntiles, int splits,
                                                             int64_t nt, float* Sigma, int64_t p,
                                                             int accumulate, const int* status)
 {
     if (failed(status)) return;
-    __shared__ float tl[kTile * kTStride];
+    __shared__ float tl[kFinRows * kTStride];
     int64_t ti, tj;
     tri_index(blockIdx.x, nt, ti, tj);
-    for (int e = threadIdx.x; e < kTileFloats; e += blockDim.x) {
-        double s = 0.0;
-        for (int sp = 0; sp < splits; ++sp)
-            s += (double)parts[((int64_t)sp * ntiles + blockIdx.x) * kTileFloats + e];
-        tl[(e / kTile) * kTStride + (e % kTile)] = (float)s;
+    const int r0 = (int)blockIdx.y * kFinRows;
+    const float* src0 = parts + (int64_t)blockIdx.x * kTileFloats + r0 * kTile;
+    const int64_t sstride = ntiles * kTileFloats;
+#pragma unroll
+    for (int u = 0; u < kFinRows * kTile / 4 / 256; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int r = f / (kTile / 4), c = 4 * (f % (kTile / 4));
+        const float* src = src0 + r * kTile + c;
+        double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+#pragma unroll 4
+        for (int sp = 0; sp < splits; ++sp) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(src + sp * sstride);
+            s0 += (double)v[0];
+            s1 += (double)v[1];
+            s2 += (double)v[2];
+            s3 += (double)v[3];
+        }
+        float* d = tl + r * kTStride + c;
+        d[0] = (float)s0;
+        d[1] = (float)s1;
+        d[2] = (float)s2;
+        d[3] = (float)s3;
     }
     __syncthreads();
-    write_symmetric(tl, ti, tj, Sigma, p, accumulate);
+    write_symmetric(tl, ti, tj, Sigma, p, accumulate, r0, kFinRows);
 }
 
 // Sigma_jj += damp * mean_j(Sigma_jj): one workgroup, fp64 mean.
@@ -205,7 +227,7 @@ qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* S
             hipLaunchKernelGGL((gram_kernel<false, false>), grid, dim3(256), 0, s, X, p, n, nt,
                                split_len, parts, accumulate, x_vec4, status);
         if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
-        hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)tiles), dim3(256), 0, s, parts,
+        hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)tiles, kTile / kFinRows), dim3(256), 0, s, parts,
                            tiles, (int)used, nt, Sigma, p, accumulate, status);
     }
     if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;

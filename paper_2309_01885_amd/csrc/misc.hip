@@ -131,72 +131,125 @@ qe_status launch_objective(const float* W, const float* Wh, const float* H, cons
 }
 
 // ---------------------------------------------------------------- lambda_max
-// Power method (Sec. 5.3): y = Sigma v (one wavefront per row), then
-// v <- y / ||y||, lambda = v^T Sigma v (Rayleigh quotient of the unit v).
-__global__ __launch_bounds__(256) void fill_kernel(float* v, int64_t n, float val)
+// Power method (Sec. 5.3): v_k = y_{k-1} / ||y_{k-1}|| (v_0 = 1/sqrt(p)),
+// y_k = Sigma v_k, lambda_k = v_k . y_k (Rayleigh quotient of the unit v_k).
+// One kernel per iteration: every workgroup first forms 1/||y_{k-1}|| from the
+// previous iteration's per-workgroup partials (same fixed-order sum in every
+// workgroup), then 4 rows of y_k (one per wavefront, fp64 dot products over
+// float4 loads of Sigma), and writes its partials of ||y_k||^2 and v_k . y_k.
+// Workgroup 0 also records lambda_{k-1}.
+constexpr int kSymvRows = 4;
+constexpr int kLambdaCheck = 8;
+
+__device__ inline void sum_pair_partials(const double* part, int n, double* sh, double& yy,
+                                         double& vy)
 {
-    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (e < n) v[e] = val;
+    double a = 0.0, b = 0.0;
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+        a += part[2 * e];
+        b += part[2 * e + 1];
+    }
+    yy = block_sum_f64(a, sh);
+    vy = block_sum_f64(b, sh);
 }
 
-__global__ __launch_bounds__(256) void symv_kernel(const float* __restrict__ Sigma, int64_t p,
-                                                   const float* __restrict__ v, float* y)
-{
-    const int lane = threadIdx.x & 63;
-    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (row >= p) return;
-    const float* srow = Sigma + row * p;
-    double acc = 0.0;
-    for (int64_t j = lane; j < p; j += 64) acc += (double)srow[j] * (double)v[j];
-    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-    if (lane == 0) y[row] = (float)acc;
-}
-
-__global__ __launch_bounds__(256) void power_normalize_kernel(const float* y, const float* v,
-                                                              int64_t p, float* vout,
-                                                              double* lam_hist, int it)
+__global__ __launch_bounds__(256) void power_step_kernel(const float* __restrict__ Sigma,
+                                                         int64_t p, const float* __restrict__ yprev,
+                                                         const double* __restrict__ pprev,
+                                                         int first, int vec4, float* y,
+                                                         double* part, double* lam_hist, int slot)
 {
     __shared__ double sh[256];
-    double yy = 0.0, vy = 0.0;
-    for (int64_t j = threadIdx.x; j < p; j += blockDim.x) {
-        yy += (double)y[j] * (double)y[j];
-        vy += (double)v[j] * (double)y[j];
+    __shared__ double wpart[4][2];
+    const int nwg = (int)gridDim.x;
+    double inv = 0.0;
+    if (first) {
+        inv = 1.0;
+    } else {
+        double yy, vy;
+        sum_pair_partials(pprev, nwg, sh, yy, vy);
+        inv = yy > 0.0 ? 1.0 / sqrt(yy) : 0.0;
+        if (blockIdx.x == 0 && threadIdx.x == 0 && slot > 0) lam_hist[slot - 1] = vy;
     }
-    const double nrm2 = block_sum_f64(yy, sh);
-    const double rq = block_sum_f64(vy, sh);
-    const double inv = nrm2 > 0.0 ? 1.0 / sqrt(nrm2) : 0.0;
-    for (int64_t j = threadIdx.x; j < p; j += blockDim.x) vout[j] = (float)((double)y[j] * inv);
-    if (threadIdx.x == 0) lam_hist[it] = rq;
+    const float v0 = (float)(1.0 / sqrt((double)p));
+    auto vj = [&](int64_t j) -> float {
+        return first ? v0 : (float)((double)yprev[j] * inv);
+    };
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    double pyy = 0.0, pvy = 0.0;
+    for (int rr = 0; rr < kSymvRows / 4; ++rr) {
+        const int64_t row = (int64_t)blockIdx.x * kSymvRows + wave * (kSymvRows / 4) + rr;
+        if (row >= p) break;
+        const float* srow = Sigma + row * p;
+        double acc = 0.0;
+        int64_t tail = 0;
+        if (vec4) {
+            const int64_t n4 = p / 4;
+#pragma unroll 8
+            for (int64_t f = lane; f < n4; f += 64) {
+                const f32x4 sv = *reinterpret_cast<const f32x4*>(srow + 4 * f);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) acc += (double)sv[u] * (double)vj(4 * f + u);
+            }
+            tail = 4 * n4;
+        }
+        for (int64_t j = tail + lane; j < p; j += 64) acc += (double)srow[j] * (double)vj(j);
+        for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+        const float yr = (float)acc;
+        if (lane == 0) y[row] = yr;
+        pyy += (double)yr * (double)yr;
+        pvy += (double)vj(row) * (double)yr;
+    }
+    if (lane == 0) {
+        wpart[wave][0] = pyy;
+        wpart[wave][1] = pvy;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        part[2 * blockIdx.x] = ((wpart[0][0] + wpart[1][0]) + wpart[2][0]) + wpart[3][0];
+        part[2 * blockIdx.x + 1] = ((wpart[0][1] + wpart[1][1]) + wpart[2][1]) + wpart[3][1];
+    }
 }
 
-constexpr int kLambdaCheck = 8;
+// lambda of the last iteration of a batch.
+__global__ __launch_bounds__(256) void power_last_kernel(const double* part, int nwg,
+                                                         double* lam_hist, int slot)
+{
+    __shared__ double sh[256];
+    double yy, vy;
+    sum_pair_partials(part, nwg, sh, yy, vy);
+    if (threadIdx.x == 0) lam_hist[slot] = vy;
+}
 
 size_t lambda_ws_bytes(int64_t p)
 {
-    return kStatusBytes + 3 * align256(sizeof(float) * p) + align256(sizeof(double) * kLambdaCheck);
+    const int64_t nwg = cdiv(p, kSymvRows);
+    return kStatusBytes + 2 * align256(sizeof(float) * p) +
+           2 * align256(sizeof(double) * 2 * nwg) + align256(sizeof(double) * kLambdaCheck);
 }
 
 qe_status launch_lambda(const float* Sigma, int64_t p, int max_iters, float tol, float* out,
                         void* ws, hipStream_t s)
 {
     Ws w(ws);
-    float* v = w.take<float>(p);
-    float* y = w.take<float>(p);
-    float* v2 = w.take<float>(p);
+    const int64_t nwg = cdiv(p, kSymvRows);
+    float* y[2] = {w.take<float>(p), w.take<float>(p)};
+    double* part[2] = {w.take<double>(2 * nwg), w.take<double>(2 * nwg)};
     double* hist = w.take<double>(kLambdaCheck);
-    hipLaunchKernelGGL(fill_kernel, dim3((unsigned)cdiv(p, 256)), dim3(256), 0, s, v, p,
-                       (float)(1.0 / sqrt((double)p)));
+    const int vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
     double last = 0.0, prev = 0.0;
-    int it = 0;
+    int it = 0, cur = 0;
     while (it < max_iters) {
         const int batch = std::min(kLambdaCheck, max_iters - it);
         for (int b = 0; b < batch; ++b) {
-            hipLaunchKernelGGL(symv_kernel, dim3((unsigned)cdiv(p, 4)), dim3(256), 0, s, Sigma, p,
-                               v, y);
-            hipLaunchKernelGGL(power_normalize_kernel, dim3(1), dim3(256), 0, s, y, v, p, v2, hist,
-                               b);
-            std::swap(v, v2);
+            const int nxt = cur ^ 1;
+            hipLaunchKernelGGL(power_step_kernel, dim3((unsigned)nwg), dim3(256), 0, s, Sigma, p,
+                               y[cur], part[cur], it + b == 0 ? 1 : 0, vec4, y[nxt], part[nxt],
+                               hist, b);
+            cur = nxt;
         }
+        hipLaunchKernelGGL(power_last_kernel, dim3(1), dim3(256), 0, s, part[cur], (int)nwg, hist,
+                           batch - 1);
         it += batch;
         if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
         double h[kLambdaCheck];

@@ -11,7 +11,11 @@
 // wavefront ballots inside each workgroup), so the support comes out sorted.
 //
 // IHT step (Sec. 5.3, Lemma 3): V = H - E / lambda_max, H+ = P_s(V), then
-// E += (H+ - H) Sigma, gathered per row from the old and new supports.
+// E += (H+ - H) Sigma.  The old and new supports are merged into one list
+// sorted by linear index (an entry in both carries new - old); the sparse
+// product walks each row's stretch of that list in ascending index.
+#include <utility>
+
 #include "qe_internal.h"
 
 namespace qe {
@@ -46,24 +50,40 @@ __global__ void sel_init_kernel(SelState* st, int64_t k, uint32_t* hist, const i
 
 // Histogram of digit (key >> shift) & dmask over the keys whose higher bits
 // (key >> (shift + dbits)) equal the current prefix (pass 0: all keys).
+__device__ inline void hist_key(uint32_t* h, uint32_t key, uint32_t prefix, int shift, int hs,
+                                uint32_t dmask, bool first)
+{
+    if (first || (key >> hs) == prefix) atomicAdd(&h[(key >> shift) & dmask], 1u);
+}
+
 __global__ __launch_bounds__(256) void sel_hist_kernel(const float* __restrict__ V, int64_t count,
                                                        int shift, int dbits, int first,
-                                                       const SelState* st, uint32_t* hist,
-                                                       const int* status)
+                                                       int vec4, const SelState* st,
+                                                       uint32_t* hist, const int* status)
 {
     if (failed(status)) return;
     __shared__ uint32_t h[kHistBins];
     for (int b = threadIdx.x; b < kHistBins; b += blockDim.x) h[b] = 0u;
     __syncthreads();
-    const uint32_t prefix = st->prefix;
+    const uint32_t prefix = first ? 0u : st->prefix;
     const uint32_t dmask = (1u << dbits) - 1u;
     const int hs = shift + dbits;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < count;
-         e += (int64_t)gridDim.x * blockDim.x) {
-        const uint32_t key = abs_key(V[e]);
-        if (!first && (key >> hs) != prefix) continue;
-        atomicAdd(&h[(key >> shift) & dmask], 1u);
+    const int64_t G = (int64_t)gridDim.x * blockDim.x;
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t tail = 0;
+    if (vec4) {
+        const int64_t n4 = count / 4;
+        const f32x4* V4 = reinterpret_cast<const f32x4*>(V);
+#pragma unroll 4
+        for (int64_t e = tid; e < n4; e += G) {
+            const f32x4 v = V4[e];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) hist_key(h, abs_key(v[u]), prefix, shift, hs, dmask, first);
+        }
+        tail = n4 * 4;
     }
+    for (int64_t e = tail + tid; e < count; e += G)
+        hist_key(h, abs_key(V[e]), prefix, shift, hs, dmask, first);
     __syncthreads();
     for (int b = threadIdx.x; b < kHistBins; b += blockDim.x)
         if (h[b]) atomicAdd(&hist[b], h[b]);
@@ -141,23 +161,56 @@ __global__ __launch_bounds__(256) void sel_count_kernel(const float* __restrict_
     }
 }
 
-// Output offset and admitted tie count of every workgroup (sequential scan).
-__global__ void sel_scan_kernel(const int64_t* cnt, int nw, int64_t cap, SelState* st,
-                                int64_t* off, int64_t* adm, int64_t* nnz_out, const int* status)
+// Output offset and admitted tie count of every workgroup.  Ties are admitted
+// greedily in workgroup order: with exclusive prefix sums GT_w, EQ_w and
+// need = #ties to admit, workgroup w admits min(eq_w, max(0, need - EQ_w))
+// ties and writes from GT_w + min(EQ_w, need).  One 256-thread workgroup,
+// kSelWgs / 256 counts per thread, exact int64 scans.
+constexpr int kScanPer = kSelWgs / 256;
+
+__global__ __launch_bounds__(256) void sel_scan_kernel(const int64_t* cnt, int64_t cap,
+                                                       SelState* st, int64_t* off, int64_t* adm,
+                                                       int64_t* nnz_out, const int* status)
 {
     if (failed(status)) return;
-    if (threadIdx.x != 0) return;
-    int64_t need = st->need_eq, pos = 0;
-    for (int w = 0; w < nw; ++w) {
-        const int64_t take = need < cnt[2 * w + 1] ? need : cnt[2 * w + 1];
-        off[w] = pos;
-        adm[w] = take;
-        pos += cnt[2 * w] + take;
-        need -= take;
+    __shared__ int64_t sg[256], se[256];
+    const int t = threadIdx.x;
+    int64_t g[kScanPer], q[kScanPer], lg = 0, le = 0;
+#pragma unroll
+    for (int u = 0; u < kScanPer; ++u) {
+        g[u] = cnt[2 * (t * kScanPer + u)];
+        q[u] = cnt[2 * (t * kScanPer + u) + 1];
+        lg += g[u];
+        le += q[u];
     }
-    if (pos > cap) pos = cap;   // never more than k <= cap by construction; guards the buffers
-    st->nnz = pos;
-    if (nnz_out) *nnz_out = pos;
+    sg[t] = lg;
+    se[t] = le;
+    __syncthreads();
+    // inclusive Hillis-Steele scan over the 256 thread totals
+    for (int d = 1; d < 256; d <<= 1) {
+        const int64_t ag = t >= d ? sg[t - d] : 0, ae = t >= d ? se[t - d] : 0;
+        __syncthreads();
+        sg[t] += ag;
+        se[t] += ae;
+        __syncthreads();
+    }
+    const int64_t need = st->need_eq;
+    int64_t pg = sg[t] - lg, pe = se[t] - le;   // exclusive prefixes of this thread's first count
+#pragma unroll
+    for (int u = 0; u < kScanPer; ++u) {
+        const int w = t * kScanPer + u;
+        const int64_t room = need - pe > 0 ? need - pe : 0;
+        off[w] = pg + (pe < need ? pe : need);
+        adm[w] = q[u] < room ? q[u] : room;
+        pg += g[u];
+        pe += q[u];
+    }
+    if (t == 255) {
+        int64_t pos = sg[255] + (se[255] < need ? se[255] : need);
+        if (pos > cap) pos = cap;   // never more than k <= cap by construction; guards the buffers
+        st->nnz = pos;
+        if (nnz_out) *nnz_out = pos;
+    }
 }
 
 // Writes the selected indices (ascending) and values, and the dense P_s(V).
@@ -211,28 +264,38 @@ __global__ __launch_bounds__(256) void sel_write_kernel(const float* __restrict_
 }
 
 // Radix select + compaction over `count` values.  idx/val receive the
-// support (val may be null); dense (may be null) receives P_s(V).
+// support (val may be null); dense (may be null) receives P_s(V).  With
+// `hist0_done`, the first-digit histogram was already accumulated into
+// `hist` (by the kernel that produced V) after sel_init_kernel cleared it.
+static void select_init(SelState* st, int64_t k, uint32_t* hist, const int* status, hipStream_t hs)
+{
+    hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, hs, st, k, hist, status);
+}
+
 static qe_status run_select(const float* V, int64_t count, int64_t s, SelState* st,
                             uint32_t* hist, int64_t* cnt, int64_t* off, int64_t* adm,
                             int64_t* idx, float* val, float* dense, int64_t* nnz_out,
-                            const int* status, hipStream_t hs)
+                            const int* status, hipStream_t hs, bool hist0_done = false)
 {
     const int64_t k = s < count ? s : count;
-    hipLaunchKernelGGL(sel_init_kernel, dim3(1), dim3(256), 0, hs, st, k, hist, status);
+    if (!hist0_done) select_init(st, k, hist, status, hs);
     const int shifts[3] = {21, 10, 0};
     const int bits[3] = {11, 11, 10};
-    const int hist_wgs = (int)std::min<int64_t>(kSelWgs, std::max<int64_t>(1, cdiv(count, 256)));
+    const int hist_wgs = (int)std::min<int64_t>(kSelWgs, std::max<int64_t>(1, cdiv(count, 1024)));
+    const int vec4 = aligned16(V) ? 1 : 0;
     for (int pass = 0; pass < 3; ++pass) {
-        hipLaunchKernelGGL(sel_hist_kernel, dim3(hist_wgs), dim3(256), 0, hs, V, count,
-                           shifts[pass], bits[pass], pass == 0 ? 1 : 0, st, hist, status);
+        if (pass > 0 || !hist0_done)
+            hipLaunchKernelGGL(sel_hist_kernel, dim3(hist_wgs), dim3(256), 0, hs, V, count,
+                               shifts[pass], bits[pass], pass == 0 ? 1 : 0, vec4, st, hist,
+                               status);
         hipLaunchKernelGGL(sel_pick_kernel, dim3(1), dim3(256), 0, hs, st, hist, bits[pass],
                            pass == 2 ? 1 : 0, status);
     }
     const int64_t chunk = cdiv(count, kSelWgs);
     hipLaunchKernelGGL(sel_count_kernel, dim3(kSelWgs), dim3(256), 0, hs, V, count, chunk, st, cnt,
                        status);
-    hipLaunchKernelGGL(sel_scan_kernel, dim3(1), dim3(64), 0, hs, cnt, kSelWgs, k, st, off, adm,
-                       nnz_out, status);
+    hipLaunchKernelGGL(sel_scan_kernel, dim3(1), dim3(256), 0, hs, cnt, k, st, off, adm, nnz_out,
+                       status);
     hipLaunchKernelGGL(sel_write_kernel, dim3(kSelWgs), dim3(256), 0, hs, V, count, chunk, st, off,
                        adm, k, idx, val, dense, status);
     return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
@@ -294,14 +357,47 @@ qe_status launch_topk(const float* V, int64_t count, int64_t s, float* out, int6
 }
 
 // ---------------------------------------------------------------- IHT step
-// V = H - E / lambda (Sec. 5.3: eta = 1 / (2 lambda_max), gradient 2E).
-__global__ void iht_target_kernel(const float* __restrict__ H, const float* __restrict__ E,
-                                  float lambda, float* V, int64_t n, const int* status)
+// V = H - E / lambda (Sec. 5.3: eta = 1 / (2 lambda_max), gradient 2E), and
+// the first-digit histogram of |V| for the radix select in the same pass.
+__global__ __launch_bounds__(256) void iht_target_kernel(const float* __restrict__ H,
+                                                         const float* __restrict__ E,
+                                                         float lambda, float* V, int64_t n,
+                                                         int vec4, uint32_t* hist,
+                                                         const int* status)
 {
     if (failed(status)) return;
-    for (int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; e < n;
-         e += (int64_t)gridDim.x * blockDim.x)
-        V[e] = H[e] - E[e] / lambda;
+    __shared__ uint32_t h[kHistBins];
+    for (int b = threadIdx.x; b < kHistBins; b += blockDim.x) h[b] = 0u;
+    __syncthreads();
+    const int64_t G = (int64_t)gridDim.x * blockDim.x;
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    int64_t tail = 0;
+    if (vec4) {
+        const int64_t n4 = n / 4;
+        const f32x4* H4 = reinterpret_cast<const f32x4*>(H);
+        const f32x4* E4 = reinterpret_cast<const f32x4*>(E);
+        f32x4* V4 = reinterpret_cast<f32x4*>(V);
+#pragma unroll 2
+        for (int64_t e = tid; e < n4; e += G) {
+            const f32x4 hv = H4[e], ev = E4[e];
+            f32x4 v;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                v[u] = hv[u] - ev[u] / lambda;
+                atomicAdd(&h[abs_key(v[u]) >> 21], 1u);
+            }
+            V4[e] = v;
+        }
+        tail = n4 * 4;
+    }
+    for (int64_t e = tail + tid; e < n; e += G) {
+        const float v = H[e] - E[e] / lambda;
+        atomicAdd(&h[abs_key(v) >> 21], 1u);
+        V[e] = v;
+    }
+    __syncthreads();
+    for (int b = threadIdx.x; b < kHistBins; b += blockDim.x)
+        if (h[b]) atomicAdd(&hist[b], h[b]);
 }
 
 // rowptr[i] = first list position whose linear index is >= i * p (i = 0..q).
@@ -339,57 +435,181 @@ __global__ void gather_kernel(const float* H, const int64_t* idx, int64_t* nnz_p
     if (blockIdx.x == 0 && threadIdx.x == 0) *nnz_p = n;
 }
 
-// E_i += sum_k (Hnew_ik - Hold_ik) Sigma_k,:  over the union of the two sorted
-// supports of row i, in ascending k (a deterministic order).  One workgroup
-// per row; columns in register chunks of 256 x kSpmmPer.
-constexpr int kSpmmPer = 16;
+// Merges the old support (values negated) and the new support into one list
+// sorted by linear index, an old entry before a new one with the same index.
+// Each entry finds its place by one binary search in the other list.
+// Entries [cap, 2 cap) of the thread range stand for the new list.
+__device__ inline int64_t count_below(const int64_t* a, int64_t n, int64_t key, bool inclusive)
+{
+    int64_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (a[mid] < key || (inclusive && a[mid] == key)) lo = mid + 1; else hi = mid;
+    }
+    return lo;
+}
 
-__global__ __launch_bounds__(256) void spmm_delta_kernel(
-    const int64_t* __restrict__ oidx, const float* __restrict__ oval, const int64_t* __restrict__ orp,
-    const int64_t* __restrict__ nidx, const float* __restrict__ nval, const int64_t* __restrict__ nrp,
-    const float* __restrict__ Sigma, int64_t p, float* E, const int* status)
+__global__ __launch_bounds__(256) void merge_supports_kernel(
+    const int64_t* __restrict__ oidx, const float* __restrict__ oval, const int64_t* on_p,
+    const int64_t* __restrict__ nidx, const float* __restrict__ nval, const int64_t* nn_p,
+    int64_t cap, int64_t* midx, float* mval, int64_t* mcount, const int* status)
 {
     if (failed(status)) return;
-    const int64_t i = blockIdx.x;
-    const int64_t o0 = orp[i], o1 = orp[i + 1], n0 = nrp[i], n1 = nrp[i + 1];
-    if (o0 == o1 && n0 == n1) return;
-    const int64_t big = INT64_MAX;
-    for (int64_t cbase = 0; cbase < p; cbase += 256 * kSpmmPer) {
-        float acc[kSpmmPer];
+    const int64_t no = min(max(*on_p, (int64_t)0), cap), nn = min(max(*nn_p, (int64_t)0), cap);
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e == 0) *mcount = no + nn;
+    if (e < cap) {
+        if (e >= no) return;
+        const int64_t k = oidx[e];
+        const int64_t pos = e + count_below(nidx, nn, k, false);
+        midx[pos] = k;
+        mval[pos] = -oval[e];
+    } else if (e < 2 * cap) {
+        const int64_t b = e - cap;
+        if (b >= nn) return;
+        const int64_t k = nidx[b];
+        const int64_t pos = b + count_below(oidx, no, k, true);
+        midx[pos] = k;
+        mval[pos] = nval[b];
+    }
+}
+
+// E_i += sum_k (Hnew_ik - Hold_ik) Sigma_k,:  from the merged list, in
+// ascending k per row (a deterministic order).  Workgroup = 16 rows x 128
+// columns: lanes 16 r .. 16 r + 15 (one DPP row) own row r, 8 columns each.
+// A batch of 16 list entries is fetched one per lane; the first entry of an
+// (old, new) pair carries new - old, its partner 0.  Entries are then taken
+// in order, broadcast with DPP, and each lane applies one Sigma row segment.
+// Workgroups are handed out column block by column block per XCD (8 XCDs
+// take workgroups round-robin), so a 2 MB column slice of Sigma is shared in
+// each XCD's L2 by all row tiles.  Indices outside row i are ignored.
+constexpr int kSpRows = 16;
+constexpr int kSpCols = 128;
+
+template <int O>
+__device__ __forceinline__ int row_bcast_i(int v)
+{
+    return __builtin_amdgcn_mov_dpp(v, 0x150 + O, 0xF, 0xF, false);
+}
+template <int O>
+__device__ __forceinline__ float row_bcast_f(float v)
+{
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x150 + O, 0xF, 0xF, false));
+}
+
+// One batch: the 16 broadcast entries' Sigma segments are fetched first (a
+// row whose entry carries 0 issues no load: its lanes are masked off), then
+// applied in list order.
+template <int... Us>
+__device__ __forceinline__ void spmm_batch(std::integer_sequence<int, Us...>, float (&acc)[8],
+                                           float dd, int col, const float* Sigma, int64_t p,
+                                           int64_t c0, bool full)
+{
+    constexpr int N = sizeof...(Us);
+    const float du[N] = {row_bcast_f<Us>(dd)...};
+    const int cu[N] = {row_bcast_i<Us>(col)...};
+    f32x4 sa[N], sb[N];
 #pragma unroll
-        for (int u = 0; u < kSpmmPer; ++u) {
-            const int64_t c = cbase + u * 256 + threadIdx.x;
-            acc[u] = c < p ? E[i * p + c] : 0.f;
-        }
-        int64_t a = o0, b = n0;
-        while (a < o1 || b < n1) {
-            const int64_t ka = a < o1 ? oidx[a] : big;
-            const int64_t kb = b < n1 ? nidx[b] : big;
-            int64_t k;
-            float d;
-            if (ka < kb) {
-                k = ka;
-                d = -oval[a++];
-            } else if (kb < ka) {
-                k = kb;
-                d = nval[b++];
+    for (int u = 0; u < N; ++u) {
+        sa[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+        sb[u] = sa[u];
+        if (du[u] != 0.f) {
+            const float* src = Sigma + (int64_t)cu[u] * p + c0;
+            if (full) {
+                sa[u] = *reinterpret_cast<const f32x4*>(src);
+                sb[u] = *reinterpret_cast<const f32x4*>(src + 4);
             } else {
-                k = ka;
-                d = nval[b++] - oval[a++];
-            }
-            if (d == 0.f || k < i * p || k >= (i + 1) * p) continue;
-            const float* srow = Sigma + (k - i * p) * p;
 #pragma unroll
-            for (int u = 0; u < kSpmmPer; ++u) {
-                const int64_t c = cbase + u * 256 + threadIdx.x;
-                if (c < p) acc[u] = fmaf(d, srow[c], acc[u]);
+                for (int e = 0; e < 4; ++e) {
+                    sa[u][e] = c0 + e < p ? src[e] : 0.f;
+                    sb[u][e] = c0 + 4 + e < p ? src[4 + e] : 0.f;
+                }
             }
         }
+    }
 #pragma unroll
-        for (int u = 0; u < kSpmmPer; ++u) {
-            const int64_t c = cbase + u * 256 + threadIdx.x;
-            if (c < p) E[i * p + c] = acc[u];
+    for (int u = 0; u < N; ++u) {
+        if (du[u] != 0.f) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                acc[e] = fmaf(du[u], sa[u][e], acc[e]);
+                acc[4 + e] = fmaf(du[u], sb[u][e], acc[4 + e]);
+            }
         }
+    }
+}
+
+__global__ __launch_bounds__(256) void spmm_delta_kernel(const int64_t* __restrict__ midx,
+                                                         const float* __restrict__ mval,
+                                                         const int64_t* __restrict__ mrp,
+                                                         const float* __restrict__ Sigma,
+                                                         int64_t q, int64_t p, int64_t n_rt,
+                                                         int64_t n_cb, int vec4, float* E,
+                                                         const int* status)
+{
+    if (failed(status)) return;
+    const int64_t work = n_rt * n_cb;
+    const int64_t per = cdiv(work, 8);
+    const int64_t w = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (w >= work) return;
+    const int64_t cb = w / n_rt, rt = w % n_rt;
+    const int r = threadIdx.x >> 4, g = threadIdx.x & 15;
+    const int64_t i = rt * kSpRows + r;
+    const int64_t c0 = cb * kSpCols + 8 * g;
+    const bool rowok = i < q;
+    const int64_t m0 = rowok ? mrp[i] : 0, m1 = rowok ? mrp[i + 1] : 0;
+    const int64_t len = m1 > m0 ? m1 - m0 : 0;
+    int64_t wl = len;   // longest stretch among the wave's four rows (wave-uniform)
+#pragma unroll
+    for (int off = 16; off < 64; off <<= 1) {
+        const int64_t o = __shfl_xor(wl, off, 64);
+        wl = o > wl ? o : wl;
+    }
+    if (wl == 0) return;
+    const bool full = vec4 && c0 + 8 <= p;
+    float* erow = E + i * p + c0;
+    float acc[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = (len > 0 && c0 + e < p) ? erow[e] : 0.f;
+    const int64_t rlo = i * p, rhi = rlo + p;
+    // lane g's entry of the batch at `base`: (delta, Sigma row), 0 if none
+    auto fetch = [&](int64_t base, float& dd, int& col) {
+        const int64_t m = m0 + base + g;
+        dd = 0.f;
+        col = 0;
+        if (m < m1) {
+            const int64_t k = midx[m];
+            const float d0 = mval[m];
+            const int64_t kp = m > m0 ? midx[m - 1] : -1;
+            int64_t kn = -1;
+            float d1 = 0.f;
+            if (m + 1 < m1) {
+                kn = midx[m + 1];
+                d1 = mval[m + 1];
+            }
+            const float d = kn == k ? d0 + d1 : d0;
+            if (kp != k && d != 0.f && k >= rlo && k < rhi) {
+                dd = d;
+                col = (int)(k - rlo);
+            }
+        }
+    };
+    float dd, dn = 0.f;
+    int col, cn = 0;
+    fetch(0, dd, col);
+    for (int64_t base = 0; base < wl; base += 16) {
+        if (base + 16 < wl) fetch(base + 16, dn, cn);   // next batch in flight
+        // entries past a row's stretch carry 0
+        spmm_batch(std::make_integer_sequence<int, 8>{}, acc, dd, col, Sigma, p, c0, full);
+        spmm_batch(std::integer_sequence<int, 8, 9, 10, 11, 12, 13, 14, 15>{}, acc, dd, col, Sigma,
+                   p, c0, full);
+        dd = dn;
+        col = cn;
+    }
+    if (len > 0) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+            if (c0 + e < p) erow[e] = acc[e];
     }
 }
 
@@ -400,8 +620,9 @@ size_t outlier_ws_bytes(int64_t q, int64_t p, int block, int64_t s)
     b += align256(sizeof(float) * q * p);                         // V
     b += sel_bytes();
     b += 2 * (align256(sizeof(int64_t) * cap) + align256(sizeof(float) * cap));  // two supports
-    b += 2 * align256(sizeof(int64_t) * (q + 1));                 // row pointers
-    b += 2 * align256(sizeof(int64_t));                           // their sizes
+    b += align256(sizeof(int64_t) * 2 * cap) + align256(sizeof(float) * 2 * cap);  // merged list
+    b += align256(sizeof(int64_t) * (q + 1));                     // its row pointers
+    b += 3 * align256(sizeof(int64_t));                           // list sizes
     b += align256(sizeof(double) * kObjBlocks);                   // objective partials
     return b;
 }
@@ -423,9 +644,16 @@ qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t 
     float* val[2] = {w.take<float>(cap), nullptr};
     idx[1] = w.take<int64_t>(cap);
     val[1] = w.take<float>(cap);
-    int64_t* rp[2] = {w.take<int64_t>(q + 1), w.take<int64_t>(q + 1)};
+    int64_t* midx = w.take<int64_t>(2 * cap);
+    float* mval = w.take<float>(2 * cap);
+    int64_t* mrp = w.take<int64_t>(q + 1);
     int64_t* cnt[2] = {w.take<int64_t>(1), w.take<int64_t>(1)};
+    int64_t* mcount = w.take<int64_t>(1);
     double* opart = w.take<double>(kObjBlocks);
+    const int vec4 = (aligned16(H) && aligned16(E) && aligned16(V)) ? 1 : 0;
+    const int sig_vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
+    const int64_t n_rt = cdiv(q, kSpRows), n_cb = cdiv(p, kSpCols);
+    const int64_t sp_grid = 8 * cdiv(n_rt * n_cb, 8);
 
     // current support = the caller's (e.g. P_s(W) for the initialisation)
     if (hipMemcpyAsync(cnt[0], support_nnz, sizeof(int64_t), hipMemcpyDeviceToDevice, hs) !=
@@ -446,18 +674,19 @@ qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t 
         if (st != QE_OK) return st;
         if (s > 0) {
             const int nxt = cur ^ 1;
+            select_init(sb.st, s < n ? s : n, sb.hist, status, hs);
             hipLaunchKernelGGL(iht_target_kernel, dim3(2048), dim3(256), 0, hs, H, E, lambda, V, n,
-                               status);
+                               vec4, sb.hist, status);
             st = run_select(V, n, s, sb.st, sb.hist, sb.cnt, sb.off, sb.adm, idx[nxt], val[nxt], H,
-                            cnt[nxt], status, hs);
+                            cnt[nxt], status, hs, true);
             if (st != QE_OK) return st;
+            hipLaunchKernelGGL(merge_supports_kernel, dim3((unsigned)cdiv(2 * cap, 256)),
+                               dim3(256), 0, hs, idx[cur], val[cur], cnt[cur], idx[nxt], val[nxt],
+                               cnt[nxt], cap, midx, mval, mcount, status);
             hipLaunchKernelGGL(rowptr_kernel, dim3((unsigned)cdiv(q + 1, 256)), dim3(256), 0, hs,
-                               idx[cur], cnt[cur], q, p, rp[cur], status);
-            hipLaunchKernelGGL(rowptr_kernel, dim3((unsigned)cdiv(q + 1, 256)), dim3(256), 0, hs,
-                               idx[nxt], cnt[nxt], q, p, rp[nxt], status);
-            hipLaunchKernelGGL(spmm_delta_kernel, dim3((unsigned)q), dim3(256), 0, hs, idx[cur],
-                               val[cur], rp[cur], idx[nxt], val[nxt], rp[nxt], Sigma, p, E,
-                               status);
+                               midx, mcount, q, p, mrp, status);
+            hipLaunchKernelGGL(spmm_delta_kernel, dim3((unsigned)sp_grid), dim3(256), 0, hs, midx,
+                               mval, mrp, Sigma, q, p, n_rt, n_cb, sig_vec4, E, status);
             cur = nxt;
         }
         if (obj) {

@@ -15,7 +15,7 @@ constexpr int kKC = 32;               // K chunk staged through LDS per pipeline
 constexpr int kLdsStride = kKC + 4;   // padded LDS row (floats)
 constexpr size_t kStatusBytes = 256;  // status word region at the head of every workspace
 constexpr int kNTLdsFloats = 2 * 2 * kTile * kLdsStride;  // double-buffered A and B chunks
-constexpr int kObjBlocks = 512;       // workgroups of the fp64 residual dot product
+constexpr int kObjBlocks = 1024;      // workgroups of the fp64 residual dot product
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
