@@ -67,6 +67,35 @@ def measured_traffic():
             if k in KERNEL_SOURCES and v.get("source_sha256") == kernel_source_hash(k)}
 
 
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def cpu_baseline(spec, X_head, W, scale, zero, sweeps):
+    """The oracle as it stands on the host cores, on a bounded sample of the
+    same step: Gram on the first n' tokens (scaled by n/n'), one CD sweep on r
+    seeded rows (scaled by q/r rows and by the sweep count)."""
+    import oracle
+    q, p, n = spec.q, spec.p, spec.n
+    n_s = X_head.shape[1]
+    t0 = time.perf_counter()
+    S = oracle.damp(oracle.gram(X_head), spec.damp)
+    t_gram = time.perf_counter() - t0
+    rows = __import__("synth").row_sample(q, 256, spec.cfg)
+    t_sweep = oracle.cd_sweep_timed(W[rows], S, spec.bits, scale[rows], zero[rows])
+    t_step = t_gram * (n / n_s) + t_sweep * (q / len(rows)) * sweeps
+    return {
+        "value": p * sweeps / t_step,
+        "unit": "column-updates/s",
+        "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": (f"Gram over {n_s} of {n} tokens (x{n / n_s:.0f}), one Lemma-1 sweep over "
+                   f"{len(rows)} of {q} rows (x{q / len(rows):.0f} rows, x{sweeps} sweeps); "
+                   f"measured {t_gram:.2f} s + {t_sweep:.2f} s"),
+        "step_s_extrapolated": t_step,
+    }
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)

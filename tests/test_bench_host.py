@@ -1,0 +1,35 @@
+"""Host-side checks of bench.py (no GPU): argument handling and the traffic
+summary reader."""
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_helpers_present():
+    for name in ("log", "cpu_baseline", "outlier_bench", "measured_traffic", "kernel_source_hash",
+                 "main"):
+        assert callable(getattr(bench, name)), name
+
+
+def test_traffic_reader_keys():
+    t = bench.measured_traffic()
+    assert set(t) <= set(bench.KERNEL_SOURCES)
+    assert all(isinstance(v, int) and v > 0 for v in t.values())
+
+
+def test_source_hash_stable():
+    for k in bench.KERNEL_SOURCES:
+        assert bench.kernel_source_hash(k) == bench.kernel_source_hash(k)
+        assert len(bench.kernel_source_hash(k)) == 64
+
+
+def test_more_than_one_gpu_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
