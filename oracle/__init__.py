@@ -308,6 +308,8 @@ class OutlierResult:
     support_hist: List[np.ndarray] = field(default_factory=list)
     codes_hist: List[np.ndarray] = field(default_factory=list)
     margin_hist: List[np.ndarray] = field(default_factory=list)
+    tau: List[float] = field(default_factory=list)      # s-th largest |V| of iteration k
+    V_last: Optional[np.ndarray] = None                 # V of the last IHT step
 
 
 def outlier_init(W, s: int):
@@ -339,8 +341,12 @@ def outlier(W, Sigma, bits: int, scale, zero, s: int, lam: float, sweeps: int,
         Wh, codes = cres.What, cres.codes
         res.g_cd.append(cres.obj[0])
         grad = 2.0 * ((H + Wh - Wd) @ S)
-        sup, H = topk_abs(H - eta * grad, s)
+        V = H - eta * grad
+        sup, H = topk_abs(V, s)
         res.g.append(objective(Wd, Wh, S, H))
+        res.tau.append(float(np.min(np.abs(V.reshape(-1)[sup]))) if len(sup) else 0.0)
+        if it == sweeps - 1:
+            res.V_last = V
         if record:
             res.support_hist.append(sup)
             res.codes_hist.append(codes.copy())

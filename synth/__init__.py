@@ -15,7 +15,15 @@ Seeding: every draw comes from ``numpy.random.Generator(PCG64(SeedSequence(
 [1885, cfg, stream, chunk])))``.  Streams: 0 weight values, 1 weight outlier
 positions, 2 activation outlier channels, 3 activation values (one chunk =
 2048 tokens, so any chunk can be regenerated alone), 4 oracle row sample,
-5 Gram entry sample, 6 free-form test inputs.  Draws are fp64, cast to fp32.
+5 Gram entry sample, 6 free-form test inputs, 7 device-drawn activations.
+Draws are fp64, cast to fp32.
+
+The Falcon-180B-shaped layer needs 59392 x 262144 activations (62 GB); the
+host generator would take the better part of an hour for them, so
+``activation_chunk_device`` draws such chunks on the GPU with torch's seeded
+Philox generator (same t4 law: Z / sqrt(chi2_4 / 4), chi2_4 the sum of four
+squared standard normals).  Tests copy the channels the oracle needs back to
+the host, so both sides still see identical numbers.
 """
 from __future__ import annotations
 
@@ -150,6 +158,32 @@ def activations(spec: LayerSpec, n: Optional[int] = None, p: Optional[int] = Non
         with ThreadPoolExecutor(threads) as ex:
             list(ex.map(fill, range(nchunks)))
     return out
+
+
+def activation_chunk_device(spec: LayerSpec, chunk: int, tokens: int, device,
+                            p: Optional[int] = None):
+    """Chunk `chunk` of a device-drawn X stream (p x tokens, fp32, on
+    `device`): t4 values (or N(0, 1)), outlier channels scaled as in
+    activation_chunk.  Seeded from SeedSequence([1885, cfg, 7, chunk])."""
+    import torch
+    p = spec.p if p is None else p
+    cfg = spec.cfg if spec.x_cfg is None else spec.x_cfg
+    seed = int(np.random.SeedSequence([SEED, cfg, 7, chunk]).generate_state(1, np.uint64)[0])
+    g = torch.Generator(device=device)
+    g.manual_seed(seed & ((1 << 63) - 1))
+    x = torch.randn((p, tokens), generator=g, device=device, dtype=torch.float32)
+    if spec.x_dist == "t4":
+        chi2 = torch.zeros_like(x)
+        for _ in range(4):
+            z = torch.randn((p, tokens), generator=g, device=device, dtype=torch.float32)
+            chi2.addcmul_(z, z)
+        x.div_(torch.sqrt(chi2 * 0.25))
+    elif spec.x_dist != "normal":
+        raise ValueError(spec.x_dist)
+    ch = outlier_channels(spec, p)
+    if ch.size:
+        x[torch.as_tensor(ch, device=device)] *= spec.x_out_mult
+    return x
 
 
 def correlated_activations(p: int, n: int, rho: float, seed: int,

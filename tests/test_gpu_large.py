@@ -6,15 +6,16 @@ launch configuration the benchmark times (block width 128).
   the oracle's one-by-one dot products; relative Frobenius <= 1e-5.
 * CD sweeps on all 4096 rows; the oracle replays a seeded sample of 64 rows
   with the same Sigma (rows are independent, Sec. 4.2, so the comparison is
-  exact): per-row objective within 1e-4, codes <= 0.1% and first
-  divergences at near ties.  Sigma comes from the oracle's Gram of the
+  exact): objective within 1e-4 over the rows whose trajectories never
+  split, every split at a near tie and followed by descent, codes <= 0.1%
+  (parity.check_row_sampled_sweeps).  Sigma comes from the oracle's Gram of the
   first 2048 tokens, damped, so the oracle finishes in seconds."""
 import numpy as np
 import pytest
 import torch
 
 import synth
-from parity import dev, first_divergence, host
+from parity import check_row_sampled_sweeps, dev, host
 
 pytestmark = pytest.mark.gpu
 
@@ -58,11 +59,6 @@ def test_cd_full_size_row_sampled(qe, oracle):
         whats.append(host(Wh[rows]))
         Rs.append(host(R[rows]))
 
-    ref = oracle.cd(W[rows], S32.astype(np.float64), bits, scale[rows], zero[rows], sweeps)
-    for k in range(sweeps):
-        f_gpu = np.sum((whats[k].astype(np.float64) - W[rows]) * Rs[k])
-        assert f_gpu == pytest.approx(ref.obj[k], rel=1e-4), f"sweep {k + 1}"
-        assert np.mean(hist[k] != ref.codes_hist[k]) <= 1e-3
-    for i, d in enumerate(first_divergence(hist, ref.codes_hist)):
-        if d is not None:
-            assert ref.margin_hist[d[0]][i, d[1]] <= 1e-4, (i, d)
+    S64 = S32.astype(np.float64)
+    ref = oracle.cd(W[rows], S64, bits, scale[rows], zero[rows], sweeps)
+    check_row_sampled_sweeps(W[rows], S64, whats, Rs, hist, ref)
