@@ -56,6 +56,14 @@ typedef int qe_status;
 #define QE_R_VALID     0x2u   /* R (or E) already holds (What [+ H] - W) Sigma: resume */
 #define QE_CODES_VALID 0x4u   /* codes hold What's grid codes: the keep-current tie rule of the
                                  modified CD (Sec. 4.3) applies from the first sweep */
+/* Relaxed sweeps (Sec. 4.2, "Initialization": some iterations skip the
+ * quantization).  With period k in [1, 255], sweeps k, 2k, ... of a call
+ * (counted from 1) write the unconstrained minimiser beta of Lemma 1 instead
+ * of q_i(beta); the last sweep of a call is never relaxed.  After a relaxed
+ * sweep What is off the grid, so the next sweep starts with codes invalid;
+ * codes are left as they were during a relaxed sweep. */
+#define QE_RELAX_PERIOD(k) ((((uint32_t)(k)) & 0xffu) << 8)
+#define QE_RELAX_MASK      0xff00u
 
 /* Human-readable name of a status code (static string). */
 const char* qe_status_string(qe_status s);
@@ -113,9 +121,9 @@ qe_status qe_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, i
  * W_hat:  q x p, device, in/out.  codes: q x p uint8, device, in/out.
  * R:      q x p, device, in/out: (What - W) Sigma on exit.
  * sweeps: >= 0 full passes over the columns.
- * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID.  Without
- *         QE_INIT_FROM_W and without QE_R_VALID, R is first computed as
- *         (What - W) Sigma (warm start from any What, Sec. 4.1).
+ * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_PERIOD(k).
+ *         Without QE_INIT_FROM_W and without QE_R_VALID, R is first
+ *         computed as (What - W) Sigma (warm start from any What, Sec. 4.1).
  * obj:    NULL, or device array of `sweeps` doubles receiving
  *         f_k = <What - W, R> = ||(W - What) X||_F^2 after sweep k.
  * ------------------------------------------------------------------------ */

@@ -167,6 +167,7 @@ struct StepArgs {
     int S;                // super-block width = row stride of dcur / dprev
     float maxq;
     int codes_valid;      // current codes may be kept on an exact tie (Sec. 4.3)
+    int relax;            // write beta unquantized (relaxed sweep, Sec. 4.2)
     int n_panel;          // workgroups [0, n_panel) run the panel
     int64_t tiles_n;      // GEMM column tiles
     int sig_vec4;
@@ -212,7 +213,7 @@ __device__ __forceinline__ void load_srow(float (&dst)[SLOTS], const float* sS, 
 // One column update (column J of the block) for all 16 rows of the workgroup.
 // FULL blocks (width == B) carry no per-column test.  The Sigma row of column
 // J + 2 is fetched from LDS while column J's dependent chain runs.
-template <int SLOTS, int J, bool FULL>
+template <int SLOTS, int J, bool FULL, bool RELAX>
 __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* sS, int g,
                                            int width, float s, float z, float inv_s,
                                            float maxq, bool cvalid)
@@ -234,7 +235,8 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
     const float kc = rintf(fmaf(w, inv_s, z));
     const bool keep = cvalid && fabsf(t - kc) <= fabsf(t - kn);
     const float k = keep ? kc : kn;
-    const float wn = s * (k - z);
+    // relaxed sweep: the unconstrained minimiser itself
+    const float wn = RELAX ? beta : s * (k - z);
     const float delta = wn - w;
     const float db = row_bcast<O>(delta);
     const bool own = g == O;
@@ -246,7 +248,7 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
     for (int mm = M; mm < SLOTS; ++mm) st.L[mm] = fmaf(db, st.srow[J % 3][mm], st.L[mm]);
 }
 
-template <int SLOTS, bool FULL, int... Js>
+template <int SLOTS, bool FULL, bool RELAX, int... Js>
 __device__ __forceinline__ void panel_run(std::integer_sequence<int, Js...>,
                                           PanelState<SLOTS>& st, const float* sS, int g,
                                           int width, float s, float z, float inv_s, float maxq,
@@ -254,7 +256,7 @@ __device__ __forceinline__ void panel_run(std::integer_sequence<int, Js...>,
 {
     load_srow<SLOTS>(st.srow[0], sS, 0, g);
     if constexpr (16 * SLOTS > 1) load_srow<SLOTS>(st.srow[1], sS, 1, g);
-    (panel_step<SLOTS, Js, FULL>(st, sS, g, width, s, z, inv_s, maxq, cvalid), ...);
+    (panel_step<SLOTS, Js, FULL, RELAX>(st, sS, g, width, s, z, inv_s, maxq, cvalid), ...);
 }
 
 // Stages Sigma[r0 + k][c0 + c] (k < kw, c < cw; else 0) into LDS with the
@@ -466,18 +468,21 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
         __syncthreads();
         stage_sigma_block<SLOTS>(a.Sigma, p, j0, width, j0, width, a.sig_vec4 != 0, sS);
         __syncthreads();
-        if (width == B)
-            panel_run<SLOTS, true>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s, z,
-                                   inv_s, a.maxq, a.codes_valid != 0);
+        if (a.relax)
+            panel_run<SLOTS, false, true>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s,
+                                          z, inv_s, a.maxq, false);
+        else if (width == B)
+            panel_run<SLOTS, true, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s,
+                                          z, inv_s, a.maxq, a.codes_valid != 0);
         else
-            panel_run<SLOTS, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s, z,
-                                    inv_s, a.maxq, a.codes_valid != 0);
+            panel_run<SLOTS, false, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width,
+                                           s, z, inv_s, a.maxq, a.codes_valid != 0);
 #pragma unroll
         for (int m = 0; m < SLOTS; ++m) {
             const int c = 16 * m + g;
             if (rowok && c < width) {
                 a.Wh[i * p + j0 + c] = st.w[m];
-                a.codes[i * p + j0 + c] = (uint8_t)rintf(fmaf(st.w[m], inv_s, z));
+                if (!a.relax) a.codes[i * p + j0 + c] = (uint8_t)rintf(fmaf(st.w[m], inv_s, z));
             }
             if (rowok) a.dcur[i * a.S + (int64_t)sub * B + c] = st.dl[m];
         }
@@ -632,8 +637,13 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     base.r_vec4 = (aligned16(R) && p % 4 == 0) ? 1 : 0;
     base.status = status;
     const bool codes_valid0 = (flags & QE_CODES_VALID) && !(flags & QE_INIT_FROM_W);
+    const int period = (int)((flags & QE_RELAX_MASK) >> 8);
+    bool prev_relaxed = false;
     for (int sw = 0; sw < sweeps; ++sw) {
-        base.codes_valid = (sw > 0 || codes_valid0) ? 1 : 0;
+        const int k = sw + 1;
+        base.relax = (period > 0 && k % period == 0 && k != sweeps) ? 1 : 0;
+        base.codes_valid = ((sw > 0 || codes_valid0) && !prev_relaxed) ? 1 : 0;
+        prev_relaxed = base.relax != 0;
         qe_status st;
         switch (B) {
             case 16: st = launch_steps<1>(base, d0, d1, q, p, s); break;

@@ -30,6 +30,12 @@ QE_LAYOUT_NP = 1
 QE_INIT_FROM_W = 0x1
 QE_R_VALID = 0x2
 QE_CODES_VALID = 0x4
+QE_RELAX_MASK = 0xff00
+
+
+def QE_RELAX_PERIOD(k: int) -> int:
+    """Flag bits for relaxed sweeps every k-th sweep of a call (qe.h)."""
+    return (int(k) & 0xff) << 8
 
 _vp = ctypes.c_void_p
 _i64 = ctypes.c_int64

@@ -233,3 +233,48 @@ def test_objective_entry_point(qe, oracle):
     assert out[1] == pytest.approx(oracle.objective(np.zeros_like(W), W, S32), rel=1e-5)
     out0 = host(qe.objective(dev(W), dev(g["What"]), dev(S32)))
     assert out0[0] == pytest.approx(g["obj"][-1], rel=1e-4)
+
+
+def test_relaxed_sweeps_from_w_stay_at_w(qe, oracle):
+    """From What = W with R = 0, a relaxed sweep writes beta = W exactly
+    (Gauss-Seidel at its fixed point), so relaxed sweeps followed by the
+    last, quantized sweep equal one plain sweep bitwise."""
+    q, p = 96, 200
+    W = synth.gaussian((q, p), seed=21, std=0.02)
+    X = synth.correlated_activations(p, 1024, 0.9, 22)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    out = []
+    for sweeps, flags in ((3, qe.QE_INIT_FROM_W | qe.QE_RELAX_PERIOD(1)), (1, qe.QE_INIT_FROM_W)):
+        Wd = dev(W)
+        Wh = torch.empty_like(Wd)
+        codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+        R = torch.empty_like(Wd)
+        qe.cd_sweep(Wd, dev(S32), 4, dev(scale), dev(zero), Wh, codes, R, sweeps, flags=flags)
+        out.append((host(Wh), host(codes), host(R)))
+    for a, b in zip(*out):
+        assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("period,sweeps", [(2, 5), (3, 6)])
+def test_relaxed_sweeps_match_oracle(qe, oracle, period, sweeps):
+    q, p = 128, 257
+    W = synth.gaussian((q, p), seed=23, std=0.02)
+    X = synth.correlated_activations(p, 2048, 0.9, 24, out_channels=3, out_mult=20.0)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 3)
+    Wd = dev(W)
+    Wh = torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    R = torch.empty_like(Wd)
+    obj = torch.zeros(sweeps, dtype=torch.float64, device="cuda")
+    qe.cd_sweep(Wd, dev(S32), 3, dev(scale), dev(zero), Wh, codes, R, sweeps,
+                flags=qe.QE_INIT_FROM_W | qe.QE_RELAX_PERIOD(period), obj=obj)
+    ref = oracle.cd(W, S32.astype(np.float64), 3, scale, zero, sweeps, relax_period=period)
+    assert np.allclose(host(obj), ref.obj, rtol=1e-4)
+    # the last sweep is quantized: codes agree (up to ties) and What is on the grid
+    assert np.mean(host(codes).astype(np.int32) != ref.codes) <= 1e-3
+    assert np.array_equal(host(Wh), oracle.dequant(host(codes), scale, zero).astype(np.float32))
+    # R stays consistent with What through relaxed sweeps
+    Rex = (host(Wh).astype(np.float64) - W) @ S32.astype(np.float64)
+    assert np.max(np.abs(host(R) - Rex)) <= 1e-5 * np.max(np.abs(Rex)) + 1e-7
