@@ -292,6 +292,29 @@ def topk_abs(V: np.ndarray, s: int):
     return sup, out.reshape(V.shape)
 
 
+def column_keys(V: np.ndarray) -> np.ndarray:
+    """Squared l2 norm of every column of V, summed in fp64 and rounded to
+    fp32: the selection key of the structured projection (both sides take
+    that integer decision on the same fp32 key)."""
+    V = np.asarray(V, np.float64)
+    return np.sum(V * V, axis=0).astype(np.float32)
+
+
+def topk_columns(V: np.ndarray, c: int):
+    """Structured P (Sec. 5.3, "Structured Outliers"): keep the c columns of V
+    with the largest l2 norm (ties: lower column index first; all-zero
+    columns never kept), zero elsewhere.  Returns (kept columns ascending,
+    support as ascending linear indices of every entry of those columns,
+    dense result in V's dtype)."""
+    V = np.asarray(V)
+    q, p = V.shape
+    cols, _ = topk_abs(column_keys(V), c)
+    sup = (np.arange(q, dtype=np.int64)[:, None] * p + cols[None, :]).reshape(-1)
+    out = np.zeros_like(V)
+    out[:, cols] = V[:, cols]
+    return cols, sup, out
+
+
 def lambda_max(Sigma) -> float:
     """Largest eigenvalue of the symmetric matrix Sigma (fp64 eigvalsh)."""
     return float(np.linalg.eigvalsh(np.asarray(Sigma, np.float64))[-1])
@@ -312,23 +335,30 @@ class OutlierResult:
     V_last: Optional[np.ndarray] = None                 # V of the last IHT step
 
 
-def outlier_init(W, s: int):
-    """H = P_s(W), What = W - H (Sec. 5.3, initialisation)."""
+def outlier_init(W, s: int, structured: bool = False):
+    """H = P_s(W), What = W - H (Sec. 5.3, initialisation).  structured: the
+    column projection with floor(s / q) columns instead of P_s."""
     Wd = np.asarray(W, np.float64)
-    sup, H = topk_abs(Wd, s)
+    if structured:
+        _, sup, H = topk_columns(Wd, int(s) // Wd.shape[0])
+    else:
+        sup, H = topk_abs(Wd, s)
     return sup, H, Wd - H
 
 
 def outlier(W, Sigma, bits: int, scale, zero, s: int, lam: float, sweeps: int,
-            record: bool = True) -> OutlierResult:
+            record: bool = True, structured: bool = False) -> OutlierResult:
     """Block coordinate descent of Sec. 5.3: per iteration, one CD sweep on
     What with H fixed (target W - H), then one IHT step
     H <- P_s(H - eta grad_H g), grad_H g = 2 (H + What - W) Sigma, eta = 1/(2 lam).
-    ``scale``/``zero`` must be the outlier-aware grid (top-s of |W| excluded)."""
+    structured: P_s is replaced by the column projection keeping the
+    floor(s / q) columns of largest l2 norm ("Structured Outliers", Sec. 5.3).
+    ``scale``/``zero`` must be the outlier-aware grid (outliers of W excluded)."""
     W = np.asarray(W)
     Wd = W.astype(np.float64)
     S = _c(Sigma, np.float64)
-    sup, H, Wh = outlier_init(W, s)
+    q = W.shape[0]
+    sup, H, Wh = outlier_init(W, s, structured)
     q, p = W.shape
     codes = np.zeros((q, p), np.int32)
     res = OutlierResult(What=Wh, H=H, codes=codes, support=sup)
@@ -342,7 +372,10 @@ def outlier(W, Sigma, bits: int, scale, zero, s: int, lam: float, sweeps: int,
         res.g_cd.append(cres.obj[0])
         grad = 2.0 * ((H + Wh - Wd) @ S)
         V = H - eta * grad
-        sup, H = topk_abs(V, s)
+        if structured:
+            _, sup, H = topk_columns(V, int(s) // q)
+        else:
+            sup, H = topk_abs(V, s)
         res.g.append(objective(Wd, Wh, S, H))
         res.tau.append(float(np.min(np.abs(V.reshape(-1)[sup]))) if len(sup) else 0.0)
         if it == sweeps - 1:

@@ -113,3 +113,77 @@ def test_lambda_max_known_spectrum(oracle):
     Q = np.eye(p) - 2.0 * np.outer(v, v)        # Householder reflection: orthogonal
     S = Q @ np.diag(lam) @ Q.T
     assert oracle.lambda_max(S) == pytest.approx(7.25, rel=1e-13)
+
+
+# ---- structured (column) outliers, Sec. 5.3 "Structured Outliers"
+def lexsort_columns(V, c):
+    V = np.asarray(V, np.float64)
+    key = np.sum(V * V, axis=0).astype(np.float32)
+    order = np.lexsort((np.arange(key.size), -key.astype(np.float64)))
+    return np.sort(np.array([j for j in order[:c] if key[j] != 0.0], np.int64))
+
+
+@pytest.mark.parametrize("c", [0, 1, 3, 7, 30])
+def test_topk_columns_matches_lexsort(oracle, c):
+    V = synth.gaussian((9, 24), seed=31)
+    V[:, 5] = V[:, 2]            # equal norms: the lower column wins
+    V[:, 11] = -V[:, 2]
+    V[:, 7] = 0.0                # a zero column is never kept
+    V[:, 19] = 0.0
+    cols, sup, out = oracle.topk_columns(V, c)
+    assert np.array_equal(cols, lexsort_columns(V, c))
+    q, p = V.shape
+    assert np.array_equal(sup, np.sort((np.arange(q)[:, None] * p + cols[None, :]).reshape(-1)))
+    keep = np.zeros(p, bool)
+    keep[cols] = True
+    assert np.array_equal(out[:, keep], V[:, keep]) and not np.any(out[:, ~keep])
+
+
+def test_topk_columns_is_the_projection(oracle):
+    """Among all sets of c columns, the kept set leaves the smallest residual
+    ||V - P(V)||_F (brute force over every subset)."""
+    import itertools
+    V = synth.gaussian((5, 7), seed=32)
+    c = 3
+    _, _, out = oracle.topk_columns(V, c)
+    best = min(np.sum(np.delete(V, list(sub), axis=1).astype(np.float64) ** 2)
+               for sub in itertools.combinations(range(7), c))
+    assert np.sum((V - out).astype(np.float64) ** 2) == pytest.approx(best, rel=1e-12)
+
+
+@pytest.mark.parametrize("seed", [8, 9])
+def test_structured_iht_step_descends(oracle, seed):
+    W, X = _layer(30, 36, 100, seed)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    s = 4 * 30                   # 4 columns
+    sup0, H0, _ = oracle.outlier_init(W, s, structured=True)
+    assert len(sup0) == s and np.count_nonzero(np.any(H0 != 0, axis=0)) == 4
+    sc, ze = oracle.grid_minmax(W, 3, H0)
+    lam = oracle.lambda_max(S)
+    r = oracle.outlier(W, S, 3, sc, ze, s, lam, 5, structured=True)
+    for k in range(5):
+        assert r.g[k] <= r.g_cd[k] * (1 + 1e-12), k          # Lemma 3 (exact projection)
+        if k > 0:
+            assert r.g_cd[k] <= r.g[k - 1] * (1 + 1e-12), k
+        assert np.count_nonzero(np.any(r.H != 0, axis=0)) <= 4
+
+
+def test_structured_identity_sigma_closed_form(oracle):
+    W, _ = _layer(12, 16, 10, 10)
+    c = 1.75
+    S = c * np.eye(16)
+    s = 3 * 12
+    _, _, H0 = oracle.topk_columns(W.astype(np.float64), 3)
+    sc, ze = oracle.grid_minmax(W, 3, H0)
+    r = oracle.outlier(W, S, 3, sc, ze, s, c, 1, structured=True)
+    _, _, Hp = oracle.topk_columns(W.astype(np.float64) - r.What, 3)
+    assert np.array_equal(r.H, Hp)
+
+
+def test_structured_budget_below_one_column_is_plain_cd(oracle):
+    W, X = _layer(24, 30, 90, 11)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    sc, ze = oracle.grid_minmax(W, 3)
+    r0 = oracle.outlier(W, S, 3, sc, ze, 23, oracle.lambda_max(S), 3, structured=True)
+    rc = oracle.cd(W, S, 3, sc, ze, 3)
+    assert np.array_equal(r0.codes, rc.codes) and not np.any(r0.H)
