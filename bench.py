@@ -300,10 +300,39 @@ def outlier_bench(P, torch, synth, W, Sigma, dev, block):
     g = obj.cpu().numpy()
     t_init = ev[0].elapsed_time(ev[1]) * 1e-3
     t_iters = ev[1].elapsed_time(ev[2]) * 1e-3
-    return {"workload": spec.name, "s": s, "lambda_max": lam, "lambda_time_s": t_lam,
-            "init_time_s": t_init, "iter_time_s": t_iters / iters,
-            "support_nnz": int(nnz.cpu().item()),
-            "g_after_cd": [float(x) for x in g[0::2]], "g_after_iht": [float(x) for x in g[1::2]]}
+    res = {"workload": spec.name, "s": s, "lambda_max": lam, "lambda_time_s": t_lam,
+           "init_time_s": t_init, "iter_time_s": t_iters / iters,
+           "support_nnz": int(nnz.cpu().item()),
+           "g_after_cd": [float(x) for x in g[0::2]], "g_after_iht": [float(x) for x in g[1::2]]}
+
+    # structured outliers (Sec. 5.3): floor(s / q) whole columns
+    ncols = s // q
+    sup = torch.zeros(s, dtype=torch.int64, device=dev)
+
+    def run_cols(timed):
+        if timed:
+            ev[3].record(stream)
+        H, _, sup_c, n = P.topk_columns(W, ncols, check=False)
+        sup[:q * ncols] = sup_c[:q * ncols]
+        scale, zero = P.grid_minmax(W, bits, H)
+        if timed:
+            ev[4].record(stream)
+        P.cd_outlier_sweep(W, Sigma, bits, scale, zero, Wh, codes, H, E, s, lam, sup, n, iters,
+                           block=block, flags=P.QE_INIT_FROM_W | P.QE_OUTLIER_COLUMNS, obj=obj,
+                           ws=ws_o, check=False)
+        if timed:
+            ev[5].record(stream)
+
+    run_cols(False)
+    torch.cuda.synchronize()
+    run_cols(True)
+    torch.cuda.synchronize()
+    assert P.sync_status(ws_o) == 0
+    g = obj.cpu().numpy()
+    res["structured"] = {"columns": ncols, "init_time_s": ev[3].elapsed_time(ev[4]) * 1e-3,
+                         "iter_time_s": ev[4].elapsed_time(ev[5]) * 1e-3 / iters,
+                         "g_after_iht": [float(x) for x in g[1::2]]}
+    return res
 
 
 if __name__ == "__main__":

@@ -64,6 +64,10 @@ typedef int qe_status;
  * codes are left as they were during a relaxed sweep. */
 #define QE_RELAX_PERIOD(k) ((((uint32_t)(k)) & 0xffu) << 8)
 #define QE_RELAX_MASK      0xff00u
+/* qe_cd_outlier_sweep only: structured outliers ("Structured Outliers",
+ * Sec. 5.3): the projection keeps the floor(s / q) whole columns of largest
+ * l2 norm instead of the s largest entries (see qe_topk_columns). */
+#define QE_OUTLIER_COLUMNS 0x10u
 
 /* Human-readable name of a status code (static string). */
 const char* qe_status_string(qe_status s);
@@ -150,6 +154,8 @@ qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, 
  * flags:    QE_INIT_FROM_W: What = W - H (H and support as given, e.g. from
  *           qe_topk_abs on W, Sec. 5.3 initialisation), E = 0.
  *           QE_R_VALID: E already valid.  QE_CODES_VALID as above.
+ *           QE_OUTLIER_COLUMNS: structured outliers (whole columns); start
+ *           from qe_topk_columns on W.
  *           Without QE_INIT_FROM_W / QE_R_VALID, E = (What + H - W) Sigma.
  * obj:      NULL or device array of 2*sweeps doubles: obj[2k] = g after the
  *           CD sweep of iteration k, obj[2k+1] = g after its IHT step.
@@ -172,6 +178,22 @@ qe_status qe_cd_outlier_sweep(const float* W, const float* Sigma, int64_t q, int
 size_t qe_topk_workspace_size(int64_t count, int64_t s);
 qe_status qe_topk_abs(const float* V, int64_t count, int64_t s, float* out, int64_t* support,
                       int64_t* nnz, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * Structured projection ("Structured Outliers", Sec. 5.3): keep the c whole
+ * columns of the q x p matrix V with the largest l2 norm, zero elsewhere.
+ * Selection key of column j: sum_i V_ij^2 accumulated in fp64, rounded to
+ * fp32; ties go to the lower column; all-zero columns are never kept.
+ * out: q x p floats, device.  columns: NULL or device int64[c]: the kept
+ * columns, ascending.  support: device int64[q * c]: linear indices of every
+ * entry of the kept columns, ascending (the support format of
+ * qe_cd_outlier_sweep).  nnz: device int64: number of support entries
+ * (q x number of kept columns).
+ * ------------------------------------------------------------------------ */
+size_t qe_topk_columns_workspace_size(int64_t q, int64_t p);
+qe_status qe_topk_columns(const float* V, int64_t q, int64_t p, int64_t c, float* out,
+                          int64_t* columns, int64_t* support, int64_t* nnz, void* ws,
+                          size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
  * Exact objective and its normaliser (Sec. 3 problem (1); Sec. 4.4 relative

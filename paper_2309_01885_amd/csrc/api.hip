@@ -132,7 +132,8 @@ qe_status qe_cd_outlier_sweep(const float* W, const float* Sigma, int64_t q, int
     if (bad_dims(q, p) || bad_bits(bits) || bad_block(block) || sweeps < 0) return QE_ERR_ARG;
     if (s < 0 || s > q * p || (s > 0 && !support)) return QE_ERR_ARG;
     if (!(lambda_max > 0.f) || !std::isfinite(lambda_max)) return QE_ERR_ARG;
-    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID)) return QE_ERR_ARG;
+    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_OUTLIER_COLUMNS))
+        return QE_ERR_ARG;
     if (!ws || ws_bytes < outlier_ws_bytes(q, p, block, s)) return QE_ERR_WORKSPACE;
     hipStream_t st = as_stream(stream);
     if (clear_status(ws, st) != QE_OK) return QE_ERR_HIP;
@@ -156,6 +157,24 @@ qe_status qe_topk_abs(const float* V, int64_t count, int64_t s, float* out, int6
     hipStream_t st = as_stream(stream);
     if (clear_status(ws, st) != QE_OK) return QE_ERR_HIP;
     return launch_topk(V, count, s, out, support, nnz, ws, st);
+}
+
+size_t qe_topk_columns_workspace_size(int64_t q, int64_t p)
+{
+    if (bad_dims(q, p)) return 0;
+    return topk_columns_ws_bytes(q, p);
+}
+
+qe_status qe_topk_columns(const float* V, int64_t q, int64_t p, int64_t c, float* out,
+                          int64_t* columns, int64_t* support, int64_t* nnz, void* ws,
+                          size_t ws_bytes, void* stream)
+{
+    if (!V || !out || !nnz || bad_dims(q, p) || c < 0 || c > p || (c > 0 && !support))
+        return QE_ERR_ARG;
+    if (!ws || ws_bytes < topk_columns_ws_bytes(q, p)) return QE_ERR_WORKSPACE;
+    hipStream_t st = as_stream(stream);
+    if (clear_status(ws, st) != QE_OK) return QE_ERR_HIP;
+    return launch_topk_columns(V, q, p, c, out, columns, support, nnz, ws, st);
 }
 
 // ------------------------------------------------------------------ objective

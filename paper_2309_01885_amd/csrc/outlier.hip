@@ -384,7 +384,7 @@ __global__ __launch_bounds__(256) void iht_target_kernel(const float* __restrict
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 v[u] = hv[u] - ev[u] / lambda;
-                atomicAdd(&h[abs_key(v[u]) >> 21], 1u);
+                if (hist) atomicAdd(&h[abs_key(v[u]) >> 21], 1u);
             }
             V4[e] = v;
         }
@@ -392,9 +392,10 @@ __global__ __launch_bounds__(256) void iht_target_kernel(const float* __restrict
     }
     for (int64_t e = tail + tid; e < n; e += G) {
         const float v = H[e] - E[e] / lambda;
-        atomicAdd(&h[abs_key(v) >> 21], 1u);
+        if (hist) atomicAdd(&h[abs_key(v) >> 21], 1u);
         V[e] = v;
     }
+    if (!hist) return;
     __syncthreads();
     for (int b = threadIdx.x; b < kHistBins; b += blockDim.x)
         if (h[b]) atomicAdd(&hist[b], h[b]);
@@ -613,6 +614,151 @@ __global__ __launch_bounds__(256) void spmm_delta_kernel(const int64_t* __restri
     }
 }
 
+// ---------------------------------------------------------------- structured projection
+// "Structured Outliers" (Sec. 5.3): keep the floor(s / q) whole columns of V
+// with the largest l2 norm.  Key of column j: sum_i V_ij^2 in fp64 (row
+// chunks summed in a fixed order), rounded to fp32; the columns are then
+// chosen by the radix select above (ties: lower column first; all-zero
+// columns never kept), and the kept columns are expanded into the dense
+// result and the ascending list of their entries.
+constexpr int kColChunkRows = 256;
+
+__global__ __launch_bounds__(256) void colnorm_partial_kernel(const float* __restrict__ V,
+                                                              int64_t q, int64_t p,
+                                                              double* part, const int* status)
+{
+    if (failed(status)) return;
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= p) return;
+    const int64_t r0 = (int64_t)blockIdx.y * kColChunkRows;
+    const int64_t r1 = min(q, r0 + kColChunkRows);
+    double acc = 0.0;
+    for (int64_t i = r0; i < r1; ++i) {
+        const double v = (double)V[i * p + c];
+        acc += v * v;
+    }
+    part[(int64_t)blockIdx.y * p + c] = acc;
+}
+
+__global__ __launch_bounds__(256) void colnorm_key_kernel(const double* __restrict__ part,
+                                                          int nchunks, int64_t p, float* key,
+                                                          uint8_t* mask, const int* status)
+{
+    if (failed(status)) return;
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= p) return;
+    double acc = 0.0;
+    for (int k = 0; k < nchunks; ++k) acc += part[(int64_t)k * p + c];
+    key[c] = (float)acc;
+    mask[c] = 0;
+}
+
+__global__ void colmask_kernel(const int64_t* cols, const int64_t* ncols_p, int64_t p,
+                               uint8_t* mask, const int* status)
+{
+    if (failed(status)) return;
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= *ncols_p) return;
+    const int64_t c = cols[k];
+    if (c >= 0 && c < p) mask[c] = 1;
+}
+
+// dense result, and (idx, val) of every entry of the kept columns, ascending
+__global__ __launch_bounds__(256) void colexpand_kernel(const float* __restrict__ V, int64_t q,
+                                                        int64_t p, const uint8_t* __restrict__ mask,
+                                                        const int64_t* __restrict__ cols,
+                                                        const int64_t* ncols_p, int64_t cap,
+                                                        float* dense, int64_t* idx, float* val,
+                                                        int64_t* nnz, const int* status)
+{
+    if (failed(status)) return;
+    const int64_t G = (int64_t)gridDim.x * blockDim.x;
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (dense)
+        for (int64_t i = blockIdx.x; i < q; i += gridDim.x)
+            for (int64_t c = threadIdx.x; c < p; c += blockDim.x)
+                dense[i * p + c] = mask[c] ? V[i * p + c] : 0.f;
+    const int64_t nc = *ncols_p;
+    const int64_t total = nc > 0 ? min(q * nc, cap) : 0;
+    for (int64_t e = tid; e < total; e += G) {
+        const int64_t i = e / nc, c = cols[e % nc];
+        idx[e] = i * p + c;
+        if (val) val[e] = V[i * p + c];
+    }
+    if (tid == 0 && nnz) *nnz = total;
+}
+
+struct ColBufs {
+    double* part;
+    float* key;
+    uint8_t* mask;
+    int64_t* cols;
+    int64_t* ncols;
+};
+
+static size_t col_bytes(int64_t q, int64_t p)
+{
+    const int64_t nch = cdiv(q, kColChunkRows);
+    return align256(sizeof(double) * nch * p) + align256(sizeof(float) * p) + align256(p) +
+           align256(sizeof(int64_t) * p) + align256(sizeof(int64_t));
+}
+
+static ColBufs take_col(Ws& w, int64_t q, int64_t p)
+{
+    ColBufs b;
+    b.part = w.take<double>(cdiv(q, kColChunkRows) * p);
+    b.key = w.take<float>(p);
+    b.mask = w.take<uint8_t>(p);
+    b.cols = w.take<int64_t>(p);
+    b.ncols = w.take<int64_t>(1);
+    return b;
+}
+
+// columns: the kept column list (ascending, device) may be b.cols itself
+static qe_status run_select_columns(const float* V, int64_t q, int64_t p, int64_t c,
+                                    const SelBufs& sb, const ColBufs& cb, float* dense,
+                                    int64_t* idx, float* val, int64_t* nnz, int64_t cap,
+                                    const int* status, hipStream_t hs)
+{
+    const int nch = (int)cdiv(q, kColChunkRows);
+    hipLaunchKernelGGL(colnorm_partial_kernel, dim3((unsigned)cdiv(p, 256), (unsigned)nch),
+                       dim3(256), 0, hs, V, q, p, cb.part, status);
+    hipLaunchKernelGGL(colnorm_key_kernel, dim3((unsigned)cdiv(p, 256)), dim3(256), 0, hs,
+                       cb.part, nch, p, cb.key, cb.mask, status);
+    if (c > 0) {
+        const qe_status st = run_select(cb.key, p, c, sb.st, sb.hist, sb.cnt, sb.off, sb.adm,
+                                        cb.cols, nullptr, nullptr, cb.ncols, status, hs);
+        if (st != QE_OK) return st;
+    } else {
+        hipLaunchKernelGGL(set_i64_kernel, dim3(1), dim3(64), 0, hs, cb.ncols, (int64_t)0);
+    }
+    hipLaunchKernelGGL(colmask_kernel, dim3((unsigned)cdiv(p, 256)), dim3(256), 0, hs, cb.cols,
+                       cb.ncols, p, cb.mask, status);
+    hipLaunchKernelGGL(colexpand_kernel, dim3(2048), dim3(256), 0, hs, V, q, p, cb.mask, cb.cols,
+                       cb.ncols, cap, dense, idx, val, nnz, status);
+    return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
+size_t topk_columns_ws_bytes(int64_t q, int64_t p) { return kStatusBytes + sel_bytes() + col_bytes(q, p); }
+
+qe_status launch_topk_columns(const float* V, int64_t q, int64_t p, int64_t c, float* out,
+                              int64_t* columns, int64_t* support, int64_t* nnz, void* ws,
+                              hipStream_t hs)
+{
+    const int* status = static_cast<const int*>(ws);
+    Ws w(ws);
+    SelBufs sb = take_sel(w);
+    ColBufs cb = take_col(w, q, p);
+    const qe_status st = run_select_columns(V, q, p, c, sb, cb, out, support, nullptr, nnz,
+                                            q * c, status, hs);
+    if (st != QE_OK) return st;
+    if (columns && c > 0 &&
+        hipMemcpyAsync(columns, cb.cols, sizeof(int64_t) * c, hipMemcpyDeviceToDevice, hs) !=
+            hipSuccess)
+        return QE_ERR_HIP;
+    return QE_OK;
+}
+
 size_t outlier_ws_bytes(int64_t q, int64_t p, int block, int64_t s)
 {
     const int64_t cap = s > 0 ? s : 1;
@@ -624,6 +770,7 @@ size_t outlier_ws_bytes(int64_t q, int64_t p, int block, int64_t s)
     b += align256(sizeof(int64_t) * (q + 1));                     // its row pointers
     b += 3 * align256(sizeof(int64_t));                           // list sizes
     b += align256(sizeof(double) * kObjBlocks);                   // objective partials
+    b += col_bytes(q, p);                                         // structured projection
     return b;
 }
 
@@ -650,6 +797,8 @@ qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t 
     int64_t* cnt[2] = {w.take<int64_t>(1), w.take<int64_t>(1)};
     int64_t* mcount = w.take<int64_t>(1);
     double* opart = w.take<double>(kObjBlocks);
+    ColBufs cb = take_col(w, q, p);
+    const bool columns = (flags & QE_OUTLIER_COLUMNS) != 0;
     const int vec4 = (aligned16(H) && aligned16(E) && aligned16(V)) ? 1 : 0;
     const int sig_vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
     const int64_t n_rt = cdiv(q, kSpRows), n_cb = cdiv(p, kSpCols);
@@ -668,17 +817,24 @@ qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t 
     }
     int cur = 0;
     for (int it = 0; it < sweeps; ++it) {
-        const uint32_t f = it == 0 ? flags : (QE_R_VALID | QE_CODES_VALID);
+        const uint32_t f = it == 0 ? (flags & ~QE_OUTLIER_COLUMNS) : (QE_R_VALID | QE_CODES_VALID);
         qe_status st = launch_cd(W, Sigma, q, p, bits, scale, zero, Wh, codes, E, H, 1, block, f,
                                  obj ? obj + 2 * it : nullptr, 2, ws, hs);
         if (st != QE_OK) return st;
         if (s > 0) {
             const int nxt = cur ^ 1;
-            select_init(sb.st, s < n ? s : n, sb.hist, status, hs);
-            hipLaunchKernelGGL(iht_target_kernel, dim3(2048), dim3(256), 0, hs, H, E, lambda, V, n,
-                               vec4, sb.hist, status);
-            st = run_select(V, n, s, sb.st, sb.hist, sb.cnt, sb.off, sb.adm, idx[nxt], val[nxt], H,
-                            cnt[nxt], status, hs, true);
+            if (columns) {
+                hipLaunchKernelGGL(iht_target_kernel, dim3(2048), dim3(256), 0, hs, H, E, lambda,
+                                   V, n, vec4, (uint32_t*)nullptr, status);
+                st = run_select_columns(V, q, p, s / q, sb, cb, H, idx[nxt], val[nxt], cnt[nxt],
+                                        cap, status, hs);
+            } else {
+                select_init(sb.st, s < n ? s : n, sb.hist, status, hs);
+                hipLaunchKernelGGL(iht_target_kernel, dim3(2048), dim3(256), 0, hs, H, E, lambda,
+                                   V, n, vec4, sb.hist, status);
+                st = run_select(V, n, s, sb.st, sb.hist, sb.cnt, sb.off, sb.adm, idx[nxt],
+                                val[nxt], H, cnt[nxt], status, hs, true);
+            }
             if (st != QE_OK) return st;
             hipLaunchKernelGGL(merge_supports_kernel, dim3((unsigned)cdiv(2 * cap, 256)),
                                dim3(256), 0, hs, idx[cur], val[cur], cnt[cur], idx[nxt], val[nxt],

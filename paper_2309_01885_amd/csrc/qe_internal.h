@@ -451,6 +451,10 @@ qe_status launch_residual_dot(const float* W, const float* Wh, const float* H, c
 size_t topk_ws_bytes(int64_t count, int64_t s);
 qe_status launch_topk(const float* V, int64_t count, int64_t s, float* out, int64_t* support,
                       int64_t* nnz, void* ws, hipStream_t st);
+size_t topk_columns_ws_bytes(int64_t q, int64_t p);
+qe_status launch_topk_columns(const float* V, int64_t q, int64_t p, int64_t c, float* out,
+                              int64_t* columns, int64_t* support, int64_t* nnz, void* ws,
+                              hipStream_t st);
 size_t outlier_ws_bytes(int64_t q, int64_t p, int block, int64_t s);
 qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
                          const float* scale, const float* zero, float* Wh, uint8_t* codes,

@@ -31,6 +31,7 @@ QE_INIT_FROM_W = 0x1
 QE_R_VALID = 0x2
 QE_CODES_VALID = 0x4
 QE_RELAX_MASK = 0xff00
+QE_OUTLIER_COLUMNS = 0x10
 
 
 def QE_RELAX_PERIOD(k: int) -> int:
@@ -60,6 +61,8 @@ SIGNATURES = {
                                    _sz, _vp]),
     "qe_topk_workspace_size": (_sz, [_i64, _i64]),
     "qe_topk_abs": (_int, [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "qe_topk_columns_workspace_size": (_sz, [_i64, _i64]),
+    "qe_topk_columns": (_int, [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "qe_objective_workspace_size": (_sz, [_i64, _i64]),
     "qe_objective": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _sz, _vp]),
     "qe_lambda_workspace_size": (_sz, [_i64]),
@@ -240,6 +243,28 @@ def topk_abs(V: torch.Tensor, s: int, ws: Optional[torch.Tensor] = None, check: 
                            _stream(stream)), "qe_topk_abs")
     _finish(ws, check, "qe_topk_abs", stream)
     return out, support, nnz
+
+
+def topk_columns(V: torch.Tensor, c: int, ws: Optional[torch.Tensor] = None,
+                 check: bool = True, stream=None):
+    """Structured projection of the q x p matrix V (c whole columns of largest
+    l2 norm): returns (dense result, kept columns int64[c], support int64[q*c],
+    nnz int64[1])."""
+    lib = load()
+    q, p = V.shape
+    out = torch.empty_like(V)
+    cols = torch.full((max(int(c), 1),), -1, dtype=torch.int64, device=V.device)
+    support = torch.zeros(max(int(q * c), 1), dtype=torch.int64, device=V.device)
+    nnz = torch.zeros(1, dtype=torch.int64, device=V.device)
+    if ws is None:
+        ws = workspace(lib.qe_topk_columns_workspace_size(q, p), V.device)
+    _check(lib.qe_topk_columns(_ptr(V, torch.float32, "V"), q, p, int(c),
+                               _ptr(out, torch.float32, "out"), _vp(cols.data_ptr()),
+                               _vp(support.data_ptr()), _ptr(nnz, torch.int64, "nnz"),
+                               _vp(ws.data_ptr()), ws.numel(), _stream(stream)),
+           "qe_topk_columns")
+    _finish(ws, check, "qe_topk_columns", stream)
+    return out, cols, support, nnz
 
 
 # ---------------------------------------------------------------------------- objective

@@ -215,3 +215,42 @@ def test_c5_cd_row_sampled(qe, oracle):
     del S64
     cd_row_sampled(qe, oracle, W, S32, spec.bits, spec.sweeps,
                    synth.row_sample(spec.q, 16, spec.cfg))
+
+
+def test_c4_structured_outlier_run(qe, oracle):
+    """The outlier-aware configuration with structured outliers (Sec. 5.3):
+    floor(s / q) = 40 whole columns, 4 iterations against the oracle."""
+    spec = synth.CONFIGS["c4"]
+    q, p, bits, s = spec.q, spec.p, spec.bits, spec.s_budget
+    iters = 4
+    W = synth.weights(spec)
+    S32 = host_sigma(oracle, spec, 2048).astype(np.float32)
+    lam = float(np.float32(oracle.lambda_max(S32)))
+    ncols = s // q
+    H0, cols0, sup_c, n0 = qe.topk_columns(dev(W), ncols)
+    ref_cols0, _, ref_H0 = oracle.topk_columns(W, ncols)
+    assert np.array_equal(host(cols0), ref_cols0)
+    scale, zero = oracle.grid_minmax(W, bits, ref_H0)
+    Wd, Sd = dev(W), dev(S32)
+    Wh = torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    E = torch.empty_like(Wd)
+    sup = torch.zeros(s, dtype=torch.int64, device="cuda")
+    n = int(host(n0)[0])
+    sup[:n] = sup_c[:n]
+    obj = torch.zeros(2 * iters, dtype=torch.float64, device="cuda")
+    qe.cd_outlier_sweep(Wd, Sd, bits, dev(scale), dev(zero), Wh, codes, H0, E, s, lam, sup, n0,
+                        iters, block=128, flags=qe.QE_INIT_FROM_W | qe.QE_OUTLIER_COLUMNS,
+                        obj=obj)
+    g = host(obj)
+    Hcols = np.nonzero(np.any(host(H0) != 0, axis=0))[0]
+    codes_g = host(codes).astype(np.int32)
+    del Wd, Sd, Wh, codes, E
+    torch.cuda.empty_cache()
+    ref = oracle.outlier(W, S32, bits, scale, zero, s, lam, iters, structured=True)
+    for k in range(iters):
+        assert g[2 * k] == pytest.approx(ref.g_cd[k], rel=1e-4), f"g after CD, it {k + 1}"
+        assert g[2 * k + 1] == pytest.approx(ref.g[k], rel=1e-4), f"g after IHT, it {k + 1}"
+        assert g[2 * k + 1] <= g[2 * k] * (1 + 1e-6)                  # Lemma 3
+    assert np.array_equal(Hcols, np.nonzero(np.any(ref.H != 0, axis=0))[0])
+    assert np.mean(codes_g != ref.codes) <= 1e-3

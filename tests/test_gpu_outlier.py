@@ -103,3 +103,58 @@ def test_zero_budget_equals_plain_cd(qe, oracle):
     assert np.array_equal(g["What"], host(Wh))
     assert np.array_equal(g["codes"], host(codes).astype(np.int32))
     assert not np.any(g["H"])
+
+
+# ---- structured (column) outliers, Sec. 5.3 "Structured Outliers"
+@pytest.mark.parametrize("q,p,c", [(64, 300, 7), (512, 512, 5), (33, 70, 0), (40, 50, 60)])
+def test_topk_columns_identical(qe, oracle, q, p, c):
+    V = synth.gaussian((q, p), seed=41)
+    V[:, 9] = V[:, 3]              # equal norms: the lower column is kept
+    V[:, 17] = -V[:, 3]
+    V[:, 5] = 0.0                  # all-zero columns are never kept
+    c = min(c, p)
+    out, cols, sup, nnz = qe.topk_columns(dev(V), c)
+    ref_cols, ref_sup, ref_out = oracle.topk_columns(V, c)
+    n = int(host(nnz)[0])
+    assert n == len(ref_sup)
+    assert np.array_equal(host(cols)[:len(ref_cols)], ref_cols)
+    assert np.array_equal(host(sup)[:n], ref_sup)
+    assert np.array_equal(host(out), ref_out)
+
+
+@pytest.mark.parametrize("q,p,ncols,corr", [(256, 384, 6, 0.9), (96, 200, 3, 0.5)])
+def test_structured_outlier_matches_oracle(qe, oracle, q, p, ncols, corr):
+    W = synth.gaussian((q, p), seed=43, std=0.02)
+    W[:, ::37] *= 8.0              # a few heavy columns
+    X = synth.correlated_activations(p, 2048, corr, 44, out_channels=max(1, p // 100),
+                                     out_mult=30.0)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    s = ncols * q
+    lam = float(np.float32(oracle.lambda_max(S32)))
+    H0, cols0, sup0, n0 = qe.topk_columns(dev(W), ncols)
+    ref_cols0, ref_sup0, ref_H0 = oracle.topk_columns(W, ncols)
+    assert np.array_equal(host(cols0), ref_cols0)
+    scale, zero = oracle.grid_minmax(W, 3, ref_H0)
+    sweeps = 4
+    Wd, Sd = dev(W), dev(S32)
+    Wh = torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    E = torch.empty_like(Wd)
+    sup = torch.zeros(s, dtype=torch.int64, device="cuda")
+    sup[:int(host(n0)[0])] = sup0[:int(host(n0)[0])]
+    obj = torch.zeros(2 * sweeps, dtype=torch.float64, device="cuda")
+    qe.cd_outlier_sweep(Wd, Sd, 3, dev(scale), dev(zero), Wh, codes, H0, E, s, lam, sup, n0,
+                        sweeps, flags=qe.QE_INIT_FROM_W | qe.QE_OUTLIER_COLUMNS, obj=obj)
+    g = host(obj)
+    ref = oracle.outlier(W, S32, 3, scale, zero, s, lam, sweeps, structured=True)
+    for k in range(sweeps):
+        assert g[2 * k] == pytest.approx(ref.g_cd[k], rel=1e-4), f"g after CD, it {k + 1}"
+        assert g[2 * k + 1] == pytest.approx(ref.g[k], rel=1e-4), f"g after IHT, it {k + 1}"
+        assert g[2 * k + 1] <= g[2 * k] * (1 + 1e-6)                  # Lemma 3
+    n = int(host(n0)[0])
+    assert np.array_equal(host(sup)[:n], ref.support)
+    Hg = host(H0)
+    assert np.array_equal(np.nonzero(np.any(Hg != 0, axis=0))[0],
+                          np.nonzero(np.any(ref.H != 0, axis=0))[0])
+    assert np.allclose(Hg, ref.H, rtol=1e-3, atol=1e-7)
+    assert np.mean(host(codes).astype(np.int32) != ref.codes) <= 1e-3
