@@ -166,6 +166,58 @@ def dequant(codes: np.ndarray, scale: np.ndarray, zero: np.ndarray) -> np.ndarra
 
 
 # --------------------------------------------------------------------------
+# Export for serving: bit-packed codes and the outliers in CSR form.  The
+# paper leaves serving kernels out of scope (Sec. 5.3, "Structured
+# Outliers"); the layout here is this library's: each row of codes is one
+# little-endian bit stream, code j in bits [j*bits, (j+1)*bits), bytes
+# filled from their least significant bit; rows start on a byte boundary.
+# --------------------------------------------------------------------------
+def packed_row_bytes(p: int, bits: int) -> int:
+    return (p * bits + 7) // 8
+
+
+def pack_codes(codes: np.ndarray, bits: int) -> np.ndarray:
+    """q x p codes in [0, 2^bits) -> q x packed_row_bytes(p, bits) uint8."""
+    codes = np.asarray(codes, np.int64)
+    q, p = codes.shape
+    nb = packed_row_bytes(p, bits)
+    out = np.zeros((q, nb), np.uint8)
+    for i in range(q):
+        for j in range(p):
+            for b in range(bits):
+                if (codes[i, j] >> b) & 1:
+                    pos = j * bits + b
+                    out[i, pos // 8] |= np.uint8(1 << (pos % 8))
+    return out
+
+
+def unpack_codes(packed: np.ndarray, p: int, bits: int) -> np.ndarray:
+    packed = np.asarray(packed, np.uint8)
+    q = packed.shape[0]
+    out = np.zeros((q, p), np.int64)
+    for i in range(q):
+        for j in range(p):
+            v = 0
+            for b in range(bits):
+                pos = j * bits + b
+                v |= ((int(packed[i, pos // 8]) >> (pos % 8)) & 1) << b
+            out[i, j] = v
+    return out
+
+
+def outliers_csr(H: np.ndarray, support: np.ndarray):
+    """The support entries of H (q x p; support = ascending linear indices)
+    as CSR: row pointers int64[q + 1], column indices int32, values float32."""
+    H = np.asarray(H)
+    q, p = H.shape
+    support = np.asarray(support, np.int64)
+    rows, cols = support // p, support % p
+    rowptr = np.zeros(q + 1, np.int64)
+    np.add.at(rowptr, rows + 1, 1)
+    return np.cumsum(rowptr), cols.astype(np.int32), H[rows, cols].astype(np.float32)
+
+
+# --------------------------------------------------------------------------
 # Objective (problem (1) of Sec. 3) and relative calibration error (Sec. 4.4)
 # --------------------------------------------------------------------------
 def objective(W, What, Sigma, H=None) -> float:

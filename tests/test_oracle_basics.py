@@ -119,3 +119,31 @@ def test_objective_through_sigma_equals_direct(oracle):
     relerr = oracle.rel_error(W, Wh, S)
     d2 = np.linalg.norm(W.astype(np.float64) @ X - Wh.astype(np.float64) @ X) ** 2
     assert relerr == pytest.approx(d2 / np.linalg.norm(W.astype(np.float64) @ X) ** 2, rel=1e-12)
+
+
+# ---- export for serving (bit-packed codes, outliers as CSR)
+def test_pack_codes_hand_fixture(oracle):
+    # 4-bit: code j in the low nibble for even j; 3-bit: 8 codes per 3 bytes
+    c4 = np.array([[1, 2, 3, 15, 0]])
+    assert oracle.pack_codes(c4, 4).tolist() == [[0x21, 0xF3, 0x00]]
+    c3 = np.array([[1, 2, 3, 4, 5, 6, 7, 0]])
+    # bit stream (LSB first): 001 010 011 100 101 110 111 000 read little-endian per code
+    assert oracle.pack_codes(c3, 3).tolist() == [[0b11010001, 0b01011000, 0b00011111]]
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4, 5, 8])
+def test_pack_roundtrip(oracle, bits):
+    codes = synth.integers((7, 29), seed=bits, lo=0, hi=2 ** bits)
+    packed = oracle.pack_codes(codes, bits)
+    assert packed.shape == (7, (29 * bits + 7) // 8)
+    assert np.array_equal(oracle.unpack_codes(packed, 29, bits), codes)
+
+
+def test_outliers_csr_matches_scipy(oracle):
+    import scipy.sparse as sp
+    H = synth.gaussian((9, 13), seed=3)
+    H[np.abs(H) < 1.2] = 0.0
+    rowptr, cols, vals = oracle.outliers_csr(H, np.flatnonzero(H))
+    ref = sp.csr_matrix(H)
+    assert np.array_equal(rowptr, ref.indptr) and np.array_equal(cols, ref.indices)
+    assert np.array_equal(vals, ref.data.astype(np.float32))
