@@ -218,6 +218,29 @@ size_t qe_lambda_workspace_size(int64_t p);
 qe_status qe_lambda_max(const float* Sigma, int64_t p, int max_iters, float tol,
                         float* lambda_out, void* ws, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------------------------------
+ * Export for serving.  The paper leaves serving kernels out of scope
+ * (Sec. 5.3, "Structured Outliers"); these layouts are this library's.
+ *
+ * qe_pack_codes: each row of the q x p codes (device uint8, values < 2^bits,
+ * bits in [1, 8]) becomes one little-endian bit stream of
+ * qe_packed_row_bytes(p, bits) bytes (device, out): code j occupies bits
+ * [j*bits, (j+1)*bits), bytes are filled from their least significant bit,
+ * rows start on a byte boundary.  Higher code bits are ignored.
+ *
+ * qe_outliers_csr: the support entries of H (q x p, device) as CSR:
+ * support = ascending linear indices (device int64, capacity cap), nnz =
+ * device int64 count (clamped to [0, cap]); rowptr: device int64[q + 1],
+ * cols: device int32[cap], vals: device float[cap] (out).  Out-of-range
+ * indices are clamped into the matrix.
+ * ------------------------------------------------------------------------ */
+int64_t qe_packed_row_bytes(int64_t p, int bits);
+qe_status qe_pack_codes(const uint8_t* codes, int64_t q, int64_t p, int bits, uint8_t* packed,
+                        void* stream);
+qe_status qe_outliers_csr(const float* H, int64_t q, int64_t p, const int64_t* support,
+                          const int64_t* nnz, int64_t cap, int64_t* rowptr, int32_t* cols,
+                          float* vals, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -180,29 +180,16 @@ def pack_codes(codes: np.ndarray, bits: int) -> np.ndarray:
     """q x p codes in [0, 2^bits) -> q x packed_row_bytes(p, bits) uint8."""
     codes = np.asarray(codes, np.int64)
     q, p = codes.shape
-    nb = packed_row_bytes(p, bits)
-    out = np.zeros((q, nb), np.uint8)
-    for i in range(q):
-        for j in range(p):
-            for b in range(bits):
-                if (codes[i, j] >> b) & 1:
-                    pos = j * bits + b
-                    out[i, pos // 8] |= np.uint8(1 << (pos % 8))
-    return out
+    stream = ((codes[:, :, None] >> np.arange(bits)) & 1).reshape(q, p * bits).astype(np.uint8)
+    pad = packed_row_bytes(p, bits) * 8 - p * bits
+    stream = np.concatenate([stream, np.zeros((q, pad), np.uint8)], axis=1)
+    return np.packbits(stream, axis=1, bitorder="little")
 
 
 def unpack_codes(packed: np.ndarray, p: int, bits: int) -> np.ndarray:
-    packed = np.asarray(packed, np.uint8)
-    q = packed.shape[0]
-    out = np.zeros((q, p), np.int64)
-    for i in range(q):
-        for j in range(p):
-            v = 0
-            for b in range(bits):
-                pos = j * bits + b
-                v |= ((int(packed[i, pos // 8]) >> (pos % 8)) & 1) << b
-            out[i, j] = v
-    return out
+    bitsarr = np.unpackbits(np.asarray(packed, np.uint8), axis=1, bitorder="little")
+    stream = bitsarr[:, :p * bits].reshape(-1, p, bits).astype(np.int64)
+    return np.sum(stream << np.arange(bits), axis=2)
 
 
 def outliers_csr(H: np.ndarray, support: np.ndarray):

@@ -6,5 +6,5 @@ of include/qe.h); ``paper_2309_01885_amd.qe`` is its ctypes binding.
 from .qe import (QE_CODES_VALID, QE_INIT_FROM_W, QE_LAYOUT_NP, QE_LAYOUT_PN, QE_R_VALID,  # noqa: F401
                  QE_OUTLIER_COLUMNS, QE_RELAX_MASK, QE_RELAX_PERIOD,
                  QEError, cd_outlier_sweep, cd_sweep, cd_workspace_size, gram, grid_minmax,
-                 lambda_max, load, objective, outlier_workspace_size, sync_status, topk_abs, topk_columns,
-                 workspace)
+                 lambda_max, load, objective, outliers_csr, outlier_workspace_size, pack_codes,
+                 sync_status, topk_abs, topk_columns, workspace)

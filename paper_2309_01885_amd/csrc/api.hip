@@ -177,6 +177,29 @@ qe_status qe_topk_columns(const float* V, int64_t q, int64_t p, int64_t c, float
     return launch_topk_columns(V, q, p, c, out, columns, support, nnz, ws, st);
 }
 
+// ------------------------------------------------------------------ export
+int64_t qe_packed_row_bytes(int64_t p, int bits)
+{
+    if (p < 0 || bad_bits(bits)) return 0;
+    return packed_row_bytes(p, bits);
+}
+
+qe_status qe_pack_codes(const uint8_t* codes, int64_t q, int64_t p, int bits, uint8_t* packed,
+                        void* stream)
+{
+    if (!codes || !packed || bad_dims(q, p) || bad_bits(bits)) return QE_ERR_ARG;
+    return launch_pack_codes(codes, q, p, bits, packed, as_stream(stream));
+}
+
+qe_status qe_outliers_csr(const float* H, int64_t q, int64_t p, const int64_t* support,
+                          const int64_t* nnz, int64_t cap, int64_t* rowptr, int32_t* cols,
+                          float* vals, void* stream)
+{
+    if (!H || !nnz || !rowptr || bad_dims(q, p) || cap < 0) return QE_ERR_ARG;
+    if (cap > 0 && (!support || !cols || !vals)) return QE_ERR_ARG;
+    return launch_outliers_csr(H, q, p, support, nnz, cap, rowptr, cols, vals, as_stream(stream));
+}
+
 // ------------------------------------------------------------------ objective
 size_t qe_objective_workspace_size(int64_t q, int64_t p)
 {

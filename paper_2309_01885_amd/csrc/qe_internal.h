@@ -461,6 +461,12 @@ qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t 
                          float* H, float* E, int64_t s, float lambda, int64_t* support,
                          int64_t* support_nnz, int sweeps, int block, uint32_t flags,
                          double* obj, void* ws, hipStream_t st);
+int64_t packed_row_bytes(int64_t p, int bits);
+qe_status launch_pack_codes(const uint8_t* codes, int64_t q, int64_t p, int bits,
+                            uint8_t* packed, hipStream_t s);
+qe_status launch_outliers_csr(const float* H, int64_t q, int64_t p, const int64_t* support,
+                              const int64_t* nnz, int64_t cap, int64_t* rowptr, int32_t* cols,
+                              float* vals, hipStream_t s);
 size_t lambda_ws_bytes(int64_t p);
 qe_status launch_lambda(const float* Sigma, int64_t p, int max_iters, float tol, float* out,
                         void* ws, hipStream_t s);

@@ -63,6 +63,9 @@ SIGNATURES = {
     "qe_topk_abs": (_int, [_vp, _i64, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "qe_topk_columns_workspace_size": (_sz, [_i64, _i64]),
     "qe_topk_columns": (_int, [_vp, _i64, _i64, _i64, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "qe_packed_row_bytes": (_i64, [_i64, _int]),
+    "qe_pack_codes": (_int, [_vp, _i64, _i64, _int, _vp, _vp]),
+    "qe_outliers_csr": (_int, [_vp, _i64, _i64, _vp, _vp, _i64, _vp, _vp, _vp, _vp]),
     "qe_objective_workspace_size": (_sz, [_i64, _i64]),
     "qe_objective": (_int, [_vp, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _sz, _vp]),
     "qe_lambda_workspace_size": (_sz, [_i64]),
@@ -265,6 +268,34 @@ def topk_columns(V: torch.Tensor, c: int, ws: Optional[torch.Tensor] = None,
            "qe_topk_columns")
     _finish(ws, check, "qe_topk_columns", stream)
     return out, cols, support, nnz
+
+
+# ---------------------------------------------------------------------------- export
+def pack_codes(codes: torch.Tensor, bits: int, stream=None) -> torch.Tensor:
+    """q x p uint8 codes -> q x qe_packed_row_bytes(p, bits) uint8 bit streams."""
+    lib = load()
+    q, p = codes.shape
+    out = torch.empty((q, int(lib.qe_packed_row_bytes(p, bits))), dtype=torch.uint8,
+                      device=codes.device)
+    _check(lib.qe_pack_codes(_ptr(codes, torch.uint8, "codes"), q, p, int(bits),
+                             _vp(out.data_ptr()), _stream(stream)), "qe_pack_codes")
+    return out
+
+
+def outliers_csr(H: torch.Tensor, support: torch.Tensor, nnz: torch.Tensor, stream=None):
+    """CSR (rowptr int64[q+1], cols int32[cap], vals float32[cap]) of the
+    support entries of H; the first nnz entries of cols / vals are valid."""
+    lib = load()
+    q, p = H.shape
+    cap = support.numel()
+    rowptr = torch.empty(q + 1, dtype=torch.int64, device=H.device)
+    cols = torch.empty(max(cap, 1), dtype=torch.int32, device=H.device)
+    vals = torch.empty(max(cap, 1), dtype=torch.float32, device=H.device)
+    _check(lib.qe_outliers_csr(_ptr(H, torch.float32, "H"), q, p,
+                               _ptr(support, torch.int64, "support"), _ptr(nnz, torch.int64, "nnz"),
+                               cap, _vp(rowptr.data_ptr()), _vp(cols.data_ptr()),
+                               _vp(vals.data_ptr()), _stream(stream)), "qe_outliers_csr")
+    return rowptr, cols, vals
 
 
 # ---------------------------------------------------------------------------- objective
