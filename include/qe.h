@@ -46,9 +46,10 @@ typedef int qe_status;
 #define QE_ERR_HIP         5  /* a HIP runtime call failed */
 #define QE_ERR_UNSUPPORTED 6  /* a valid request this build does not implement */
 
-/* Layouts of X for qe_gram. */
+/* Layouts of X for qe_gram, optionally or-ed with QE_GRAM_FP32. */
 #define QE_LAYOUT_PN 0        /* X is p x n: each channel's n tokens contiguous */
 #define QE_LAYOUT_NP 1        /* X is n x p: each token's p channels contiguous */
+#define QE_GRAM_FP32 0x100    /* products on the fp32 matrix cores instead of the split bf16 ones */
 
 /* Flags for qe_cd_sweep / qe_cd_outlier_sweep. */
 #define QE_INIT_FROM_W 0x1u   /* start from What = W (Sec. 4.1) or What = W - H (Sec. 5.3);
@@ -87,8 +88,13 @@ qe_status qe_sync_status(void* ws, void* stream);
  * Sigma: p x p fp32, device; overwritten (accumulate = 0) or added to
  * (accumulate = 1, for token chunks streamed through several calls; pass
  * damp = 0 on all but the last).  The result is exactly symmetric.
- * Accumulation: fp32 matrix-core products over short token chunks, chunk
- * sums added in fp32, split partial sums reduced in fp64.
+ * Products: by default each fp32 value x is split exactly into three bf16
+ * values (h = bf16(x), m = bf16(x - h), l = x - h - m) and x_i x_j is formed
+ * from the six products h h, h m, m h, h l, m m, l h on the bf16 matrix
+ * cores, every product exact in fp32; the dropped terms are below 2^-23
+ * |x_i x_j| (one fp32 rounding).  With QE_GRAM_FP32 the products run on the
+ * fp32 matrix cores.  Accumulation: fp32 over short token chunks, chunk sums
+ * added in fp32, split partial sums reduced in fp64.
  * ------------------------------------------------------------------------ */
 size_t qe_gram_workspace_size(int64_t p, int64_t n);
 qe_status qe_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma,

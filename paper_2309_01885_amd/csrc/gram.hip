@@ -1,4 +1,9 @@
-// Gram matrix Sigma = X X^T on fp32 matrix cores (gfx950).
+// Gram matrix Sigma = X X^T on the matrix cores of gfx950.
+//
+// Products: by default on the bf16 matrix cores, every fp32 operand split
+// exactly into three bf16 values and six bf16 products kept per fp32 product
+// (gram_x3_kernel, see nt_x3.h); with QE_GRAM_FP32 on the fp32 matrix cores
+// (gram_kernel).  Both share the work split and the reductions below.
 //
 // Lemma 1 (Sec. 4.2) needs X only through Sigma, a p x p statistic whose size
 // does not grow with the token count n.  Work split: 128 x 128 tiles of the
@@ -11,6 +16,7 @@
 // tokens with a two-level accumulator (inner sums of 512 tokens added into a
 // second fp32 accumulator) and writes Sigma directly.  The lower triangle is
 // written as an exact mirror through an LDS transpose.
+#include "nt_x3.h"
 #include "qe_internal.h"
 
 namespace qe {
@@ -33,6 +39,32 @@ __device__ inline void tri_index(int64_t t, int64_t nt, int64_t& ti, int64_t& tj
     while (r + 1 < nt && start(r + 1) <= t) ++r;
     ti = r;
     tj = r + (t - start(r));
+}
+
+__device__ inline int64_t tri_row_start(int64_t i, int64_t nt) { return i * nt - i * (i - 1) / 2; }
+
+// Tile t of the upper triangle in banded order: bands of 8 tile rows, each
+// band ordered by tile column, so that consecutive tiles share their row
+// panels (and, within a band, their column panel).
+__device__ inline void band_index(int64_t t, int64_t nt, int64_t& ti, int64_t& tj)
+{
+    int64_t r, c;
+    tri_index(t, nt, r, c);
+    const int64_t b0 = (r / 8) * 8;
+    const int64_t bh = min((int64_t)8, nt - b0);
+    const int64_t u = t - tri_row_start(b0, nt);
+    const int64_t tri = bh * (bh + 1) / 2;
+    if (u < tri) {
+        int64_t m = (int64_t)((sqrt(8.0 * (double)u + 1.0) - 1.0) * 0.5);
+        while (m > 0 && m * (m + 1) / 2 > u) --m;
+        while ((m + 1) * (m + 2) / 2 <= u) ++m;
+        tj = b0 + m;
+        ti = b0 + (u - m * (m + 1) / 2);
+    } else {
+        const int64_t v = u - tri;
+        tj = b0 + bh + v / bh;
+        ti = b0 + v % bh;
+    }
 }
 
 // Writes rows [r0, r0 + nr) of the 128 x 128 tile (held in LDS as rows
@@ -112,6 +144,85 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_kernel(
         zero_acc(acc);
         run(k0, k1);
         float* dst = out + ((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * kTileFloats;
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    dst[acc_row(mi, v) * kTile + acc_col(ni)] = acc[mi][ni][v];
+    }
+}
+
+// The same work on the bf16 matrix cores with the exact three-way split of
+// each fp32 operand (six bf16 products per fp32 product, fp32 accumulation).
+// Work items (tile, split) are dealt to the 8 XCDs in contiguous ranges (the
+// hardware places workgroup b on XCD b % 8), split-major and in banded tile
+// order inside a split, so the workgroups resident on one XCD at a time share
+// their X panels through that XCD's L2.
+// FULL launches (every 128-row panel inside X, every K range a multiple of
+// 32, aligned rows) take the unguarded two-stage-prefetch loop; any other
+// shape takes the guarded loop for every tile.
+template <bool TRANS, bool TWO_LEVEL, bool FULL>
+__global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
+    const float* __restrict__ X, int64_t p, int64_t n, int64_t nt, int64_t tiles,
+    int64_t splits, int64_t split_len, float* __restrict__ out, int accumulate, const int* status)
+{
+    if (failed(status)) return;
+    // the two-level mode also stages the finished 128 x kTStride tile here
+    constexpr int kLds = TWO_LEVEL && kTile * kTStride > kX3LdsDw ? kTile * kTStride : kX3LdsDw;
+    __shared__ __attribute__((aligned(16))) uint32_t lds[kLds];
+    const int64_t items = tiles * splits;
+    const int64_t per = cdiv(items, 8);
+    const int64_t item = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= items) return;                    // uniform: the whole workgroup leaves
+    const int64_t sp = item / tiles;
+    int64_t ti, tj;
+    band_index(item % tiles, nt, ti, tj);
+    const int64_t k0 = sp * split_len;
+    const int64_t k1 = min(n, k0 + split_len);
+
+    f32x16 acc[2][2];
+    auto run = [&](int64_t kb, int64_t ke) {
+        const int64_t K = ke - kb;
+        if constexpr (TRANS) {
+            const X3Col op{X + kb * p, p, p, K};
+            if constexpr (FULL) nt_tile_x3_full(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
+        } else {
+            const X3Row op{X + kb, n, p, K};
+            if constexpr (FULL) nt_tile_x3_full(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
+        }
+    };
+    float* tl = reinterpret_cast<float*>(lds);
+    if constexpr (TWO_LEVEL) {
+        f32x16 outer[2][2];
+        zero_acc(outer);
+        const int64_t inner = (int64_t)kInnerChunks * kKC;
+        for (int64_t kb = k0; kb < k1; kb += inner) {
+            zero_acc(acc);
+            run(kb, min(k1, kb + inner));
+#pragma unroll
+            for (int a = 0; a < 2; ++a)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) outer[a][b] += acc[a][b];
+        }
+        // the K loop ended with a barrier: the stage area is free
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    tl[acc_row(mi, v) * kTStride + acc_col(ni)] = outer[mi][ni][v];
+        __syncthreads();
+        write_symmetric(tl, ti, tj, out, p, accumulate, 0, kTile);
+    } else {
+        zero_acc(acc);
+        run(k0, k1);
+        const int64_t slot = tri_row_start(ti, nt) + (tj - ti);
+        float* dst = out + (sp * tiles + slot) * kTileFloats;
 #pragma unroll
         for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
@@ -203,34 +314,55 @@ qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* S
     const int64_t nt = cdiv(p, kTile);
     const int64_t tiles = nt * (nt + 1) / 2;
     const int64_t splits = gram_splits(p, n);
+    const bool fp32 = (layout & QE_GRAM_FP32) != 0;
+    const bool trans = (layout & ~QE_GRAM_FP32) == QE_LAYOUT_NP;
     // 16-byte loads need an aligned base and a row stride that keeps them aligned
-    const int x_vec4 = aligned16(X) && ((layout == QE_LAYOUT_PN ? n : p) % 4 == 0);
-    const bool trans = layout == QE_LAYOUT_NP;
-    if (splits == 0) {
-        dim3 grid((unsigned)tiles, 1);
-        if (trans)
-            hipLaunchKernelGGL((gram_kernel<true, true>), grid, dim3(256), 0, s, X, p, n, nt, n,
-                               Sigma, accumulate, x_vec4, status);
-        else
-            hipLaunchKernelGGL((gram_kernel<false, true>), grid, dim3(256), 0, s, X, p, n, nt, n,
-                               Sigma, accumulate, x_vec4, status);
-    } else {
-        // split length: a multiple of the K chunk, at most kSplitTokensMax
-        const int64_t split_len = cdiv(cdiv(n, splits), kKC) * kKC;
-        const int64_t used = cdiv(n, split_len);
-        float* parts = reinterpret_cast<float*>(static_cast<char*>(ws) + kStatusBytes);
+    const int x_vec4 = aligned16(X) && ((trans ? p : n) % 4 == 0);
+    // split length: a multiple of the K chunk, at most kSplitTokensMax
+    const int64_t split_len = splits == 0 ? n : cdiv(cdiv(n, splits), kKC) * kKC;
+    const int64_t used = splits == 0 ? 1 : cdiv(n, split_len);
+    float* parts = reinterpret_cast<float*>(static_cast<char*>(ws) + kStatusBytes);
+    float* dst = splits == 0 ? Sigma : parts;
+    if (fp32) {
         dim3 grid((unsigned)tiles, (unsigned)used);
-        if (trans)
-            hipLaunchKernelGGL((gram_kernel<true, false>), grid, dim3(256), 0, s, X, p, n, nt,
-                               split_len, parts, accumulate, x_vec4, status);
-        else
-            hipLaunchKernelGGL((gram_kernel<false, false>), grid, dim3(256), 0, s, X, p, n, nt,
-                               split_len, parts, accumulate, x_vec4, status);
-        if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
-        hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)tiles, kTile / kFinRows), dim3(256), 0, s, parts,
-                           tiles, (int)used, nt, Sigma, p, accumulate, status);
+        if (splits == 0) {
+            if (trans)
+                hipLaunchKernelGGL((gram_kernel<true, true>), grid, dim3(256), 0, s, X, p, n, nt,
+                                   n, Sigma, accumulate, x_vec4, status);
+            else
+                hipLaunchKernelGGL((gram_kernel<false, true>), grid, dim3(256), 0, s, X, p, n, nt,
+                                   n, Sigma, accumulate, x_vec4, status);
+        } else {
+            if (trans)
+                hipLaunchKernelGGL((gram_kernel<true, false>), grid, dim3(256), 0, s, X, p, n, nt,
+                                   split_len, parts, accumulate, x_vec4, status);
+            else
+                hipLaunchKernelGGL((gram_kernel<false, false>), grid, dim3(256), 0, s, X, p, n,
+                                   nt, split_len, parts, accumulate, x_vec4, status);
+        }
+    } else {
+        const unsigned grid = (unsigned)(8 * cdiv(tiles * used, 8));
+        // every panel inside X, every K range a multiple of 32 (split_len is)
+        const bool full = x_vec4 && p % kTile == 0 && n % (2 * kX3KC) == 0;
+#define QE_GRAM_X3(T, L, F)                                                                     \
+    hipLaunchKernelGGL((gram_x3_kernel<T, L, F>), dim3(grid), dim3(256), 0, s, X, p, n, nt, tiles, \
+                       used, split_len, dst, accumulate, status)
+        const bool two = splits == 0;
+        if (trans) {
+            if (two) { if (full) QE_GRAM_X3(true, true, true); else QE_GRAM_X3(true, true, false); }
+            else { if (full) QE_GRAM_X3(true, false, true); else QE_GRAM_X3(true, false, false); }
+        } else {
+            if (two) { if (full) QE_GRAM_X3(false, true, true); else QE_GRAM_X3(false, true, false); }
+            else { if (full) QE_GRAM_X3(false, false, true); else QE_GRAM_X3(false, false, false); }
+        }
+#undef QE_GRAM_X3
     }
     if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+    if (splits != 0) {
+        hipLaunchKernelGGL(gram_finalize_kernel, dim3((unsigned)tiles, kTile / kFinRows), dim3(256),
+                           0, s, parts, tiles, (int)used, nt, Sigma, p, accumulate, status);
+        if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+    }
     if (damp > 0.f) {
         hipLaunchKernelGGL(damp_kernel, dim3(1), dim3(256), 0, s, Sigma, p, damp, status);
         if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;

@@ -1,0 +1,276 @@
+// fp32 NT tile products on the bf16 matrix cores of gfx950 (three-way split).
+//
+// Every fp32 operand x is split exactly into three bf16 values,
+//     h = bf16(x),  m = bf16(x - h),  l = x - h - m     (x = h + m + l),
+// with round-to-nearest-even conversions: x - h and (x - h) - m are exact
+// (Sterbenz), |m| <= 2^-8 |x| and l has at most 8 significant bits, so it is a
+// bf16 value.  The product of two bf16 values is exact in fp32, and
+//     a b = ha hb + (ha mb + ma hb) + (ha lb + ma mb + la hb) + E,
+// where the dropped part E = ma lb + la mb + la lb is below 2^-23 |a b| with a
+// random sign, the size of one fp32 rounding.  The six kept products run as
+// v_mfma_f32_32x32x16_bf16 with fp32 accumulation: six bf16 passes take 6/16
+// of the fp32 matrix-core time of the same tile.
+//
+// Tile geometry as the fp32 NT tile: C[128 x 128] (+)= A[128 x K] B[128 x K]^T,
+// four waves in 2 x 2, each wave a 64 x 64 quarter of 2 x 2 32 x 32 blocks.
+// K runs in stages of 16 through a double-buffered LDS area.  Per operand and
+// stage the LDS holds 128 rows of 24 dwords: the h, m and l planes of the
+// row's 16 values, 8 dwords (two 16-byte halves of 8 values) each.  The half
+// index is XOR-ed with bit 3 of the row, which keeps both the 16-byte operand
+// reads (16 consecutive rows, one half) and the staging writes (8 rows, both
+// halves) free of LDS bank conflicts.  Lane l of a wave reads row l % 32 of a
+// block and half l / 32 for both A and B, so the k order inside a stage is the
+// same on both sides.
+#pragma once
+
+#include "qe_internal.h"
+
+namespace qe {
+
+constexpr int kX3KC = 16;                        // K per stage
+constexpr int kX3RowDw = 24;                     // h, m, l: 8 dwords each
+constexpr int kX3OpDw = kTile * kX3RowDw;        // one operand of one stage
+constexpr int kX3LdsDw = 4 * kX3OpDw;            // A and B, double buffered: 49,152 bytes
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Dword offset of (row, half, plane) inside one operand's stage area.
+__device__ inline int x3_addr(int row, int half, int plane)
+{
+    return row * kX3RowDw + 8 * plane + 4 * (half ^ ((row >> 3) & 1));
+}
+
+// Two floats (a: low half, b: high half) as three packed bf16 pairs h, m, l.
+struct X3Pair { uint32_t h, m, l; };
+__device__ inline X3Pair split3(float a, float b)
+{
+    X3Pair r;
+    r.h = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){a, b}, bf16x2));
+    const float ra = a - __uint_as_float(r.h << 16);
+    const float rb = b - __uint_as_float(r.h & 0xffff0000u);
+    r.m = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){ra, rb}, bf16x2));
+    const float la = ra - __uint_as_float(r.m << 16);
+    const float lb = rb - __uint_as_float(r.m & 0xffff0000u);
+    r.l = __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){la, lb}, bf16x2));
+    return r;
+}
+
+// Staging registers of one operand for one stage (8 floats per thread).
+struct X3Stage { f32x4 v[2]; };
+
+// Row-major operand, element (r, k) at base[r * ld + k].  Thread t stages row
+// t / 2, k = 8 (t % 2) .. +7 (one 16-byte half of each plane).
+struct X3Row {
+    const float* base;
+    int64_t ld, rows, kvalid;
+    // whole stage inside the matrix, 16-byte aligned rows
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const float* src = base + (row0 + (t >> 1)) * ld + k0 + 8 * (t & 1);
+        st.v[0] = *reinterpret_cast<const f32x4*>(src);
+        st.v[1] = *reinterpret_cast<const f32x4*>(src + 4);
+    }
+    // any stage: elements outside rows x kvalid read as 0
+    __device__ inline void load(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int64_t r = row0 + (t >> 1);
+        const int64_t k = k0 + 8 * (t & 1);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            st.v[u >> 2][u & 3] = (r < rows && k + u < kvalid) ? base[r * ld + k + u] : 0.f;
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        u32x4 h, m, l;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const X3Pair q = split3(st.v[u >> 1][2 * (u & 1)], st.v[u >> 1][2 * (u & 1) + 1]);
+            h[u] = q.h;
+            m[u] = q.m;
+            l[u] = q.l;
+        }
+        *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 0)) = h;
+        *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 1)) = m;
+        *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 2)) = l;
+    }
+};
+
+// Transposed operand, element (r, k) at base[k * ld + r] (token-major X).
+// Thread t stages rows 2 (t % 64) and 2 (t % 64) + 1, k = 4 (t / 64) .. +3:
+// the 64 threads of a wave read 512 contiguous bytes per k.
+struct X3Col {
+    const float* base;
+    int64_t ld, rows, kvalid;
+    // whole stage inside the matrix, 8-byte aligned row pairs
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const float* src = base + (k0 + 4 * (t >> 6)) * ld + row0 + 2 * (t & 63);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const f32x2 v = *reinterpret_cast<const f32x2*>(src + u * ld);
+            st.v[0][u] = v[0];
+            st.v[1][u] = v[1];
+        }
+    }
+    __device__ inline void load(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int64_t r = row0 + 2 * (t & 63);
+        const int64_t k = k0 + 4 * (t >> 6);
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+            for (int e = 0; e < 2; ++e)
+                st.v[e][u] = (r + e < rows && k + u < kvalid) ? base[(k + u) * ld + r + e] : 0.f;
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int kq = t >> 6;                   // k = 4 kq .. 4 kq + 3: half kq / 2
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int row = 2 * (t & 63) + e;
+            const X3Pair q0 = split3(st.v[e][0], st.v[e][1]);
+            const X3Pair q1 = split3(st.v[e][2], st.v[e][3]);
+            const int o = x3_addr(row, kq >> 1, 0) + 2 * (kq & 1);
+            *reinterpret_cast<u32x2*>(op + o) = u32x2{q0.h, q1.h};
+            *reinterpret_cast<u32x2*>(op + o + 8) = u32x2{q0.m, q1.m};
+            *reinterpret_cast<u32x2*>(op + o + 16) = u32x2{q0.l, q1.l};
+        }
+    }
+};
+
+// acc[mi][ni] += A(wave rows mi) B(wave cols ni)^T over one staged K = 16.
+__device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t* sB, f32x16 (&acc)[2][2])
+{
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int r = lane & 31, half = lane >> 5;
+    bf16x8 a[2][3], b[2][3];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int pl = 0; pl < 3; ++pl) {
+            a[i][pl] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(sA + x3_addr(wm * 64 + i * 32 + r, half, pl)));
+            b[i][pl] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(sB + x3_addr(wn * 64 + i * 32 + r, half, pl)));
+        }
+    // small terms first; the four accumulators interleave so that no MFMA
+    // waits on the one just issued
+    constexpr int PA[6] = {2, 1, 0, 1, 0, 0};
+    constexpr int PB[6] = {0, 1, 2, 0, 1, 0};
+#pragma unroll
+    for (int q = 0; q < 6; ++q)
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int ni = 0; ni < 2; ++ni)
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[ni][PB[q]],
+                                                                      acc[mi][ni], 0, 0, 0);
+}
+
+// acc += A[row0a.., 0..K) B[row0b.., 0..K)^T for operands whose 128-row panels
+// lie inside the matrix, with K a positive multiple of 32 and aligned rows.
+// Global loads run two stages ahead of the matrix cores; every load is
+// unconditional so that the wait before a stage's LDS store leaves the next
+// stage's loads in flight.  `lds` holds kX3LdsDw dwords.  Ends with a barrier.
+template <class OA, class OB>
+__device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                       int64_t K, uint32_t* lds, f32x16 (&acc)[2][2])
+{
+    uint32_t* const a0 = lds;
+    uint32_t* const b0 = lds + kX3OpDw;
+    uint32_t* const a1 = lds + 2 * kX3OpDw;
+    uint32_t* const b1 = lds + 3 * kX3OpDw;
+    const int64_t nst = K / kX3KC;
+    X3Stage ra0, rb0, ra1, rb1;
+    A.load_full(row0a, 0, ra0);
+    B.load_full(row0b, 0, rb0);
+    A.load_full(row0a, kX3KC, ra1);
+    B.load_full(row0b, kX3KC, rb1);
+    A.store(a0, ra0);
+    B.store(b0, rb0);
+    __syncthreads();
+    for (int64_t c = 0; c + 2 < nst; c += 2) {
+        // LDS 0: stage c; registers 1: stage c + 1; registers 0 take stage c + 2
+        A.load_full(row0a, (c + 2) * kX3KC, ra0);
+        B.load_full(row0b, (c + 2) * kX3KC, rb0);
+        __builtin_amdgcn_sched_barrier(0);
+        x3_mfma_stage(a0, b0, acc);
+        __builtin_amdgcn_sched_barrier(0);
+        A.store(a1, ra1);
+        B.store(b1, rb1);
+        __syncthreads();
+        // LDS 1: stage c + 1; registers 0: stage c + 2; registers 1 take stage c + 3
+        A.load_full(row0a, (c + 3) * kX3KC, ra1);
+        B.load_full(row0b, (c + 3) * kX3KC, rb1);
+        __builtin_amdgcn_sched_barrier(0);
+        x3_mfma_stage(a1, b1, acc);
+        __builtin_amdgcn_sched_barrier(0);
+        A.store(a0, ra0);
+        B.store(b0, rb0);
+        __syncthreads();
+    }
+    x3_mfma_stage(a0, b0, acc);
+    A.store(a1, ra1);
+    B.store(b1, rb1);
+    __syncthreads();
+    x3_mfma_stage(a1, b1, acc);
+    __syncthreads();
+}
+
+// Any shape: guarded loads (out-of-range elements read as 0), one stage of
+// prefetch.  Ends with a barrier.
+template <class OA, class OB>
+__device__ __forceinline__ void nt_tile_x3_edge(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                       int64_t K, uint32_t* lds, f32x16 (&acc)[2][2])
+{
+    uint32_t* const a0 = lds;
+    uint32_t* const b0 = lds + kX3OpDw;
+    uint32_t* const a1 = lds + 2 * kX3OpDw;
+    uint32_t* const b1 = lds + 3 * kX3OpDw;
+    const int64_t nst = cdiv(K, kX3KC);
+    X3Stage sa, sb;
+    A.load(row0a, 0, sa);
+    B.load(row0b, 0, sb);
+    A.store(a0, sa);
+    B.store(b0, sb);
+    __syncthreads();
+    for (int64_t c = 0; c < nst; c += 2) {
+        bool more = c + 1 < nst;
+        if (more) {
+            A.load(row0a, (c + 1) * kX3KC, sa);
+            B.load(row0b, (c + 1) * kX3KC, sb);
+        }
+        x3_mfma_stage(a0, b0, acc);
+        if (more) {
+            A.store(a1, sa);
+            B.store(b1, sb);
+        }
+        __syncthreads();
+        if (!more) break;
+        more = c + 2 < nst;
+        if (more) {
+            A.load(row0a, (c + 2) * kX3KC, sa);
+            B.load(row0b, (c + 2) * kX3KC, sb);
+        }
+        x3_mfma_stage(a1, b1, acc);
+        if (more) {
+            A.store(a0, sa);
+            B.store(b0, sb);
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace qe

@@ -26,6 +26,7 @@ QE_ERR_UNSUPPORTED = 6
 
 QE_LAYOUT_PN = 0
 QE_LAYOUT_NP = 1
+QE_GRAM_FP32 = 0x100
 
 QE_INIT_FROM_W = 0x1
 QE_R_VALID = 0x2
@@ -142,11 +143,15 @@ def _finish(ws, check, where, stream=None):
 # ---------------------------------------------------------------------------- Gram
 def gram(X: torch.Tensor, layout: int = QE_LAYOUT_PN, Sigma: Optional[torch.Tensor] = None,
          accumulate: bool = False, damp: float = 0.0, ws: Optional[torch.Tensor] = None,
-         check: bool = True, stream=None) -> torch.Tensor:
+         check: bool = True, stream=None, fp32: bool = False) -> torch.Tensor:
+    """Sigma (+)= X X^T (qe_gram).  fp32=True selects the fp32 matrix-core
+    products (QE_GRAM_FP32) instead of the exact three-way bf16 split."""
     lib = load()
     if X.dim() != 2:
         raise ValueError("X must be 2-D")
     p, n = (X.shape if layout == QE_LAYOUT_PN else X.shape[::-1])
+    if fp32:
+        layout |= QE_GRAM_FP32
     if Sigma is None:
         Sigma = torch.empty((p, p), dtype=torch.float32, device=X.device)
     need = lib.qe_gram_workspace_size(p, n)

@@ -1,6 +1,9 @@
 """GPU parity of qe_gram (Sigma = X X^T, Lemma 1) against the fp64 oracle.
 
-Bar: relative Frobenius error <= 1e-5; Sigma exactly symmetric."""
+Bar: relative Frobenius error <= 1e-5; Sigma exactly symmetric.  Both product
+paths are covered: the default three-way bf16 split and QE_GRAM_FP32.  Shapes
+with p a multiple of 128 and n a multiple of 32 take the unguarded loop, the
+others the guarded one."""
 import numpy as np
 import pytest
 import torch
@@ -15,25 +18,54 @@ def _gram(qe, X, layout=0, **kw):
     return host(qe.gram(dev(X), layout=layout, **kw))
 
 
-@pytest.mark.parametrize("p,n", [(512, 2048), (200, 1000), (1, 7), (129, 33), (300, 5000)])
-def test_gram_matches_oracle(qe, oracle, p, n):
+@pytest.mark.parametrize("fp32", [False, True])
+@pytest.mark.parametrize("p,n", [(512, 2048), (200, 1000), (1, 7), (129, 33), (300, 5000),
+                                 (384, 4096 + 32), (256, 16)])
+def test_gram_matches_oracle(qe, oracle, p, n, fp32):
     spec = synth.CONFIGS["c1"]
     X = synth.activations(spec, n=n, p=p)
-    S = _gram(qe, X)
+    S = _gram(qe, X, fp32=fp32)
     ref = oracle.gram(X)
     assert rel_fro(S, ref) <= 1e-5
     assert np.array_equal(S, S.T)
 
 
-@pytest.mark.parametrize("p,n", [(256, 1024), (130, 77)])
-def test_gram_token_major_layout(qe, oracle, p, n):
+@pytest.mark.parametrize("fp32", [False, True])
+@pytest.mark.parametrize("p,n", [(256, 1024), (130, 77), (384, 96)])
+def test_gram_token_major_layout(qe, oracle, p, n, fp32):
     X = synth.gaussian((p, n), seed=3)
-    S_pn = _gram(qe, X, 0)
-    S_np = _gram(qe, np.ascontiguousarray(X.T), 1)
+    S_pn = _gram(qe, X, 0, fp32=fp32)
+    S_np = _gram(qe, np.ascontiguousarray(X.T), 1, fp32=fp32)
     ref = oracle.gram(X)
     assert rel_fro(S_np, ref) <= 1e-5
     assert rel_fro(S_np, S_pn) <= 1e-6
     assert np.array_equal(S_np, S_np.T)
+
+
+def test_gram_split_products_exact_on_short_values(qe):
+    """Values with at most 8 significant bits are their own bf16 h part
+    (m = l = 0); with integer products and partial sums below 2^24 every
+    step is exact, so both product paths return the exact integer Gram."""
+    rng = np.random.default_rng(11)
+    X = rng.integers(-15, 16, size=(256, 2048)).astype(np.float32)
+    exact = (X.astype(np.int64) @ X.T.astype(np.int64)).astype(np.float32)
+    assert np.array_equal(_gram(qe, X), exact)
+    assert np.array_equal(_gram(qe, X, fp32=True), exact)
+
+
+def test_gram_split_reconstructs_low_bits(qe, oracle):
+    """x = +-(1 + k 2^-20), k < 16: bf16(x) = +-1, so all of the k part lives in
+    the m plane.  The off-diagonal error must stay far below what the h plane
+    alone would give (the Gram of the signs)."""
+    rng = np.random.default_rng(12)
+    k = rng.integers(0, 16, size=(128, 512)).astype(np.float64)
+    sgn = rng.choice([-1.0, 1.0], size=(128, 512))
+    X = (sgn * (1.0 + k * 2.0 ** -20)).astype(np.float32)
+    ref = oracle.gram(X)
+    off = ~np.eye(128, dtype=bool)
+    err = np.max(np.abs(_gram(qe, X) - ref)[off])
+    gap = np.max(np.abs(oracle.gram(sgn.astype(np.float32)) - ref)[off])
+    assert err <= 0.05 * gap
 
 
 def test_gram_accumulates_token_chunks(qe, oracle):
