@@ -69,6 +69,9 @@ typedef int qe_status;
  * Sec. 5.3): the projection keeps the floor(s / q) whole columns of largest
  * l2 norm instead of the s largest entries (see qe_topk_columns). */
 #define QE_OUTLIER_COLUMNS 0x10u
+/* Block-update and residual products on the fp32 matrix cores instead of the
+ * default exact three-way bf16 split (the split is described at qe_gram). */
+#define QE_CD_FP32 0x20u
 
 /* Human-readable name of a status code (static string). */
 const char* qe_status_string(qe_status s);

@@ -106,7 +106,8 @@ qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, 
 {
     if (!W || !Sigma || !scale || !zero || !W_hat || !codes || !R) return QE_ERR_ARG;
     if (bad_dims(q, p) || bad_bits(bits) || bad_block(block) || sweeps < 0) return QE_ERR_ARG;
-    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_MASK)) return QE_ERR_ARG;
+    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_MASK | QE_CD_FP32))
+        return QE_ERR_ARG;
     if (!ws || ws_bytes < cd_ws_bytes(q, p, block)) return QE_ERR_WORKSPACE;
     hipStream_t s = as_stream(stream);
     if (clear_status(ws, s) != QE_OK) return QE_ERR_HIP;
@@ -133,7 +134,7 @@ qe_status qe_cd_outlier_sweep(const float* W, const float* Sigma, int64_t q, int
     if (bad_dims(q, p) || bad_bits(bits) || bad_block(block) || sweeps < 0) return QE_ERR_ARG;
     if (s < 0 || s > q * p || (s > 0 && !support)) return QE_ERR_ARG;
     if (!(lambda_max > 0.f) || !std::isfinite(lambda_max)) return QE_ERR_ARG;
-    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_OUTLIER_COLUMNS))
+    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_OUTLIER_COLUMNS | QE_CD_FP32))
         return QE_ERR_ARG;
     if (!ws || ws_bytes < outlier_ws_bytes(q, p, block, s)) return QE_ERR_WORKSPACE;
     hipStream_t st = as_stream(stream);

@@ -25,6 +25,7 @@
 // t-1; after the last one a GEMM-only step leaves R = (What - W) Sigma exact.
 #include <utility>
 
+#include "nt_x3.h"
 #include "qe_internal.h"
 
 namespace qe {
@@ -74,7 +75,7 @@ __global__ void init_from_w_kernel(const float* __restrict__ W, const float* __r
 __global__ __launch_bounds__(256, 2) void residual_init_kernel(const float* Wh, const float* H,
                                                             const float* W, const float* Sigma,
                                                             int64_t q, int64_t p, float* R,
-                                                            int vec4, const int* status)
+                                                            int vec4, int fp32, const int* status)
 {
     if (failed(status)) return;
     __shared__ __attribute__((aligned(16))) float lds[kNTLdsFloats];
@@ -82,9 +83,20 @@ __global__ __launch_bounds__(256, 2) void residual_init_kernel(const float* Wh, 
     const int64_t row0 = (blockIdx.x / tn_count) * kTile, col0 = (blockIdx.x % tn_count) * kTile;
     f32x16 acc[2][2];
     zero_acc(acc);
-    const CompOp A{Wh, H, W, p, q, p, vec4 != 0};
-    const RowOp B{Sigma, p, p, p, vec4 != 0};
-    nt_tile(A, row0, B, col0, p, lds, acc);
+    if (fp32) {
+        const CompOp A{Wh, H, W, p, q, p, vec4 != 0};
+        const RowOp B{Sigma, p, p, p, vec4 != 0};
+        nt_tile(A, row0, B, col0, p, lds, acc);
+    } else {
+        // split bf16 products (nt_x3.h)
+        const X3Comp A{Wh, H, W, p, q, p};
+        const X3Row B{Sigma, p, p, p};
+        uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
+        if (vec4 && row0 + kTile <= q && col0 + kTile <= p && p % (2 * kX3KC) == 0)
+            nt_tile_x3_full(A, row0, B, col0, p, l32, acc);
+        else
+            nt_tile_x3_edge(A, row0, B, col0, p, l32, acc);
+    }
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
@@ -168,6 +180,7 @@ struct StepArgs {
     float maxq;
     int codes_valid;      // current codes may be kept on an exact tie (Sec. 4.3)
     int relax;            // write beta unquantized (relaxed sweep, Sec. 4.2)
+    int fp32;             // GEMM role on the fp32 matrix cores (else the split bf16 ones)
     int n_panel;          // workgroups [0, n_panel) run the panel
     int64_t tiles_n;      // GEMM column tiles
     int sig_vec4;
@@ -504,10 +517,21 @@ __device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t
     if (a.sb >= 0 && col0 >= ex0 && min(col0 + kTile, a.p) <= ex1) return;   // all excluded
     f32x16 acc[2][2];
     zero_acc(acc);
-    const RowOp A{a.dprev, a.S, a.q, a.psbw, true};
-    const RowOp Bo{a.Sigma + a.psb, a.p, a.p, a.psbw, a.sig_vec4 != 0};
-    nt_tile(A, row0, Bo, col0, a.psbw, lds, acc);
-    acc_to_lds(acc, lds);                                // nt_tile ended with a barrier
+    if (a.fp32) {
+        const RowOp A{a.dprev, a.S, a.q, a.psbw, true};
+        const RowOp Bo{a.Sigma + a.psb, a.p, a.p, a.psbw, a.sig_vec4 != 0};
+        nt_tile(A, row0, Bo, col0, a.psbw, lds, acc);
+    } else {
+        // split bf16 products (nt_x3.h); Delta rows are 16-byte aligned (stride S)
+        const X3Row A{a.dprev, a.S, a.q, a.psbw};
+        const X3Row Bo{a.Sigma + a.psb, a.p, a.p, a.psbw};
+        uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
+        if (a.sig_vec4 && row0 + kTile <= a.q && col0 + kTile <= a.p && a.psbw % (2 * kX3KC) == 0)
+            nt_tile_x3_full(A, row0, Bo, col0, a.psbw, l32, acc);
+        else
+            nt_tile_x3_edge(A, row0, Bo, col0, a.psbw, l32, acc);
+    }
+    acc_to_lds(acc, lds);                                // the K loop ended with a barrier
     __syncthreads();
     TileRM rv;
     tile_load_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv);
@@ -616,7 +640,7 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     } else if (!(flags & QE_R_VALID)) {
         const int64_t tiles = cdiv(q, kTile) * cdiv(p, kTile);
         hipLaunchKernelGGL(residual_init_kernel, dim3((unsigned)tiles), dim3(256), 0, s, Wh, H, W,
-                           Sigma, q, p, R, vec4 ? 1 : 0, status);
+                           Sigma, q, p, R, vec4 ? 1 : 0, (flags & QE_CD_FP32) ? 1 : 0, status);
     }
     if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
 
@@ -635,6 +659,7 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     base.maxq = (float)((1 << bits) - 1);
     base.sig_vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
     base.r_vec4 = (aligned16(R) && p % 4 == 0) ? 1 : 0;
+    base.fp32 = (flags & QE_CD_FP32) ? 1 : 0;
     base.status = status;
     const bool codes_valid0 = (flags & QE_CODES_VALID) && !(flags & QE_INIT_FROM_W);
     const int period = (int)((flags & QE_RELAX_MASK) >> 8);

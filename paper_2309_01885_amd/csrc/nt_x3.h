@@ -62,8 +62,25 @@ __device__ inline X3Pair split3(float a, float b)
 // Staging registers of one operand for one stage (8 floats per thread).
 struct X3Stage { f32x4 v[2]; };
 
-// Row-major operand, element (r, k) at base[r * ld + k].  Thread t stages row
-// t / 2, k = 8 (t % 2) .. +7 (one 16-byte half of each plane).
+// Splits and stores a stage held as thread t: row t / 2, k = 8 (t % 2) .. +7
+// (one 16-byte half of each plane).
+__device__ inline void x3_store_row8(uint32_t* op, const X3Stage& st)
+{
+    const int t = threadIdx.x;
+    u32x4 h, m, l;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const X3Pair q = split3(st.v[u >> 1][2 * (u & 1)], st.v[u >> 1][2 * (u & 1) + 1]);
+        h[u] = q.h;
+        m[u] = q.m;
+        l[u] = q.l;
+    }
+    *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 0)) = h;
+    *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 1)) = m;
+    *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 2)) = l;
+}
+
+// Row-major operand, element (r, k) at base[r * ld + k], staged as above.
 struct X3Row {
     const float* base;
     int64_t ld, rows, kvalid;
@@ -85,21 +102,44 @@ struct X3Row {
         for (int u = 0; u < 8; ++u)
             st.v[u >> 2][u & 3] = (r < rows && k + u < kvalid) ? base[r * ld + k + u] : 0.f;
     }
-    __device__ inline void store(uint32_t* op, const X3Stage& st) const
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const { x3_store_row8(op, st); }
+};
+
+// Row-major composite operand P1 + P2 - P3 (P2, P3 may be null), e.g.
+// What + H - W, staged as X3Row.
+struct X3Comp {
+    const float *p1, *p2, *p3;
+    int64_t ld, rows, kvalid;
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
     {
         const int t = threadIdx.x;
-        u32x4 h, m, l;
+        const int64_t off = (row0 + (t >> 1)) * ld + k0 + 8 * (t & 1);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const X3Pair q = split3(st.v[u >> 1][2 * (u & 1)], st.v[u >> 1][2 * (u & 1) + 1]);
-            h[u] = q.h;
-            m[u] = q.m;
-            l[u] = q.l;
+        for (int h = 0; h < 2; ++h) {
+            f32x4 v = *reinterpret_cast<const f32x4*>(p1 + off + 4 * h);
+            if (p2) v = v + *reinterpret_cast<const f32x4*>(p2 + off + 4 * h);
+            if (p3) v = v - *reinterpret_cast<const f32x4*>(p3 + off + 4 * h);
+            st.v[h] = v;
         }
-        *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 0)) = h;
-        *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 1)) = m;
-        *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 2)) = l;
     }
+    __device__ inline void load(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int64_t r = row0 + (t >> 1);
+        const int64_t k = k0 + 8 * (t & 1);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            float x = 0.f;
+            if (r < rows && k + u < kvalid) {
+                const int64_t e = r * ld + k + u;
+                x = p1[e];
+                if (p2) x = x + p2[e];
+                if (p3) x = x - p3[e];
+            }
+            st.v[u >> 2][u & 3] = x;
+        }
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const { x3_store_row8(op, st); }
 };
 
 // Transposed operand, element (r, k) at base[k * ld + r] (token-major X).

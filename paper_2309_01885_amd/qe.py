@@ -33,6 +33,7 @@ QE_R_VALID = 0x2
 QE_CODES_VALID = 0x4
 QE_RELAX_MASK = 0xff00
 QE_OUTLIER_COLUMNS = 0x10
+QE_CD_FP32 = 0x20
 
 
 def QE_RELAX_PERIOD(k: int) -> int:

@@ -37,7 +37,8 @@ def test_lambda_max(qe, oracle):
     assert lam == pytest.approx(oracle.lambda_max(S), rel=1e-5)
 
 
-def run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0, block=0):
+def run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0, block=0,
+                    extra=0):
     q, p = W.shape
     Wd, Sd = dev(W), dev(S32)
     Wh = torch.empty_like(Wd)
@@ -48,15 +49,17 @@ def run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0,
     nnz = n0.clone()
     obj = torch.zeros(2 * sweeps, dtype=torch.float64, device="cuda")
     qe.cd_outlier_sweep(Wd, Sd, bits, dev(scale), dev(zero), Wh, codes, H, E, s, lam, sup, nnz,
-                        sweeps, block=block, flags=qe.QE_INIT_FROM_W, obj=obj)
+                        sweeps, block=block, flags=qe.QE_INIT_FROM_W | extra, obj=obj)
     n = int(host(nnz)[0])
     return dict(What=host(Wh), codes=host(codes).astype(np.int32), H=host(H), E=host(E),
                 support=host(sup)[:n], obj=host(obj))
 
 
-@pytest.mark.parametrize("q,p,bits,frac,corr", [(512, 512, 3, 0.01, 0.9), (96, 200, 3, 0.02, 0.5),
-                                                 (130, 257, 2, 0.005, 0.9)])
-def test_outlier_matches_oracle(qe, oracle, q, p, bits, frac, corr):
+@pytest.mark.parametrize("q,p,bits,frac,corr,fp32", [(512, 512, 3, 0.01, 0.9, False),
+                                                      (512, 512, 3, 0.01, 0.9, True),
+                                                      (96, 200, 3, 0.02, 0.5, False),
+                                                      (130, 257, 2, 0.005, 0.9, False)])
+def test_outlier_matches_oracle(qe, oracle, q, p, bits, frac, corr, fp32):
     W = synth.gaussian((q, p), seed=5, std=0.02)
     W.reshape(-1)[::487] *= 10.0
     X = synth.correlated_activations(p, 2048, corr, 6, out_channels=max(1, p // 100),
@@ -74,7 +77,8 @@ def test_outlier_matches_oracle(qe, oracle, q, p, bits, frac, corr):
     assert np.array_equal(host(scale_d), scale) and np.array_equal(host(zero_d), zero)
 
     sweeps = 4
-    g = run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0)
+    g = run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0,
+                        extra=qe.QE_CD_FP32 if fp32 else 0)
     ref = oracle.outlier(W, S32, bits, scale, zero, s, lam, sweeps)
     for k in range(sweeps):
         assert g["obj"][2 * k] == pytest.approx(ref.g_cd[k], rel=1e-4), f"g after CD, it {k + 1}"
