@@ -209,7 +209,8 @@ qe_status qe_topk_columns(const float* V, int64_t q, int64_t p, int64_t c, float
  * calibration error), recomputed from scratch, independent of R:
  *   out[0] = <D, D Sigma> = ||(What + H - W) X||_F^2,  D = What + H - W,
  *   out[1] = <W, W Sigma> = ||W X||_F^2.
- * H may be NULL.  out: device, 2 doubles.
+ * The products D Sigma use the exact three-way bf16 split (see qe_gram);
+ * <D, D Sigma> is summed in fp64.  H may be NULL.  out: device, 2 doubles.
  * ------------------------------------------------------------------------ */
 size_t qe_objective_workspace_size(int64_t q, int64_t p);
 qe_status qe_objective(const float* W, const float* W_hat, const float* H, const float* Sigma,

@@ -188,12 +188,16 @@ struct StepArgs {
     const int* status;
 };
 
+// Per lane, slot m holds block column 16 m + g.  Quantized sweeps keep What
+// fixed during the block and track codes: the new What and the deltas follow
+// from the final codes after the block.
 template <int SLOTS>
 struct PanelState {
     float L[SLOTS];     // residual of the lane's block columns (local copy of R_{i,J})
-    float w[SLOTS];     // What_{i,J}
-    float dl[SLOTS];    // delta of the columns this lane owns
-    float invd[SLOTS];  // 1 / Sigma_jj
+    float w[SLOTS];     // What_{i,J} (relaxed sweeps: updated as the block runs)
+    float u[SLOTS];     // quantized: 1 / (Sigma_jj s_i); relaxed: 1 / Sigma_jj
+    float v[SLOTS];     // quantized: What_ij / s_i + z_i; relaxed: delta of owned columns
+    float k[SLOTS];     // quantized: code of the column (NaN while none is valid)
     float srow[3][SLOTS];   // Sigma rows J, J+1, J+2 (lane's columns), fetched ahead
 };
 
@@ -205,14 +209,19 @@ __device__ __forceinline__ float row_bcast(float v)
 }
 
 // Fetches this lane's entries of Sigma row `row` of the block, from slot FIRST
-// on (float4 granules; earlier slots are no longer needed).
+// on (earlier slots are no longer needed): single floats up to the next float4
+// boundary, then float4 granules.  Loading only live slots matters: a register
+// loaded but dead may be reused at once, which makes the fetch wait.
 template <int SLOTS, int FIRST = 0>
 __device__ __forceinline__ void load_srow(float (&dst)[SLOTS], const float* sS, int row, int g)
 {
     const float* src = sS + row * (16 * SLOTS) + g * SLOTS;
     if constexpr (SLOTS % 4 == 0) {
+        constexpr int A = (FIRST + 3) / 4 * 4;
 #pragma unroll
-        for (int q4 = FIRST / 4; q4 < SLOTS / 4; ++q4) {
+        for (int m = FIRST; m < A; ++m) dst[m] = src[m];
+#pragma unroll
+        for (int q4 = A / 4; q4 < SLOTS / 4; ++q4) {
             const f32x4 v = *reinterpret_cast<const f32x4*>(src + 4 * q4);
 #pragma unroll
             for (int u = 0; u < 4; ++u) dst[4 * q4 + u] = v[u];
@@ -228,8 +237,7 @@ __device__ __forceinline__ void load_srow(float (&dst)[SLOTS], const float* sS, 
 // J + 2 is fetched from LDS while column J's dependent chain runs.
 template <int SLOTS, int J, bool FULL, bool RELAX>
 __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* sS, int g,
-                                           int width, float s, float z, float inv_s,
-                                           float maxq, bool cvalid)
+                                           int width, float s, float z, float maxq)
 {
     constexpr int B = 16 * SLOTS;
     constexpr int M = J / 16, O = J % 16;
@@ -238,23 +246,27 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
     // keep the fetch here: the scheduler would otherwise sink it next to its use
     __builtin_amdgcn_sched_barrier(0);
     const float w = st.w[M];
-    // Lemma 1: unconstrained minimiser, then its position t on the grid
-    const float beta = fmaf(-st.L[M], st.invd[M], w);
-    const float t = fmaf(beta, inv_s, z);
-    // nearest level (half to even), clamped to the finite grid
-    const float kn = __builtin_amdgcn_fmed3f(rintf(t), 0.f, maxq);
-    // modified CD: a valid, equally near current level is kept (its code is
-    // recovered exactly from What: |k - z| <= 255 keeps the error far below 1/2)
-    const float kc = rintf(fmaf(w, inv_s, z));
-    const bool keep = cvalid && fabsf(t - kc) <= fabsf(t - kn);
-    const float k = keep ? kc : kn;
-    // relaxed sweep: the unconstrained minimiser itself
-    const float wn = RELAX ? beta : s * (k - z);
-    const float delta = wn - w;
-    const float db = row_bcast<O>(delta);
     const bool own = g == O;
-    st.w[M] = own ? wn : w;
-    st.dl[M] = own ? delta : st.dl[M];
+    float delta;
+    if constexpr (RELAX) {
+        // relaxed sweep: the unconstrained minimiser of Lemma 1 itself
+        const float beta = fmaf(-st.L[M], st.u[M], w);
+        delta = beta - w;
+        st.w[M] = own ? beta : w;
+        st.v[M] = own ? delta : st.v[M];
+    } else {
+        // Lemma 1's minimiser on the grid axis: t = beta / s + z with
+        // beta = What_ij - R_ij / Sigma_jj
+        const float t = fmaf(-st.L[M], st.u[M], st.v[M]);
+        // nearest level (half to even), clamped to the finite grid
+        const float kn = __builtin_amdgcn_fmed3f(rintf(t), 0.f, maxq);
+        // modified CD: a valid, equally near current level is kept (NaN never is)
+        const float kc = st.k[M];
+        const float k = fabsf(t - kc) <= fabsf(t - kn) ? kc : kn;
+        delta = fmaf(s, k - z, -w);                  // s (k - z) - What_ij
+        st.k[M] = own ? k : kc;
+    }
+    const float db = row_bcast<O>(delta);
     // rank-1 update restricted to the block: L_{i,c} += delta_i Sigma_{j,c}.
     // Slot mm holds columns 16 mm + g; slots below M are finished this block.
 #pragma unroll
@@ -264,12 +276,11 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
 template <int SLOTS, bool FULL, bool RELAX, int... Js>
 __device__ __forceinline__ void panel_run(std::integer_sequence<int, Js...>,
                                           PanelState<SLOTS>& st, const float* sS, int g,
-                                          int width, float s, float z, float inv_s, float maxq,
-                                          bool cvalid)
+                                          int width, float s, float z, float maxq)
 {
     load_srow<SLOTS>(st.srow[0], sS, 0, g);
     if constexpr (16 * SLOTS > 1) load_srow<SLOTS>(st.srow[1], sS, 1, g);
-    (panel_step<SLOTS, Js, FULL, RELAX>(st, sS, g, width, s, z, inv_s, maxq, cvalid), ...);
+    (panel_step<SLOTS, Js, FULL, RELAX>(st, sS, g, width, s, z, maxq), ...);
 }
 
 // Stages Sigma[r0 + k][c0 + c] (k < kw, c < cw; else 0) into LDS with the
@@ -449,6 +460,7 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
         const int64_t j0 = a.sb + (int64_t)sub * B;
         const int width = (int)min((int64_t)B, a.sb + a.sbw - j0);
         PanelState<SLOTS> st;
+        const bool cvalid = a.codes_valid != 0;
 #pragma unroll
         for (int m = 0; m < SLOTS; ++m) {
             const int c = 16 * m + g;
@@ -456,8 +468,17 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
             const int64_t idx = i * p + j0 + c;
             st.L[m] = ok ? a.R[idx] : 0.f;
             st.w[m] = ok ? a.Wh[idx] : 0.f;
-            st.invd[m] = c < width ? a.inv_d[j0 + c] : 0.f;
-            st.dl[m] = 0.f;
+            const float invd = c < width ? a.inv_d[j0 + c] : 0.f;
+            if (a.relax) {
+                st.u[m] = invd;
+                st.v[m] = 0.f;
+            } else {
+                st.u[m] = invd * inv_s;
+                st.v[m] = fmaf(st.w[m], inv_s, z);
+                // the current code is recovered exactly from What (|k - z| <= 255
+                // keeps the rounding error far below 1/2)
+                st.k[m] = cvalid ? rintf(st.v[m]) : __builtin_nanf("");
+            }
         }
         // (1) look-ahead: deltas of the previous super-block, R_{i,J} written back
         if (a.psb >= 0) {
@@ -483,21 +504,29 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
         __syncthreads();
         if (a.relax)
             panel_run<SLOTS, false, true>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s,
-                                          z, inv_s, a.maxq, false);
+                                          z, a.maxq);
         else if (width == B)
             panel_run<SLOTS, true, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s,
-                                          z, inv_s, a.maxq, a.codes_valid != 0);
+                                          z, a.maxq);
         else
             panel_run<SLOTS, false, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width,
-                                           s, z, inv_s, a.maxq, a.codes_valid != 0);
+                                           s, z, a.maxq);
 #pragma unroll
         for (int m = 0; m < SLOTS; ++m) {
             const int c = 16 * m + g;
-            if (rowok && c < width) {
-                a.Wh[i * p + j0 + c] = st.w[m];
-                if (!a.relax) a.codes[i * p + j0 + c] = (uint8_t)rintf(fmaf(st.w[m], inv_s, z));
+            float d;
+            if (a.relax) {
+                d = st.v[m];
+                if (rowok && c < width) a.Wh[i * p + j0 + c] = st.w[m];
+            } else {
+                // the same delta the column's step broadcast
+                d = c < width ? fmaf(s, st.k[m] - z, -st.w[m]) : 0.f;
+                if (rowok && c < width) {
+                    a.Wh[i * p + j0 + c] = s * (st.k[m] - z);
+                    a.codes[i * p + j0 + c] = (uint8_t)st.k[m];
+                }
             }
-            if (rowok) a.dcur[i * a.S + (int64_t)sub * B + c] = st.dl[m];
+            if (rowok) a.dcur[i * a.S + (int64_t)sub * B + c] = d;
         }
         // This block's deltas are read back only by this workgroup (its next
         // blocks), after the __syncthreads() that opens add_block_update: a

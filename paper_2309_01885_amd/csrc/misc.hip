@@ -1,4 +1,5 @@
 // Grid, exact objective and lambda_max kernels (gfx950).
+#include "nt_x3.h"
 #include "qe_internal.h"
 
 namespace qe {
@@ -69,9 +70,14 @@ __global__ __launch_bounds__(256, 2) void quad_form_kernel(const float* p1, cons
     const int64_t row0 = (blockIdx.x / tn_count) * kTile, col0 = (blockIdx.x % tn_count) * kTile;
     f32x16 acc[2][2];
     zero_acc(acc);
-    const CompOp A{p1, p2, p3, p, q, p, vec4 != 0};
-    const RowOp B{Sigma, p, p, p, vec4 != 0};
-    nt_tile(A, row0, B, col0, p, lds, acc);
+    // (D Sigma) tile on the bf16 matrix cores with the exact three-way split
+    const X3Comp A{p1, p2, p3, p, q, p};
+    const X3Row B{Sigma, p, p, p};
+    uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
+    if (vec4 && row0 + kTile <= q && col0 + kTile <= p && p % (2 * kX3KC) == 0)
+        nt_tile_x3_full(A, row0, B, col0, p, l32, acc);
+    else
+        nt_tile_x3_edge(A, row0, B, col0, p, l32, acc);
     double d = 0.0;
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
