@@ -221,14 +221,16 @@ def main():
                "traffic": traffic.get("cd_step_kernel"),
                "avg_launch_s": cd_avg, "flops_per_launch": cd_mfma_flops,
                "products": "bf16, 6 per fp32 product (exact 3-way split)",
-               "fp32_equivalent_tflops": cd_tflops}
+               "fp32_equivalent_tflops": cd_tflops,
+               "fp32_equivalent_frac": cd_tflops / FP32_MFMA_PEAK_TFLOPS}
     roof_gram = {"kernel": "gram_x3_kernel", "bound": "mfma", "achieved": gram_bf16_tflops,
                  "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                  "frac": gram_bf16_tflops / BF16_MFMA_PEAK_TFLOPS,
                  "traffic": traffic.get("gram_x3_kernel"),
                  "call_s": gram_t, "flops_per_call": gram_mfma_flops,
                  "products": "bf16, 6 per fp32 product (exact 3-way split)",
-                 "fp32_equivalent_tflops": gram_tflops}
+                 "fp32_equivalent_tflops": gram_tflops,
+                 "fp32_equivalent_frac": gram_tflops / FP32_MFMA_PEAK_TFLOPS}
     dominant = roof_gram if gram_t > sweeps * sweep_t else roof_cd
 
     result = {

@@ -187,11 +187,11 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
         const int64_t K = ke - kb;
         if constexpr (TRANS) {
             const X3Col op{X + kb * p, p, p, K};
-            if constexpr (FULL) nt_tile_x3_full(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            if constexpr (FULL) nt_tile_x3_full<true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
             else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
         } else {
             const X3Row op{X + kb, n, p, K};
-            if constexpr (FULL) nt_tile_x3_full(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            if constexpr (FULL) nt_tile_x3_full<true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
             else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
         }
     };

@@ -219,12 +219,27 @@ __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t
                                                                       acc[mi][ni], 0, 0, 0);
 }
 
+// Instruction order of one stage when INTERLEAVE is set: the operand reads,
+// then each MFMA followed by four VALU instructions of the next stage's split,
+// then the LDS writes, so that the split runs while the matrix cores work.
+__device__ __forceinline__ void x3_interleave()
+{
+    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);      // DS reads
+#pragma unroll
+    for (int i = 0; i < 24; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // VALU
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, 6, 0);       // DS writes
+}
+
 // acc += A[row0a.., 0..K) B[row0b.., 0..K)^T for operands whose 128-row panels
 // lie inside the matrix, with K a positive multiple of 32 and aligned rows.
 // Global loads run two stages ahead of the matrix cores; every load is
 // unconditional so that the wait before a stage's LDS store leaves the next
 // stage's loads in flight.  `lds` holds kX3LdsDw dwords.  Ends with a barrier.
-template <class OA, class OB>
+// INTERLEAVE pays off in long K loops (the Gram), not in the CD block update.
+template <bool INTERLEAVE = false, class OA, class OB>
 __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                        int64_t K, uint32_t* lds, f32x16 (&acc)[2][2])
 {
@@ -247,18 +262,20 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         B.load_full(row0b, (c + 2) * kX3KC, rb0);
         __builtin_amdgcn_sched_barrier(0);
         x3_mfma_stage(a0, b0, acc);
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a1, ra1);
         B.store(b1, rb1);
+        if constexpr (INTERLEAVE) x3_interleave();
         __syncthreads();
         // LDS 1: stage c + 1; registers 0: stage c + 2; registers 1 take stage c + 3
         A.load_full(row0a, (c + 3) * kX3KC, ra1);
         B.load_full(row0b, (c + 3) * kX3KC, rb1);
         __builtin_amdgcn_sched_barrier(0);
         x3_mfma_stage(a1, b1, acc);
-        __builtin_amdgcn_sched_barrier(0);
+        if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a0, ra0);
         B.store(b0, rb0);
+        if constexpr (INTERLEAVE) x3_interleave();
         __syncthreads();
     }
     x3_mfma_stage(a0, b0, acc);
