@@ -34,7 +34,7 @@ CALIB_COPY_BYTES = 256 << 20
 
 # HIP sources each measured kernel is compiled from
 KERNEL_SOURCES = {
-    "gram_x3_kernel": ["gram.hip", "nt_x3.h", "qe_internal.h"],
+    "gram_x3w_kernel": ["gram.hip", "nt_x3.h", "qe_internal.h"],
     "cd_step_kernel": ["cd.hip", "nt_x3.h", "qe_internal.h"],
 }
 
@@ -223,10 +223,10 @@ def main():
                "products": "bf16, 6 per fp32 product (exact 3-way split)",
                "fp32_equivalent_tflops": cd_tflops,
                "fp32_equivalent_frac": cd_tflops / FP32_MFMA_PEAK_TFLOPS}
-    roof_gram = {"kernel": "gram_x3_kernel", "bound": "mfma", "achieved": gram_bf16_tflops,
+    roof_gram = {"kernel": "gram_x3w_kernel", "bound": "mfma", "achieved": gram_bf16_tflops,
                  "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                  "frac": gram_bf16_tflops / BF16_MFMA_PEAK_TFLOPS,
-                 "traffic": traffic.get("gram_x3_kernel"),
+                 "traffic": traffic.get("gram_x3w_kernel"),
                  "call_s": gram_t, "flops_per_call": gram_mfma_flops,
                  "products": "bf16, 6 per fp32 product (exact 3-way split)",
                  "fp32_equivalent_tflops": gram_tflops,

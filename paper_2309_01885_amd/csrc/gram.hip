@@ -187,11 +187,11 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
         const int64_t K = ke - kb;
         if constexpr (TRANS) {
             const X3Col op{X + kb * p, p, p, K};
-            if constexpr (FULL) nt_tile_x3_full<true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            if constexpr (FULL) nt_tile_x3_full<2, true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
             else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
         } else {
             const X3Row op{X + kb, n, p, K};
-            if constexpr (FULL) nt_tile_x3_full<true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            if constexpr (FULL) nt_tile_x3_full<2, true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
             else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
         }
     };
@@ -231,6 +231,80 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
                 for (int v = 0; v < 16; ++v)
                     dst[acc_row(mi, v) * kTile + acc_col(ni)] = acc[mi][ni][v];
     }
+}
+
+// Split mode on 256 x 256 tiles: one workgroup of eight waves per CU, each
+// wave a 64 x 128 block, so that every staged operand value feeds twice the
+// matrix-core work of the 128 x 128 tile (half the split work, LDS traffic
+// and L2 traffic per product).  Used when every 256-row panel lies inside X
+// (p a multiple of 256, aligned rows, token ranges multiples of 32, p x n
+// layout).  Each wave's 64 x 128 block lies in one 128 x 128 tile of the
+// upper triangle, so the partials use the same slots as gram_x3_kernel and
+// the same finalize.
+constexpr int kWide = 256;
+
+__device__ inline void band_index_wide(int64_t t, int64_t nt, int64_t& ti, int64_t& tj)
+{
+    // bands of 4 tile rows: about the 32 workgroups an XCD holds at a time
+    int64_t r, c;
+    tri_index(t, nt, r, c);
+    const int64_t b0 = (r / 4) * 4;
+    const int64_t bh = min((int64_t)4, nt - b0);
+    const int64_t u = t - tri_row_start(b0, nt);
+    const int64_t tri = bh * (bh + 1) / 2;
+    if (u < tri) {
+        int64_t m = (int64_t)((sqrt(8.0 * (double)u + 1.0) - 1.0) * 0.5);
+        while (m > 0 && m * (m + 1) / 2 > u) --m;
+        while ((m + 1) * (m + 2) / 2 <= u) ++m;
+        tj = b0 + m;
+        ti = b0 + (u - m * (m + 1) / 2);
+    } else {
+        const int64_t v = u - tri;
+        tj = b0 + bh + v / bh;
+        ti = b0 + v % bh;
+    }
+}
+
+__global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
+    const float* __restrict__ X, int64_t n, int64_t ntw, int64_t tiles_w, int64_t nt, int64_t tiles,
+    int64_t splits, int64_t split_len, float* __restrict__ parts, const int* status)
+{
+    if (failed(status)) return;
+    __shared__ __attribute__((aligned(16))) uint32_t lds[4 * kWide * kX3RowDw];
+    const int64_t items = tiles_w * splits;
+    const int64_t per = cdiv(items, 8);
+    const int64_t item = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= items) return;                    // uniform: the whole workgroup leaves
+    const int64_t sp = item / tiles_w;
+    int64_t ti, tj;
+    band_index_wide(item % tiles_w, ntw, ti, tj);
+    const int64_t k0 = sp * split_len;
+    const int64_t K = min(n, k0 + split_len) - k0;
+    f32x16 acc[2][4];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
+    const X3Row op{X + k0, n, 0, K};
+    nt_tile_x3_full<4, true>(op, ti * kWide, op, tj * kWide, K, lds, acc);
+    // wave (wm, wn): rows 64 wm .. of the tile, columns 128 wn ..
+    const int wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int64_t qi = 2 * ti + wm / 2, qj = 2 * tj + wn;
+    if (qi > qj) return;                          // below the diagonal of a diagonal tile
+    float* dst = parts + (sp * tiles + tri_row_start(qi, nt) + (qj - qi)) * kTileFloats;
+    const int lane = threadIdx.x & 63;
+    const int r0 = (wm & 1) * 64;
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                dst[(r0 + 32 * mi + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * kTile + 32 * ni +
+                    (lane & 31)] = acc[mi][ni][v];
 }
 
 // Adds the split partial tiles in fixed split order (fp64) and writes Sigma.
@@ -348,7 +422,13 @@ qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* S
     hipLaunchKernelGGL((gram_x3_kernel<T, L, F>), dim3(grid), dim3(256), 0, s, X, p, n, nt, tiles, \
                        used, split_len, dst, accumulate, status)
         const bool two = splits == 0;
-        if (trans) {
+        if (full && !two && !trans && p % kWide == 0) {
+            const int64_t ntw = p / kWide;
+            const int64_t tiles_w = ntw * (ntw + 1) / 2;
+            hipLaunchKernelGGL(gram_x3w_kernel, dim3((unsigned)(8 * cdiv(tiles_w * used, 8))),
+                               dim3(512), 0, s, X, n, ntw, tiles_w, nt, tiles, used, split_len,
+                               parts, status);
+        } else if (trans) {
             if (two) { if (full) QE_GRAM_X3(true, true, true); else QE_GRAM_X3(true, true, false); }
             else { if (full) QE_GRAM_X3(true, false, true); else QE_GRAM_X3(true, false, false); }
         } else {

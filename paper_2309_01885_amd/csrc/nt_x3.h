@@ -189,64 +189,96 @@ struct X3Col {
 };
 
 // acc[mi][ni] += A(wave rows mi) B(wave cols ni)^T over one staged K = 16.
-__device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t* sB, f32x16 (&acc)[2][2])
+// Waves form a (waves / 2) x 2 grid; wave (wm, wn) owns rows wm * 64 + 32 mi
+// (mi < 2) and columns wn * 32 NB + 32 ni (ni < NB): NB = 2 is the 128 x 128
+// tile of four waves, NB = 4 the 256 x 256 tile of eight waves.
+template <int NB = 2>
+__device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t* sB,
+                                              f32x16 (&acc)[2][NB])
 {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int r = lane & 31, half = lane >> 5;
-    bf16x8 a[2][3], b[2][3];
+    // small terms first
+    constexpr int PA[6] = {2, 1, 0, 1, 0, 0};
+    constexpr int PB[6] = {0, 1, 2, 0, 1, 0};
+    bf16x8 a[2][3];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int pl = 0; pl < 3; ++pl) {
+        for (int pl = 0; pl < 3; ++pl)
             a[i][pl] = __builtin_bit_cast(
                 bf16x8, *reinterpret_cast<const u32x4*>(sA + x3_addr(wm * 64 + i * 32 + r, half, pl)));
-            b[i][pl] = __builtin_bit_cast(
-                bf16x8, *reinterpret_cast<const u32x4*>(sB + x3_addr(wn * 64 + i * 32 + r, half, pl)));
+    if constexpr (NB == 2) {
+        bf16x8 b[2][3];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+                b[i][pl] = __builtin_bit_cast(
+                    bf16x8, *reinterpret_cast<const u32x4*>(sB + x3_addr(wn * 64 + i * 32 + r, half, pl)));
+        // the four accumulators interleave so that no MFMA waits on the one just issued
+#pragma unroll
+        for (int q = 0; q < 6; ++q)
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                for (int ni = 0; ni < 2; ++ni)
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[ni][PB[q]],
+                                                                          acc[mi][ni], 0, 0, 0);
+    } else {
+        // B streamed one 32-column block at a time (register budget)
+#pragma unroll
+        for (int ni = 0; ni < NB; ++ni) {
+            bf16x8 b[3];
+#pragma unroll
+            for (int pl = 0; pl < 3; ++pl)
+                b[pl] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+                                                       sB + x3_addr(wn * 32 * NB + ni * 32 + r, half, pl)));
+#pragma unroll
+            for (int q = 0; q < 6; ++q)
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi)
+                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[PB[q]],
+                                                                          acc[mi][ni], 0, 0, 0);
         }
-    // small terms first; the four accumulators interleave so that no MFMA
-    // waits on the one just issued
-    constexpr int PA[6] = {2, 1, 0, 1, 0, 0};
-    constexpr int PB[6] = {0, 1, 2, 0, 1, 0};
-#pragma unroll
-    for (int q = 0; q < 6; ++q)
-#pragma unroll
-        for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-            for (int ni = 0; ni < 2; ++ni)
-                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[ni][PB[q]],
-                                                                      acc[mi][ni], 0, 0, 0);
+    }
 }
 
 // Instruction order of one stage when INTERLEAVE is set: the operand reads,
-// then each MFMA followed by four VALU instructions of the next stage's split,
-// then the LDS writes, so that the split runs while the matrix cores work.
+// then the MFMAs, each followed by a few VALU instructions of the next stage's
+// split, then the LDS writes, so that the split runs while the matrix cores
+// work.
+template <int NB = 2>
 __device__ __forceinline__ void x3_interleave()
 {
-    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);      // DS reads
+    __builtin_amdgcn_sched_group_barrier(0x100, 6 + 3 * NB, 0);    // DS reads
 #pragma unroll
-    for (int i = 0; i < 24; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);   // VALU
+    for (int i = 0; i < 12 * NB; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);         // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 8 / NB, 0);    // VALU
     }
-    __builtin_amdgcn_sched_group_barrier(0x200, 6, 0);       // DS writes
+    __builtin_amdgcn_sched_group_barrier(0x200, 6, 0);             // DS writes
 }
 
-// acc += A[row0a.., 0..K) B[row0b.., 0..K)^T for operands whose 128-row panels
-// lie inside the matrix, with K a positive multiple of 32 and aligned rows.
+// acc += A[row0a.., 0..K) B[row0b.., 0..K)^T for operands whose 64 NB-row
+// panels lie inside the matrix, with K a positive multiple of 32 and aligned
+// rows (NB = 2: 128 x 128 tile, 256 threads; NB = 4: 256 x 256, 512 threads).
 // Global loads run two stages ahead of the matrix cores; every load is
 // unconditional so that the wait before a stage's LDS store leaves the next
-// stage's loads in flight.  `lds` holds kX3LdsDw dwords.  Ends with a barrier.
-// INTERLEAVE pays off in long K loops (the Gram), not in the CD block update.
-template <bool INTERLEAVE = false, class OA, class OB>
+// stage's loads in flight.  `lds` holds 4 x 64 NB x kX3RowDw dwords.  Ends
+// with a barrier.  INTERLEAVE pays off in long K loops (the Gram), not in the
+// CD block update.
+template <int NB = 2, bool INTERLEAVE = false, class OA, class OB>
 __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
-                                       int64_t K, uint32_t* lds, f32x16 (&acc)[2][2])
+                                       int64_t K, uint32_t* lds, f32x16 (&acc)[2][NB])
 {
+    constexpr int OPDW = 64 * NB * kX3RowDw;
     uint32_t* const a0 = lds;
-    uint32_t* const b0 = lds + kX3OpDw;
-    uint32_t* const a1 = lds + 2 * kX3OpDw;
-    uint32_t* const b1 = lds + 3 * kX3OpDw;
+    uint32_t* const b0 = lds + OPDW;
+    uint32_t* const a1 = lds + 2 * OPDW;
+    uint32_t* const b1 = lds + 3 * OPDW;
     const int64_t nst = K / kX3KC;
     X3Stage ra0, rb0, ra1, rb1;
     A.load_full(row0a, 0, ra0);
@@ -261,28 +293,28 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         A.load_full(row0a, (c + 2) * kX3KC, ra0);
         B.load_full(row0b, (c + 2) * kX3KC, rb0);
         __builtin_amdgcn_sched_barrier(0);
-        x3_mfma_stage(a0, b0, acc);
+        x3_mfma_stage<NB>(a0, b0, acc);
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a1, ra1);
         B.store(b1, rb1);
-        if constexpr (INTERLEAVE) x3_interleave();
+        if constexpr (INTERLEAVE) x3_interleave<NB>();
         __syncthreads();
         // LDS 1: stage c + 1; registers 0: stage c + 2; registers 1 take stage c + 3
         A.load_full(row0a, (c + 3) * kX3KC, ra1);
         B.load_full(row0b, (c + 3) * kX3KC, rb1);
         __builtin_amdgcn_sched_barrier(0);
-        x3_mfma_stage(a1, b1, acc);
+        x3_mfma_stage<NB>(a1, b1, acc);
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a0, ra0);
         B.store(b0, rb0);
-        if constexpr (INTERLEAVE) x3_interleave();
+        if constexpr (INTERLEAVE) x3_interleave<NB>();
         __syncthreads();
     }
-    x3_mfma_stage(a0, b0, acc);
+    x3_mfma_stage<NB>(a0, b0, acc);
     A.store(a1, ra1);
     B.store(b1, rb1);
     __syncthreads();
-    x3_mfma_stage(a1, b1, acc);
+    x3_mfma_stage<NB>(a1, b1, acc);
     __syncthreads();
 }
 

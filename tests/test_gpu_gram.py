@@ -1,9 +1,10 @@
 """GPU parity of qe_gram (Sigma = X X^T, Lemma 1) against the fp64 oracle.
 
 Bar: relative Frobenius error <= 1e-5; Sigma exactly symmetric.  Both product
-paths are covered: the default three-way bf16 split and QE_GRAM_FP32.  Shapes
-with p a multiple of 128 and n a multiple of 32 take the unguarded loop, the
-others the guarded one."""
+paths are covered: the default three-way bf16 split and QE_GRAM_FP32.  Split
+products: p a multiple of 256 with n a multiple of 32 takes the 256 x 256
+tiles, p a multiple of 128 the unguarded 128 x 128 loop, other shapes the
+guarded one."""
 import numpy as np
 import pytest
 import torch
@@ -20,7 +21,7 @@ def _gram(qe, X, layout=0, **kw):
 
 @pytest.mark.parametrize("fp32", [False, True])
 @pytest.mark.parametrize("p,n", [(512, 2048), (200, 1000), (1, 7), (129, 33), (300, 5000),
-                                 (384, 4096 + 32), (256, 16)])
+                                 (384, 4096 + 32), (256, 16), (768, 4096 + 64)])
 def test_gram_matches_oracle(qe, oracle, p, n, fp32):
     spec = synth.CONFIGS["c1"]
     X = synth.activations(spec, n=n, p=p)
