@@ -107,6 +107,9 @@ def main():
     ap.add_argument("--no-outlier", action="store_true", help="skip the outlier-aware timing")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with a plain 256 MiB device copy (HBM counter calibration)")
+    ap.add_argument("--configs", action="store_true",
+                    help="instead of the c2 step: Gram and CD timings of every workload "
+                         "configuration at its full size (one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: --gpus {args.gpus} is not supported "
@@ -117,6 +120,10 @@ def main():
     import torch
     import paper_2309_01885_amd as P
     import synth
+
+    if args.configs:
+        print(json.dumps(configs_bench(P, torch, synth)), flush=True)
+        return
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
@@ -274,6 +281,57 @@ def main():
         b.copy_(a)
         torch.cuda.synchronize()
     print(json.dumps(result), flush=True)
+
+
+def configs_bench(P, torch, synth):
+    """Every workload configuration at its full size: the Gram over all
+    n = 262144 device-drawn tokens (one call when X fits comfortably, else
+    token chunks accumulated into Sigma), damping, the per-row grid and the
+    configured number of CD sweeps from What = W.  Times from HIP events on
+    the library's stream."""
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    out = {}
+    for key in ("c1", "c2", "c3up", "c3down", "c5"):
+        spec = synth.CONFIGS[key]
+        q, p, n = spec.q, spec.p, spec.n
+        log(f"{key}: {q}x{p}, {n} tokens")
+        chunk = n if p * n * 4 <= (16 << 30) else 32768
+        Sigma = torch.empty((p, p), dtype=torch.float32, device=dev)
+        gram_s = 0.0
+        for c in range(n // chunk):
+            Xc = synth.activation_chunk_device(spec, c, chunk, dev)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            P.gram(Xc, Sigma=Sigma, accumulate=c > 0, damp=spec.damp if c == n // chunk - 1 else 0.0)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            gram_s += e0.elapsed_time(e1) * 1e-3
+            del Xc
+        torch.cuda.empty_cache()
+        W = torch.from_numpy(synth.weights(spec)).to(dev)
+        scale, zero = P.grid_minmax(W, spec.bits)
+        Wh = torch.empty_like(W)
+        R = torch.empty_like(W)
+        codes = torch.empty((q, p), dtype=torch.uint8, device=dev)
+        ws = P.workspace(P.cd_workspace_size(q, p, 128), dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        P.cd_sweep(W, Sigma, spec.bits, scale, zero, Wh, codes, R, spec.sweeps, block=128,
+                   flags=P.QE_INIT_FROM_W, ws=ws, check=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        cd_s = e0.elapsed_time(e1) * 1e-3
+        out[spec.name] = {"q": q, "p": p, "n": n, "bits": spec.bits, "sweeps": spec.sweeps,
+                          "gram_s": gram_s, "gram_chunks": n // chunk,
+                          "gram_fp32_equivalent_tflops": float(p) * (p + 1) * n / gram_s / 1e12,
+                          "sweep_s": cd_s / spec.sweeps,
+                          "cd_fp32_equivalent_tflops": 2.0 * q * p * p * spec.sweeps / cd_s / 1e12,
+                          "layer_s": gram_s + cd_s,
+                          "column_updates_per_s": p * spec.sweeps / (gram_s + cd_s)}
+        del Sigma, W, Wh, R, codes, ws
+        torch.cuda.empty_cache()
+    return {"configs": out}
 
 
 def outlier_bench(P, torch, synth, W, Sigma, dev, block):
