@@ -560,10 +560,12 @@ __device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t
         else
             nt_tile_x3_edge(A, row0, Bo, col0, a.psbw, l32, acc);
     }
-    acc_to_lds(acc, lds);                                // the K loop ended with a barrier
-    __syncthreads();
+    // R's tile is fetched before the accumulators pass through LDS, which
+    // hides part of its latency
     TileRM rv;
     tile_load_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv);
+    acc_to_lds(acc, lds);                                // the K loop ended with a barrier
+    __syncthreads();
     tile_add_store_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv, lds, ex0, ex1);
 }
 
