@@ -69,12 +69,14 @@ def test_gram_split_reconstructs_low_bits(qe, oracle):
     assert err <= 0.05 * gap
 
 
-def test_gram_accumulates_token_chunks(qe, oracle):
-    X = synth.gaussian((320, 3000), seed=4)
-    Sigma = torch.empty((320, 320), dtype=torch.float32, device="cuda")
-    qe.gram(dev(X[:, :1000]), Sigma=Sigma)
-    qe.gram(dev(X[:, 1000:2100]), Sigma=Sigma, accumulate=True)
-    qe.gram(dev(X[:, 2100:]), Sigma=Sigma, accumulate=True, damp=0.01)
+@pytest.mark.parametrize("p,cuts", [(320, (1000, 2100)), (512, (1024, 2048 + 512))])
+def test_gram_accumulates_token_chunks(qe, oracle, p, cuts):
+    X = synth.gaussian((p, 3000 if p == 320 else 4096), seed=4)
+    a, b = cuts
+    Sigma = torch.empty((p, p), dtype=torch.float32, device="cuda")
+    qe.gram(dev(X[:, :a]), Sigma=Sigma)
+    qe.gram(dev(X[:, a:b]), Sigma=Sigma, accumulate=True)
+    qe.gram(dev(X[:, b:]), Sigma=Sigma, accumulate=True, damp=0.01)
     ref = oracle.damp(oracle.gram(X), 0.01)
     S = host(Sigma)
     assert rel_fro(S, ref) <= 1e-5
