@@ -265,9 +265,16 @@ __device__ inline void band_index_wide(int64_t t, int64_t nt, int64_t& ti, int64
     }
 }
 
+// DIRECT: one token range per launch (n <= kSplitTokensMax, a single fp32
+// running sum), written to Sigma itself (with accumulate) through the same
+// LDS-transposed symmetric writes as the two-level mode, 128 x 128 quadrant
+// by quadrant; the large-p replacement of the two-level mode for streamed
+// token chunks.
+template <bool DIRECT>
 __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
-    const float* __restrict__ X, int64_t n, int64_t ntw, int64_t tiles_w, int64_t nt, int64_t tiles,
-    int64_t splits, int64_t split_len, float* __restrict__ parts, const int* status)
+    const float* __restrict__ X, int64_t p, int64_t n, int64_t ntw, int64_t tiles_w, int64_t nt,
+    int64_t tiles, int64_t splits, int64_t split_len, float* __restrict__ out, int accumulate,
+    const int* status)
 {
     if (failed(status)) return;
     __shared__ __attribute__((aligned(16))) uint32_t lds[4 * kWide * kX3RowDw];
@@ -293,10 +300,34 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
     const int wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
     const int64_t qi = 2 * ti + wm / 2, qj = 2 * tj + wn;
-    if (qi > qj) return;                          // below the diagonal of a diagonal tile
-    float* dst = parts + (sp * tiles + tri_row_start(qi, nt) + (qj - qi)) * kTileFloats;
     const int lane = threadIdx.x & 63;
     const int r0 = (wm & 1) * 64;
+    if constexpr (DIRECT) {
+        // the K loop ended with a barrier: its LDS holds a 128 x kTStride tile
+        float* tl = reinterpret_cast<float*>(lds);
+#pragma unroll 1
+        for (int quad = 0; quad < 4; ++quad) {
+            const int a = quad >> 1, b = quad & 1;          // rows 128 a.., columns 128 b..
+            const int64_t gi = 2 * ti + a, gj = 2 * tj + b;
+            if (gi > gj) continue;                           // uniform across the workgroup
+            if (wm / 2 == a && wn == b) {
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+                    for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v)
+                            tl[(r0 + 32 * mi + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * kTStride +
+                               32 * ni + (lane & 31)] = acc[mi][ni][v];
+            }
+            __syncthreads();
+            write_symmetric(tl, gi, gj, out, p, accumulate, 0, kTile);
+            __syncthreads();
+        }
+        return;
+    }
+    if (qi > qj) return;                          // below the diagonal of a diagonal tile
+    float* dst = out + (sp * tiles + tri_row_start(qi, nt) + (qj - qi)) * kTileFloats;
 #pragma unroll
     for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
@@ -422,12 +453,16 @@ qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* S
     hipLaunchKernelGGL((gram_x3_kernel<T, L, F>), dim3(grid), dim3(256), 0, s, X, p, n, nt, tiles, \
                        used, split_len, dst, accumulate, status)
         const bool two = splits == 0;
-        if (full && !two && !trans && p % kWide == 0) {
+        if (full && !trans && p % kWide == 0 && (!two || n <= kSplitTokensMax)) {
             const int64_t ntw = p / kWide;
             const int64_t tiles_w = ntw * (ntw + 1) / 2;
-            hipLaunchKernelGGL(gram_x3w_kernel, dim3((unsigned)(8 * cdiv(tiles_w * used, 8))),
-                               dim3(512), 0, s, X, n, ntw, tiles_w, nt, tiles, used, split_len,
-                               parts, status);
+            const dim3 grid((unsigned)(8 * cdiv(tiles_w * used, 8)));
+            if (two)
+                hipLaunchKernelGGL(gram_x3w_kernel<true>, grid, dim3(512), 0, s, X, p, n, ntw,
+                                   tiles_w, nt, tiles, (int64_t)1, n, Sigma, accumulate, status);
+            else
+                hipLaunchKernelGGL(gram_x3w_kernel<false>, grid, dim3(512), 0, s, X, p, n, ntw,
+                                   tiles_w, nt, tiles, used, split_len, parts, accumulate, status);
         } else if (trans) {
             if (two) { if (full) QE_GRAM_X3(true, true, true); else QE_GRAM_X3(true, true, false); }
             else { if (full) QE_GRAM_X3(true, false, true); else QE_GRAM_X3(true, false, false); }
