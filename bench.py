@@ -113,7 +113,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: --gpus {args.gpus} is not supported "
-              "(the CD sweep shards by rows with no communication; see DESIGN.md)",
+              "(the CD sweep would shard by rows with no communication)",
               file=sys.stderr)
         sys.exit(2)
 

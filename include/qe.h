@@ -44,7 +44,7 @@ typedef int qe_status;
 #define QE_ERR_SCALE       3  /* some grid scale <= 0 or not finite */
 #define QE_ERR_WORKSPACE   4  /* workspace null or smaller than the size query */
 #define QE_ERR_HIP         5  /* a HIP runtime call failed */
-#define QE_ERR_UNSUPPORTED 6  /* a valid request this build does not implement */
+#define QE_ERR_UNSUPPORTED 6  /* a valid request this library does not implement */
 
 /* Layouts of X for qe_gram, optionally or-ed with QE_GRAM_FP32. */
 #define QE_LAYOUT_PN 0        /* X is p x n: each channel's n tokens contiguous */
