@@ -7,14 +7,15 @@
 //
 // Lemma 1 (Sec. 4.2) needs X only through Sigma, a p x p statistic whose size
 // does not grow with the token count n.  Work split: 128 x 128 tiles of the
-// upper triangle (ti <= tj) x token splits of at most kSplitTokens tokens.
+// upper triangle (ti <= tj) x token splits of at most kSplitTokensMax tokens,
+// their count chosen to fill the last round of workgroups (gram_splits).
 // Each workgroup sums its split in the fp32 matrix-core accumulators (a
-// running sum of <= 16384 products: ~3e-7 relative error at this workload's
-// statistics), writes the partial tile to the workspace, and a finalize kernel
-// adds the splits in a fixed order in fp64.  When the split partials would
-// not fit the workspace budget (very large p), one workgroup per tile sums all
-// tokens with a two-level accumulator (inner sums of 512 tokens added into a
-// second fp32 accumulator) and writes Sigma directly.  The lower triangle is
+// running sum of at most 32768 products), writes the partial tile to the
+// workspace, and a finalize kernel adds the splits in a fixed order in fp64.
+// When the split partials would not fit the workspace budget (very large p),
+// one workgroup per tile sums all tokens with a two-level accumulator (inner
+// sums of 512 tokens added into a second fp32 accumulator) and writes Sigma
+// directly.  The lower triangle is
 // written as an exact mirror through an LDS transpose.
 #include "nt_x3.h"
 #include "qe_internal.h"
@@ -22,7 +23,6 @@
 namespace qe {
 
 constexpr int kInnerChunks = 16;          // two-level mode: 16 x 32 = 512 tokens per inner sum
-constexpr int64_t kSplitTokens = 16384;   // split mode: preferred tokens per workgroup
 constexpr int64_t kSplitTokensMax = 32768;  // longest single fp32 running sum allowed
 constexpr size_t kSplitBudget = size_t(2) << 30;   // bytes of split partials allowed
 constexpr int kTileFloats = kTile * kTile;
@@ -392,16 +392,44 @@ __global__ __launch_bounds__(256) void damp_kernel(float* Sigma, int64_t p, floa
     for (int64_t j = threadIdx.x; j < p; j += blockDim.x) Sigma[j * p + j] += add;
 }
 
-// Number of token splits (each <= kSplitTokens), or 0 for the two-level direct mode.
+// Number of token splits, or 0 for the two-level direct mode.
+//
+// The tile kernels hold one workgroup per slot (256 slots for the 256 x 256
+// tiles at one workgroup per CU, 512 for the 128 x 128 tiles at two, on the 256
+// CUs of the MI355X), so a launch of items = tiles x splits workgroups of
+// ceil(n / splits) tokens takes ceil(items / slots) rounds.  The count chosen
+// minimises, in units of one workgroup's time per token, rounds x (tokens per
+// split + a fixed cost per workgroup) + the finalize's reads of the partials,
+// over the counts whose splits hold at most kSplitTokensMax tokens and whose
+// partials fit kSplitBudget; ties keep the fewer splits.  Depends only on (p, n).
+constexpr int64_t kGramSlotsWide = 256, kGramSlotsNarrow = 512;
+constexpr double kGramWgCostTokens = 32.0;        // prologue, pipeline fill, partial-tile store
+constexpr double kGramFinalizeTokensPerTile = 0.11;   // one 64 KB partial tile read in finalize
+
 static int64_t gram_splits(int64_t p, int64_t n)
 {
     const int64_t nt = cdiv(p, kTile);
     const int64_t tiles = nt * (nt + 1) / 2;
-    for (int64_t len = kSplitTokens; len <= kSplitTokensMax; len *= 2) {
-        const int64_t s = cdiv(n, len);
-        if ((size_t)s * tiles * kTileFloats * sizeof(float) <= kSplitBudget) return s;
+    const bool wide = p % kWide == 0;
+    const int64_t items = wide ? (p / kWide) * (p / kWide + 1) / 2 : tiles;
+    const int64_t slots = wide ? kGramSlotsWide : kGramSlotsNarrow;
+    const int64_t s_min = cdiv(n, kSplitTokensMax);
+    const int64_t s_max = std::min<int64_t>(
+        (int64_t)(kSplitBudget / ((size_t)tiles * kTileFloats * sizeof(float))), cdiv(n, kKC));
+    if (s_min > s_max) return 0;
+    int64_t best = s_min;
+    double best_cost = 0.0;
+    for (int64_t sp = s_min; sp <= s_max; ++sp) {
+        const int64_t len = cdiv(cdiv(n, sp), kKC) * kKC;
+        const int64_t used = cdiv(n, len);
+        const double cost = (double)cdiv(items * used, slots) * ((double)len + kGramWgCostTokens) +
+                            kGramFinalizeTokensPerTile * (double)(used * tiles);
+        if (sp == s_min || cost < best_cost) {
+            best = sp;
+            best_cost = cost;
+        }
     }
-    return 0;
+    return best;
 }
 
 size_t gram_ws_bytes(int64_t p, int64_t n)
