@@ -187,11 +187,11 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
         const int64_t K = ke - kb;
         if constexpr (TRANS) {
             const X3Col op{X + kb * p, p, p, K};
-            if constexpr (FULL) nt_tile_x3_full<2, true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            if constexpr (FULL) nt_tile_x3_full<true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
             else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
         } else {
             const X3Row op{X + kb, n, p, K};
-            if constexpr (FULL) nt_tile_x3_full<2, true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
+            if constexpr (FULL) nt_tile_x3_full<true>(op, ti * kTile, op, tj * kTile, K, lds, acc);
             else nt_tile_x3_edge(op, ti * kTile, op, tj * kTile, K, lds, acc);
         }
     };
@@ -236,9 +236,10 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
 // Split mode on 256 x 256 tiles: one workgroup of eight waves per CU, each
 // wave a 64 x 128 block, so that every staged operand value feeds twice the
 // matrix-core work of the 128 x 128 tile (half the split work, LDS traffic
-// and L2 traffic per product).  Used when every 256-row panel lies inside X
-// (p a multiple of 256, aligned rows, token ranges multiples of 32, p x n
-// layout).  Each wave's 64 x 128 block lies in one 128 x 128 tile of the
+// and L2 traffic per product), with the operand reads pipelined through three
+// LDS stage buffers (nt_tile_x3_wide).  Used when every 256-row panel lies
+// inside X (p a multiple of 256, aligned rows, token ranges multiples of 32,
+// p x n layout).  Each wave's 64 x 128 block lies in one 128 x 128 tile of the
 // upper triangle, so the partials use the same slots as gram_x3_kernel and
 // the same finalize.
 constexpr int kWide = 256;
@@ -277,7 +278,7 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
     const int* status)
 {
     if (failed(status)) return;
-    __shared__ __attribute__((aligned(16))) uint32_t lds[4 * kWide * kX3RowDw];
+    __shared__ __attribute__((aligned(16))) uint32_t lds[kX3wLdsDw];
     const int64_t items = tiles_w * splits;
     const int64_t per = cdiv(items, 8);
     const int64_t item = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
@@ -295,7 +296,7 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
     const X3Row op{X + k0, n, 0, K};
-    nt_tile_x3_full<4, true>(op, ti * kWide, op, tj * kWide, K, lds, acc);
+    nt_tile_x3_wide(op, ti * kWide, op, tj * kWide, K, lds, acc);
     // wave (wm, wn): rows 64 wm .. of the tile, columns 128 wn ..
     const int wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;

@@ -188,13 +188,11 @@ struct X3Col {
     }
 };
 
-// acc[mi][ni] += A(wave rows mi) B(wave cols ni)^T over one staged K = 16.
-// Waves form a (waves / 2) x 2 grid; wave (wm, wn) owns rows wm * 64 + 32 mi
-// (mi < 2) and columns wn * 32 NB + 32 ni (ni < NB): NB = 2 is the 128 x 128
-// tile of four waves, NB = 4 the 256 x 256 tile of eight waves.
-template <int NB = 2>
+// acc[mi][ni] += A(wave rows mi) B(wave cols ni)^T over one staged K = 16 of
+// the 128 x 128 tile: waves form a 2 x 2 grid, wave (wm, wn) owns rows
+// wm * 64 + 32 mi and columns wn * 64 + 32 ni (mi, ni < 2).
 __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t* sB,
-                                              f32x16 (&acc)[2][NB])
+                                              f32x16 (&acc)[2][2])
 {
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
@@ -203,78 +201,57 @@ __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t
     // small terms first
     constexpr int PA[6] = {2, 1, 0, 1, 0, 0};
     constexpr int PB[6] = {0, 1, 2, 0, 1, 0};
-    bf16x8 a[2][3];
+    bf16x8 a[2][3], b[2][3];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
         for (int pl = 0; pl < 3; ++pl)
             a[i][pl] = __builtin_bit_cast(
                 bf16x8, *reinterpret_cast<const u32x4*>(sA + x3_addr(wm * 64 + i * 32 + r, half, pl)));
-    if constexpr (NB == 2) {
-        bf16x8 b[2][3];
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-            for (int pl = 0; pl < 3; ++pl)
-                b[i][pl] = __builtin_bit_cast(
-                    bf16x8, *reinterpret_cast<const u32x4*>(sB + x3_addr(wn * 64 + i * 32 + r, half, pl)));
-        // the four accumulators interleave so that no MFMA waits on the one just issued
+        for (int pl = 0; pl < 3; ++pl)
+            b[i][pl] = __builtin_bit_cast(
+                bf16x8, *reinterpret_cast<const u32x4*>(sB + x3_addr(wn * 64 + i * 32 + r, half, pl)));
+    // the four accumulators interleave so that no MFMA waits on the one just issued
 #pragma unroll
-        for (int q = 0; q < 6; ++q)
+    for (int q = 0; q < 6; ++q)
 #pragma unroll
-            for (int mi = 0; mi < 2; ++mi)
+        for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
-                for (int ni = 0; ni < 2; ++ni)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[ni][PB[q]],
-                                                                          acc[mi][ni], 0, 0, 0);
-    } else {
-        // B streamed one 32-column block at a time (register budget)
-#pragma unroll
-        for (int ni = 0; ni < NB; ++ni) {
-            bf16x8 b[3];
-#pragma unroll
-            for (int pl = 0; pl < 3; ++pl)
-                b[pl] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
-                                                       sB + x3_addr(wn * 32 * NB + ni * 32 + r, half, pl)));
-#pragma unroll
-            for (int q = 0; q < 6; ++q)
-#pragma unroll
-                for (int mi = 0; mi < 2; ++mi)
-                    acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[PB[q]],
-                                                                          acc[mi][ni], 0, 0, 0);
-        }
-    }
+            for (int ni = 0; ni < 2; ++ni)
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[ni][PB[q]],
+                                                                      acc[mi][ni], 0, 0, 0);
 }
 
 // Instruction order of one stage when INTERLEAVE is set: the operand reads,
 // then the MFMAs, each followed by a few VALU instructions of the next stage's
 // split, then the LDS writes, so that the split runs while the matrix cores
 // work.
-template <int NB = 2>
 __device__ __forceinline__ void x3_interleave()
 {
-    __builtin_amdgcn_sched_group_barrier(0x100, 6 + 3 * NB, 0);    // DS reads
+    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);            // DS reads
 #pragma unroll
-    for (int i = 0; i < 12 * NB; ++i) {
+    for (int i = 0; i < 24; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);         // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 8 / NB, 0);    // VALU
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);         // VALU
     }
     __builtin_amdgcn_sched_group_barrier(0x200, 6, 0);             // DS writes
 }
 
-// acc += A[row0a.., 0..K) B[row0b.., 0..K)^T for operands whose 64 NB-row
-// panels lie inside the matrix, with K a positive multiple of 32 and aligned
-// rows (NB = 2: 128 x 128 tile, 256 threads; NB = 4: 256 x 256, 512 threads).
-// Global loads run two stages ahead of the matrix cores; every load is
-// unconditional so that the wait before a stage's LDS store leaves the next
-// stage's loads in flight.  `lds` holds 4 x 64 NB x kX3RowDw dwords.  Ends
-// with a barrier.  INTERLEAVE pays off in long K loops (the Gram), not in the
-// CD block update.
-template <int NB = 2, bool INTERLEAVE = false, class OA, class OB>
+// acc += A[row0a.., 0..K) B[row0b.., 0..K)^T on the 128 x 128 tile of 256
+// threads for operands whose 128-row panels lie inside the matrix, with K a
+// positive multiple of 32 and aligned rows.  Global loads run two stages ahead
+// of the matrix cores; every load is unconditional so that the wait before a
+// stage's LDS store leaves the next stage's loads in flight.  `lds` holds
+// kX3LdsDw dwords.  Ends with a barrier.  INTERLEAVE pays off in long K loops
+// (the Gram), not in the CD block update.
+template <bool INTERLEAVE = false, class OA, class OB>
 __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
-                                       int64_t K, uint32_t* lds, f32x16 (&acc)[2][NB])
+                                       int64_t K, uint32_t* lds, f32x16 (&acc)[2][2])
 {
-    constexpr int OPDW = 64 * NB * kX3RowDw;
+    constexpr int OPDW = kX3OpDw;
     uint32_t* const a0 = lds;
     uint32_t* const b0 = lds + OPDW;
     uint32_t* const a1 = lds + 2 * OPDW;
@@ -293,28 +270,28 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         A.load_full(row0a, (c + 2) * kX3KC, ra0);
         B.load_full(row0b, (c + 2) * kX3KC, rb0);
         __builtin_amdgcn_sched_barrier(0);
-        x3_mfma_stage<NB>(a0, b0, acc);
+        x3_mfma_stage(a0, b0, acc);
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a1, ra1);
         B.store(b1, rb1);
-        if constexpr (INTERLEAVE) x3_interleave<NB>();
+        if constexpr (INTERLEAVE) x3_interleave();
         __syncthreads();
         // LDS 1: stage c + 1; registers 0: stage c + 2; registers 1 take stage c + 3
         A.load_full(row0a, (c + 3) * kX3KC, ra1);
         B.load_full(row0b, (c + 3) * kX3KC, rb1);
         __builtin_amdgcn_sched_barrier(0);
-        x3_mfma_stage<NB>(a1, b1, acc);
+        x3_mfma_stage(a1, b1, acc);
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a0, ra0);
         B.store(b0, rb0);
-        if constexpr (INTERLEAVE) x3_interleave<NB>();
+        if constexpr (INTERLEAVE) x3_interleave();
         __syncthreads();
     }
-    x3_mfma_stage<NB>(a0, b0, acc);
+    x3_mfma_stage(a0, b0, acc);
     A.store(a1, ra1);
     B.store(b1, rb1);
     __syncthreads();
-    x3_mfma_stage<NB>(a1, b1, acc);
+    x3_mfma_stage(a1, b1, acc);
     __syncthreads();
 }
 
@@ -362,4 +339,172 @@ __device__ __forceinline__ void nt_tile_x3_edge(const OA& A, int64_t row0a, cons
     }
 }
 
+// 256 x 256 tile of eight waves (wave (wm, wn) owns rows wm * 64 + 32 mi,
+// mi < 2, and columns wn * 128 + 32 ni, ni < 4): every staged value feeds
+// twice the matrix-core work of the 128 x 128 tile.  Three LDS stage buffers
+// let each wave read the next stage's operand fragments while the current
+// stage's MFMAs run: B fragments one 32-column block ahead, A fragments right
+// after their last use in the stage's final block.  One barrier per stage,
+// placed after the stage's LDS writes and its last reads of the current
+// buffer.  Global loads run three stages ahead of the matrix cores (four
+// register stages would not fit beside the 128 accumulators).
+constexpr int kX3wOpDw = 256 * kX3RowDw;          // one operand of one stage
+constexpr int kX3wBufDw = 2 * kX3wOpDw;           // A and B of one stage
+constexpr int kX3wLdsDw = 3 * kX3wBufDw;          // three stages: 147,456 bytes
+
+__device__ __forceinline__ bf16x8 x3w_frag(const uint32_t* p)
+{
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p));
+}
+
+// One 32-column block ni of one stage: products lh, mh, mm, hh, hm, hl (A
+// planes l, m, m, h, h, h), two MFMAs (mi = 0, 1) each.
+__device__ __forceinline__ void x3w_block(const bf16x8 (&a)[2][3], const bf16x8 (&b)[3],
+                                          f32x16 (&acc)[2][4], int ni)
+{
+    constexpr int PA[6] = {2, 1, 1, 0, 0, 0};
+    constexpr int PB[6] = {0, 0, 1, 0, 1, 2};
+#pragma unroll
+    for (int q = 0; q < 6; ++q)
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[PB[q]],
+                                                                  acc[mi][ni], 0, 0, 0);
+}
+
+// Stage c of the 256 x 256 tile: multiplies the fragments of `cur` (fa and
+// fb[0] arrive holding A and B block 0), splits and writes stage c + 2 from
+// (ga, gb) to `wr`, loads stage kload into (la, lb), and leaves fa and fb[0]
+// holding the fragments of `nxt` (stage c + 1).
+template <class OA, class OB>
+__device__ __forceinline__ void x3w_stage(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                          int64_t kload, const uint32_t* cur, const uint32_t* nxt,
+                                          uint32_t* wr, X3Stage& ga, X3Stage& gb, X3Stage& la, X3Stage& lb,
+                                          int offa, int offb, bf16x8 (&fa)[2][3], bf16x8 (&fb)[2][3],
+                                          f32x16 (&acc)[2][4])
+{
+    // group 0: global loads, B block 1 reads, split of A (stage c + 2)
+    A.load_full(row0a, kload, la);
+    B.load_full(row0b, kload, lb);
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl) fb[1][pl] = x3w_frag(cur + offb + 1 * 32 * kX3RowDw + 8 * pl);
+    x3w_block(fa, fb[0], acc, 0);
+    A.store(wr, ga);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);     // VMEM reads
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);     // DS reads
+#pragma unroll
+    for (int i = 0; i < 12; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, 3, 0);     // DS writes
+    __builtin_amdgcn_sched_barrier(0);
+    // group 1: B block 2 reads, split of B
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl) fb[0][pl] = x3w_frag(cur + offb + 2 * 32 * kX3RowDw + 8 * pl);
+    x3w_block(fa, fb[1], acc, 1);
+    B.store(wr + kX3wOpDw, gb);
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+    for (int i = 0; i < 12; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, 3, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // group 2: B block 3 reads; the barrier makes stage c + 2 visible and ends
+    // this stage's reads of `cur`
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl) fb[1][pl] = x3w_frag(cur + offb + 3 * 32 * kX3RowDw + 8 * pl);
+    x3w_block(fa, fb[0], acc, 2);
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 12, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // group 3: next stage's B block 0 and A fragments, each after its last use
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl) fb[0][pl] = x3w_frag(nxt + offb + 8 * pl);
+    {
+        constexpr int PA[6] = {2, 1, 1, 0, 0, 0};
+        constexpr int PB[6] = {0, 0, 1, 0, 1, 2};
+#pragma unroll
+        for (int q = 0; q < 6; ++q) {
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+                acc[mi][3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[mi][PA[q]], fb[1][PB[q]], acc[mi][3], 0, 0, 0);
+            if (q == 0 || q == 2 || q == 5) {
+                const int pl = PA[q];
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi) fa[mi][pl] = x3w_frag(nxt + offa + mi * 32 * kX3RowDw + 8 * pl);
+            }
+        }
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Stage c with c % 3 == R: stage s lives in LDS buffer s % 3 and in
+// register set s % 3; the set that held stage c + 1 takes stage c + 4 (a
+// load past the last stage re-reads the last stage: in bounds, and it lands
+// in a buffer no stage reads).
+template <int R, class OA, class OB>
+__device__ __forceinline__ void x3w_stage3(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                           int64_t c, int64_t nst, uint32_t* lds, X3Stage (&ga)[3],
+                                           X3Stage (&gb)[3], int offa, int offb, bf16x8 (&fa)[2][3],
+                                           bf16x8 (&fb)[2][3], f32x16 (&acc)[2][4])
+{
+    x3w_stage(A, row0a, B, row0b, min(c + 4, nst - 1) * kX3KC, lds + R * kX3wBufDw,
+              lds + ((R + 1) % 3) * kX3wBufDw, lds + ((R + 2) % 3) * kX3wBufDw, ga[(R + 2) % 3],
+              gb[(R + 2) % 3], ga[(R + 1) % 3], gb[(R + 1) % 3], offa, offb, fa, fb, acc);
+}
+
+// acc += A[row0a.., 0..K) B[row0b.., 0..K)^T on the 256 x 256 tile of 512
+// threads; K a positive multiple of 32, every 256-row panel inside the matrix,
+// aligned rows.  `lds` holds kX3wLdsDw dwords.  Ends with a barrier.
+template <class OA, class OB>
+__device__ __forceinline__ void nt_tile_x3_wide(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                                int64_t K, uint32_t* lds, f32x16 (&acc)[2][4])
+{
+    const int64_t nst = K / kX3KC;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int offa = x3_addr(wm * 64 + (lane & 31), lane >> 5, 0);
+    const int offb = kX3wOpDw + x3_addr(wn * 128 + (lane & 31), lane >> 5, 0);
+    X3Stage ga[3], gb[3];
+    A.load_full(row0a, 0, ga[0]);
+    B.load_full(row0b, 0, gb[0]);
+    A.load_full(row0a, kX3KC, ga[1]);
+    B.load_full(row0b, kX3KC, gb[1]);
+    A.store(lds, ga[0]);
+    B.store(lds + kX3wOpDw, gb[0]);
+    A.load_full(row0a, min<int64_t>(2, nst - 1) * kX3KC, ga[2]);
+    B.load_full(row0b, min<int64_t>(2, nst - 1) * kX3KC, gb[2]);
+    A.load_full(row0a, min<int64_t>(3, nst - 1) * kX3KC, ga[0]);
+    B.load_full(row0b, min<int64_t>(3, nst - 1) * kX3KC, gb[0]);
+    A.store(lds + kX3wBufDw, ga[1]);
+    B.store(lds + kX3wBufDw + kX3wOpDw, gb[1]);
+    __syncthreads();
+    bf16x8 fa[2][3], fb[2][3];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int pl = 0; pl < 3; ++pl) fa[mi][pl] = x3w_frag(lds + offa + mi * 32 * kX3RowDw + 8 * pl);
+#pragma unroll
+    for (int pl = 0; pl < 3; ++pl) fb[0][pl] = x3w_frag(lds + offb + 8 * pl);
+    int64_t c = 0;
+    for (; c + 3 <= nst; c += 3) {
+        x3w_stage3<0>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+        x3w_stage3<1>(A, row0a, B, row0b, c + 1, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+        x3w_stage3<2>(A, row0a, B, row0b, c + 2, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+    }
+    if (c < nst) x3w_stage3<0>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+    if (c + 1 < nst) x3w_stage3<1>(A, row0a, B, row0b, c + 1, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+    __syncthreads();
+}
 }  // namespace qe
