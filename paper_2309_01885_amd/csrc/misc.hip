@@ -97,6 +97,87 @@ __global__ __launch_bounds__(256, 2) void quad_form_kernel(const float* p1, cons
     if (threadIdx.x == 0) partial[blockIdx.x] = s;
 }
 
+// The same on 256 x 256 tiles of eight waves (nt_tile_x3_wide: operand reads
+// pipelined through three LDS stage buffers), for q and p multiples of 256 and
+// aligned rows.  Tiles are dealt to the 8 XCDs in contiguous ranges (the
+// hardware places workgroup b on XCD b % 8) of a banded order (bands of 4 tile
+// rows, column-major inside a band), so that the 32 workgroups an XCD holds
+// at a time share 4 row panels of A and 8 of Sigma in its L2.
+// A = P1 (+ P2) (- P3) with the present terms fixed at compile time, so that
+// the loads in flight hold only the operands that exist.
+template <bool P2, bool P3>
+struct X3CompT {
+    const float *p1, *p2, *p3;
+    int64_t ld;
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int64_t off = (row0 + (t >> 1)) * ld + k0 + 8 * (t & 1);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            f32x4 v = *reinterpret_cast<const f32x4*>(p1 + off + 4 * h);
+            if constexpr (P2) v = v + *reinterpret_cast<const f32x4*>(p2 + off + 4 * h);
+            if constexpr (P3) v = v - *reinterpret_cast<const f32x4*>(p3 + off + 4 * h);
+            st.v[h] = v;
+        }
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const { x3_store_row8(op, st); }
+};
+
+template <bool P2, bool P3>
+__global__ __launch_bounds__(512, 1) void quad_form_wide_kernel(const float* p1, const float* p2,
+                                                             const float* p3,
+                                                             const float* Sigma, int64_t q,
+                                                             int64_t p, double* partial,
+                                                             const int* status)
+{
+    if (failed(status)) return;
+    __shared__ __attribute__((aligned(16))) uint32_t lds[kX3wLdsDw];
+    __shared__ double sh[512];
+    const int64_t tm_count = q / 256, tn_count = p / 256, tiles = tm_count * tn_count;
+    const int64_t per = cdiv(tiles, 8);
+    const int64_t item = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
+    if (item >= tiles) return;                    // uniform: the whole workgroup leaves
+    const int64_t b0 = (item / (4 * tn_count)) * 4;
+    const int64_t bh = min((int64_t)4, tm_count - b0);
+    const int64_t u = item - b0 * tn_count;
+    const int64_t row0 = (b0 + u % bh) * 256, col0 = (u / bh) * 256;
+    f32x16 acc[2][4];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
+    const X3CompT<P2, P3> A{p1, p2, p3, p};
+    const X3Row B{Sigma, p, p, p};
+    nt_tile_x3_wide(A, row0, B, col0, p, lds, acc);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    double d = 0.0;
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int64_t r = row0 + wm * 64 + 32 * mi + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                const int64_t c = col0 + wn * 128 + 32 * ni + (lane & 31);
+                const int64_t e = r * p + c;
+                float a = p1[e];
+                if constexpr (P2) a = a + p2[e];
+                if constexpr (P3) a = a - p3[e];
+                d += (double)a * (double)acc[mi][ni][v];
+            }
+    sh[threadIdx.x] = d;
+    __syncthreads();
+    for (int st = 256; st > 0; st >>= 1) {
+        if ((int)threadIdx.x < st) sh[threadIdx.x] += sh[threadIdx.x + st];
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) partial[item] = sh[0];
+}
+
 __global__ __launch_bounds__(256) void sum_tiles_kernel(const double* partial, int64_t n,
                                                         double* out, const int* status)
 {
@@ -124,6 +205,23 @@ qe_status launch_objective(const float* W, const float* Wh, const float* H, cons
     double* part1 = w.take<double>(tiles);
     const bool vec4 = aligned16(W) && aligned16(Wh) && aligned16(Sigma) && (!H || aligned16(H)) &&
                       p % 4 == 0;
+    if (vec4 && q % 256 == 0 && p % 256 == 0) {
+        // 256 x 256 tiles: q p / 65536 partials (fewer than the 128 x 128 count)
+        const int64_t wt = (q / 256) * (p / 256);
+        const dim3 grid((unsigned)(8 * cdiv(wt, 8)));
+        if (H)
+            hipLaunchKernelGGL((quad_form_wide_kernel<true, true>), grid, dim3(512), 0, s, Wh, H,
+                               W, Sigma, q, p, part0, status);
+        else
+            hipLaunchKernelGGL((quad_form_wide_kernel<false, true>), grid, dim3(512), 0, s, Wh,
+                               H, W, Sigma, q, p, part0, status);
+        hipLaunchKernelGGL(sum_tiles_kernel, dim3(1), dim3(256), 0, s, part0, wt, out, status);
+        hipLaunchKernelGGL((quad_form_wide_kernel<false, false>), grid, dim3(512), 0, s, W,
+                           (const float*)nullptr, (const float*)nullptr, Sigma, q, p, part1,
+                           status);
+        hipLaunchKernelGGL(sum_tiles_kernel, dim3(1), dim3(256), 0, s, part1, wt, out + 1, status);
+        return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
+    }
     // D = What + H - W
     hipLaunchKernelGGL(quad_form_kernel, dim3((unsigned)tiles), dim3(256), 0, s, Wh, H, W, Sigma,
                        q, p, part0, vec4 ? 1 : 0, status);

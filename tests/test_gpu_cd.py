@@ -238,8 +238,11 @@ def test_zero_diagonal_reports_error(qe):
     assert e.value.code == 2
 
 
-def test_objective_entry_point(qe, oracle):
-    W, X = layer(140, 260, 1024, 27, corr=0.9)
+@pytest.mark.parametrize("q,p", [(140, 260), (256, 512), (512, 256)])
+def test_objective_entry_point(qe, oracle, q, p):
+    """Exact objective with and without H; q and p multiples of 256 take the
+    256 x 256 tile kernels (one instantiation per set of present terms)."""
+    W, X = layer(q, p, 1024, 27, corr=0.9)
     S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
     scale, zero = oracle.grid_minmax(W, 4)
     g = gpu_cd(qe, W, S32, 4, scale, zero, 2)
