@@ -21,8 +21,12 @@ def _gram(qe, X, layout=0, **kw):
 
 @pytest.mark.parametrize("fp32", [False, True])
 @pytest.mark.parametrize("p,n", [(512, 2048), (200, 1000), (1, 7), (129, 33), (300, 5000),
-                                 (384, 4096 + 32), (256, 16), (768, 4096 + 64)])
+                                 (384, 4096 + 32), (256, 16), (768, 4096 + 64),
+                                 (256, 4096), (512, 8192 + 32)])
 def test_gram_matches_oracle(qe, oracle, p, n, fp32):
+    """(256, 4096) takes 128 token splits of 32: the shortest K loop of the
+    256 x 256 tile (two stages); (512, 8224) a split count that leaves a
+    shorter last split."""
     spec = synth.CONFIGS["c1"]
     X = synth.activations(spec, n=n, p=p)
     S = _gram(qe, X, fp32=fp32)
