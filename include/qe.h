@@ -220,8 +220,9 @@ qe_status qe_objective(const float* W, const float* W_hat, const float* H, const
 /* ------------------------------------------------------------------------
  * lambda_max(Sigma) by the power method (Sec. 5.3: matrix-vector products
  * only, O(p^2) per iteration).  Start vector 1/sqrt(p); the estimate is the
- * Rayleigh quotient; stops when it changes by less than tol (relative)
- * between checks, or after max_iters iterations.  Synchronises `stream`.
+ * Rayleigh quotient; the result is that of the first iteration whose quotient
+ * changed by at most tol (relative) from the previous one, else of iteration
+ * max_iters.  Synchronises `stream` every 32 iterations.
  * lambda_out: HOST float.
  * ------------------------------------------------------------------------ */
 size_t qe_lambda_workspace_size(int64_t p);

@@ -239,11 +239,14 @@ qe_status launch_objective(const float* W, const float* Wh, const float* H, cons
 // y_k = Sigma v_k, lambda_k = v_k . y_k (Rayleigh quotient of the unit v_k).
 // One kernel per iteration: every workgroup first forms 1/||y_{k-1}|| from the
 // previous iteration's per-workgroup partials (same fixed-order sum in every
-// workgroup), then 4 rows of y_k (one per wavefront, fp64 dot products over
-// float4 loads of Sigma), and writes its partials of ||y_k||^2 and v_k . y_k.
-// Workgroup 0 also records lambda_{k-1}.
-constexpr int kSymvRows = 4;
-constexpr int kLambdaCheck = 8;
+// workgroup), then 8 rows of y_k (two per wavefront, processed together so
+// that each float4 of y_{k-1} serves two rows of Sigma; fp64 dot products
+// against y_{k-1} itself, the normalisation applied once per row), and writes
+// its partials of ||y_k||^2 and v_k . y_k.  Workgroup 0 also records
+// lambda_{k-1}.  Sigma is read once per iteration: the kernel is bound by
+// that stream (HBM or, for Sigma within the die-level cache, that cache).
+constexpr int kSymvRows = 8;
+constexpr int kLambdaCheck = 32;   // iterations per host check (the stop is still per iteration)
 
 __device__ inline void sum_pair_partials(const double* part, int n, double* sh, double& yy,
                                          double& vy)
@@ -266,43 +269,61 @@ __global__ __launch_bounds__(256) void power_step_kernel(const float* __restrict
     __shared__ double sh[256];
     __shared__ double wpart[4][2];
     const int nwg = (int)gridDim.x;
-    double inv = 0.0;
+    // v_k = yprev * inv (the first iteration: yprev taken as all ones)
+    double inv;
     if (first) {
-        inv = 1.0;
+        inv = 1.0 / sqrt((double)p);
     } else {
         double yy, vy;
         sum_pair_partials(pprev, nwg, sh, yy, vy);
         inv = yy > 0.0 ? 1.0 / sqrt(yy) : 0.0;
         if (blockIdx.x == 0 && threadIdx.x == 0 && slot > 0) lam_hist[slot - 1] = vy;
     }
-    const float v0 = (float)(1.0 / sqrt((double)p));
-    auto vj = [&](int64_t j) -> float {
-        return first ? v0 : (float)((double)yprev[j] * inv);
-    };
+    auto wj = [&](int64_t j) -> float { return first ? 1.f : yprev[j]; };
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    double pyy = 0.0, pvy = 0.0;
-    for (int rr = 0; rr < kSymvRows / 4; ++rr) {
-        const int64_t row = (int64_t)blockIdx.x * kSymvRows + wave * (kSymvRows / 4) + rr;
-        if (row >= p) break;
-        const float* srow = Sigma + row * p;
-        double acc = 0.0;
-        int64_t tail = 0;
-        if (vec4) {
-            const int64_t n4 = p / 4;
-#pragma unroll 8
-            for (int64_t f = lane; f < n4; f += 64) {
-                const f32x4 sv = *reinterpret_cast<const f32x4*>(srow + 4 * f);
+    constexpr int RW = kSymvRows / 4;            // rows per wavefront
+    const int64_t r0 = (int64_t)blockIdx.x * kSymvRows + wave * RW;
+    const float* srow[RW];
+    bool ok[RW];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) acc += (double)sv[u] * (double)vj(4 * f + u);
+    for (int rr = 0; rr < RW; ++rr) {
+        ok[rr] = r0 + rr < p;
+        srow[rr] = Sigma + (ok[rr] ? r0 + rr : 0) * p;
+    }
+    double acc[RW];
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) acc[rr] = 0.0;
+    int64_t tail = 0;
+    if (vec4) {
+        const int64_t n4 = p / 4;
+#pragma unroll 4
+        for (int64_t f = lane; f < n4; f += 64) {
+            const f32x4 wv = first ? f32x4{1.f, 1.f, 1.f, 1.f}
+                                   : *reinterpret_cast<const f32x4*>(yprev + 4 * f);
+#pragma unroll
+            for (int rr = 0; rr < RW; ++rr) {
+                const f32x4 sv = *reinterpret_cast<const f32x4*>(srow[rr] + 4 * f);
+#pragma unroll
+                for (int u = 0; u < 4; ++u) acc[rr] += (double)sv[u] * (double)wv[u];
             }
-            tail = 4 * n4;
         }
-        for (int64_t j = tail + lane; j < p; j += 64) acc += (double)srow[j] * (double)vj(j);
-        for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
-        const float yr = (float)acc;
-        if (lane == 0) y[row] = yr;
+        tail = 4 * n4;
+    }
+    for (int64_t j = tail + lane; j < p; j += 64) {
+        const double wv = (double)wj(j);
+#pragma unroll
+        for (int rr = 0; rr < RW; ++rr) acc[rr] += (double)srow[rr][j] * wv;
+    }
+    double pyy = 0.0, pvy = 0.0;
+#pragma unroll
+    for (int rr = 0; rr < RW; ++rr) {
+        double a = acc[rr];
+        for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off, 64);
+        if (!ok[rr]) continue;
+        const float yr = (float)(a * inv);
+        if (lane == 0) y[r0 + rr] = yr;
         pyy += (double)yr * (double)yr;
-        pvy += (double)vj(row) * (double)yr;
+        pvy += (double)wj(r0 + rr) * inv * (double)yr;
     }
     if (lane == 0) {
         wpart[wave][0] = pyy;
@@ -360,9 +381,14 @@ qe_status launch_lambda(const float* Sigma, int64_t p, int max_iters, float tol,
         if (hipMemcpyAsync(h, hist, sizeof(double) * batch, hipMemcpyDeviceToHost, s) != hipSuccess)
             return QE_ERR_HIP;
         if (hipStreamSynchronize(s) != hipSuccess) return QE_ERR_HIP;
-        prev = batch > 1 ? h[batch - 2] : last;
-        last = h[batch - 1];
-        if (last > 0.0 && fabs(last - prev) <= (double)tol * last) break;
+        // the first iteration of the batch whose quotient moved by <= tol relative
+        bool done = false;
+        for (int b = 0; b < batch && !done; ++b) {
+            prev = last;
+            last = h[b];
+            done = it - batch + b > 0 && last > 0.0 && fabs(last - prev) <= (double)tol * last;
+        }
+        if (done) break;
     }
     *out = (float)last;
     return QE_OK;
