@@ -37,6 +37,35 @@ def test_lambda_max(qe, oracle):
     assert lam == pytest.approx(oracle.lambda_max(S), rel=1e-5)
 
 
+def _power_method(S, max_iters, tol):
+    """The stop rule of qe_lambda_max in fp64: Rayleigh quotients of the unit
+    iterates from 1/sqrt(p); the first one within tol (relative) of its
+    predecessor, else the last."""
+    S = np.asarray(S, np.float64)
+    v = np.full(S.shape[0], 1.0 / np.sqrt(S.shape[0]))
+    prev = None
+    for _ in range(max_iters):
+        y = S @ v
+        lam = float(v @ y)
+        if prev is not None and abs(lam - prev) <= tol * lam:
+            return lam
+        prev = lam
+        v = y / np.linalg.norm(y)
+    return lam
+
+
+@pytest.mark.parametrize("max_iters,tol", [(1, 1e-7), (3, 1e-7), (40, 1e-7), (500, 1e-2),
+                                           (500, 1e-4)])
+def test_lambda_max_stop_rule(qe, max_iters, tol):
+    """Iteration counts and tolerances that stop inside, at the end of and
+    across the 32-iteration host checks give the quotient of the same
+    iteration as an fp64 power method with the same rule."""
+    X = synth.correlated_activations(300, 2000, 0.9, 4, out_channels=6, out_mult=20.0)
+    S = (X.astype(np.float64) @ X.T.astype(np.float64)).astype(np.float32)
+    lam = qe.lambda_max(dev(S), max_iters=max_iters, tol=tol)
+    assert lam == pytest.approx(_power_method(S, max_iters, tol), rel=2e-6)
+
+
 def run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0, block=0,
                     extra=0):
     q, p = W.shape
