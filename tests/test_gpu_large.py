@@ -6,8 +6,9 @@ launch configuration the benchmark times (block width 128).
   the oracle's one-by-one dot products; relative Frobenius <= 1e-5.
 * CD sweeps on all 4096 rows; the oracle replays a seeded sample of 64 rows
   with the same Sigma (rows are independent, Sec. 4.2, so the comparison is
-  exact): objective within 1e-4 over the rows whose trajectories never
-  split, every split at a near tie and followed by descent, codes <= 0.1%
+  exact): identical codes and objective within 1e-4 over the rows whose
+  trajectories never split, every split at a near tie and followed by
+  descent, at most max(2, 1e-6 x decisions) split rows
   (parity.check_row_sampled_sweeps).  Sigma comes from the oracle's Gram of the
   first 2048 tokens, damped, so the oracle finishes in seconds."""
 import numpy as np
