@@ -477,7 +477,9 @@ __global__ __launch_bounds__(256) void merge_supports_kernel(
 
 // E_i += sum_k (Hnew_ik - Hold_ik) Sigma_k,:  from the merged list, in
 // ascending k per row (a deterministic order).  Workgroup = 16 rows x 128
-// columns: lanes 16 r .. 16 r + 15 (one DPP row) own row r, 8 columns each.
+// columns: lanes 16 r .. 16 r + 15 (one DPP row) own row r; lane g holds
+// columns 4 g .. 4 g + 3 and 64 + 4 g .. 64 + 4 g + 3 of the block, so that the
+// 16 lanes of each 16-byte load cover whole cache lines of a Sigma row.
 // A batch of 16 list entries is fetched one per lane; the first entry of an
 // (old, new) pair carries new - old, its partner 0.  Entries are then taken
 // in order, broadcast with DPP, and each lane applies one Sigma row segment.
@@ -518,12 +520,12 @@ __device__ __forceinline__ void spmm_batch(std::integer_sequence<int, Us...>, fl
             const float* src = Sigma + (int64_t)cu[u] * p + c0;
             if (full) {
                 sa[u] = *reinterpret_cast<const f32x4*>(src);
-                sb[u] = *reinterpret_cast<const f32x4*>(src + 4);
+                sb[u] = *reinterpret_cast<const f32x4*>(src + kSpCols / 2);
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     sa[u][e] = c0 + e < p ? src[e] : 0.f;
-                    sb[u][e] = c0 + 4 + e < p ? src[4 + e] : 0.f;
+                    sb[u][e] = c0 + kSpCols / 2 + e < p ? src[kSpCols / 2 + e] : 0.f;
                 }
             }
         }
@@ -556,7 +558,7 @@ __global__ __launch_bounds__(256) void spmm_delta_kernel(const int64_t* __restri
     const int64_t cb = w / n_rt, rt = w % n_rt;
     const int r = threadIdx.x >> 4, g = threadIdx.x & 15;
     const int64_t i = rt * kSpRows + r;
-    const int64_t c0 = cb * kSpCols + 8 * g;
+    const int64_t c0 = cb * kSpCols + 4 * g;
     const bool rowok = i < q;
     const int64_t m0 = rowok ? mrp[i] : 0, m1 = rowok ? mrp[i + 1] : 0;
     const int64_t len = m1 > m0 ? m1 - m0 : 0;
@@ -567,11 +569,13 @@ __global__ __launch_bounds__(256) void spmm_delta_kernel(const int64_t* __restri
         wl = o > wl ? o : wl;
     }
     if (wl == 0) return;
-    const bool full = vec4 && c0 + 8 <= p;
+    const bool full = vec4 && cb * kSpCols + kSpCols <= p;
     float* erow = E + i * p + c0;
+    // acc[e]: column c0 + e (e < 4) or c0 + 64 + e - 4
+    auto coff = [](int e) { return e < 4 ? e : kSpCols / 2 - 4 + e; };
     float acc[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = (len > 0 && c0 + e < p) ? erow[e] : 0.f;
+    for (int e = 0; e < 8; ++e) acc[e] = (len > 0 && c0 + coff(e) < p) ? erow[coff(e)] : 0.f;
     const int64_t rlo = i * p, rhi = rlo + p;
     // lane g's entry of the batch at `base`: (delta, Sigma row), 0 if none
     auto fetch = [&](int64_t base, float& dd, int& col) {
@@ -610,7 +614,7 @@ __global__ __launch_bounds__(256) void spmm_delta_kernel(const int64_t* __restri
     if (len > 0) {
 #pragma unroll
         for (int e = 0; e < 8; ++e)
-            if (c0 + e < p) erow[e] = acc[e];
+            if (c0 + coff(e) < p) erow[coff(e)] = acc[e];
     }
 }
 
