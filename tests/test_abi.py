@@ -1,7 +1,8 @@
 """The C ABI without a GPU: the built library loads, exports every function
 include/qe.h declares (and no undeclared qe_ symbol), and its host-only
 helpers (status strings, version, workspace and packing sizes) answer as
-documented.  No call here launches a kernel or touches a device."""
+documented, and host-detectable argument errors are reported before any
+device work.  No call here launches a kernel or touches a device."""
 import ctypes
 import os
 import re
@@ -115,3 +116,78 @@ def test_binding_names_follow_the_abi():
         if n.endswith("_workspace_size") or n in helpers:
             continue
         assert callable(getattr(Q, n[len("qe_"):], None)), n
+
+
+# ------------------------------------------------------------------ argument errors
+# Host-detectable argument errors return before any HIP call (qe.h: errors),
+# so they are checked here without a GPU.  Pointers are dummies: none is
+# dereferenced on these paths.
+QE_ERR_ARG, QE_ERR_WORKSPACE = 1, 4
+DUMMY = ctypes.c_void_p(4096)
+NULL = ctypes.c_void_p(0)
+
+
+def _gram(L, X=DUMMY, p=64, n=64, layout=0, S=DUMMY, damp=0.0, ws=DUMMY, ws_bytes=1 << 40):
+    f = L.qe_gram
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int, ctypes.c_void_p,
+                  ctypes.c_int, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    return f(X, p, n, layout, S, 0, damp, ws, ws_bytes, NULL)
+
+
+def test_gram_argument_errors(lib):
+    L, _ = lib
+    assert _gram(L, X=NULL) == QE_ERR_ARG
+    assert _gram(L, S=NULL) == QE_ERR_ARG
+    assert _gram(L, p=0) == QE_ERR_ARG            # empty input
+    assert _gram(L, n=0) == QE_ERR_ARG
+    assert _gram(L, layout=2) == QE_ERR_ARG
+    assert _gram(L, damp=-1.0) == QE_ERR_ARG
+    assert _gram(L, damp=float("nan")) == QE_ERR_ARG
+    assert _gram(L, ws=NULL) == QE_ERR_WORKSPACE
+    assert _gram(L, ws_bytes=16) == QE_ERR_WORKSPACE
+
+
+def _cd(L, q=64, p=64, bits=4, sweeps=1, block=0, flags=0, ws=DUMMY, ws_bytes=1 << 40, W=DUMMY):
+    f = L.qe_cd_sweep
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    return f(W, DUMMY, q, p, bits, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, sweeps, block, flags, NULL,
+             ws, ws_bytes, NULL)
+
+
+def test_cd_sweep_argument_errors(lib):
+    L, _ = lib
+    assert _cd(L, W=NULL) == QE_ERR_ARG
+    assert _cd(L, q=0) == QE_ERR_ARG              # empty input
+    assert _cd(L, p=0) == QE_ERR_ARG
+    assert _cd(L, bits=0) == QE_ERR_ARG           # bits outside [1, 8]
+    assert _cd(L, bits=9) == QE_ERR_ARG
+    assert _cd(L, block=48) == QE_ERR_ARG         # block widths 16, 32, 64, 128 (0 = default)
+    assert _cd(L, sweeps=-1) == QE_ERR_ARG
+    assert _cd(L, flags=0x10) == QE_ERR_ARG       # QE_OUTLIER_COLUMNS belongs to the outlier call
+    assert _cd(L, ws=NULL) == QE_ERR_WORKSPACE
+    assert _cd(L, ws_bytes=1024) == QE_ERR_WORKSPACE
+
+
+def test_lambda_and_objective_argument_errors(lib):
+    L, _ = lib
+    f = L.qe_lambda_max
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    out = ctypes.c_float(0.0)
+    assert f(DUMMY, 64, 0, 1e-7, ctypes.byref(out), DUMMY, 1 << 40, NULL) == QE_ERR_ARG
+    assert f(DUMMY, 0, 10, 1e-7, ctypes.byref(out), DUMMY, 1 << 40, NULL) == QE_ERR_ARG
+    assert f(DUMMY, 64, 10, float("nan"), ctypes.byref(out), DUMMY, 1 << 40, NULL) == QE_ERR_ARG
+    assert f(DUMMY, 64, 10, 1e-7, ctypes.byref(out), DUMMY, 8, NULL) == QE_ERR_WORKSPACE
+    g = L.qe_objective
+    g.restype = ctypes.c_int
+    g.argtypes = [ctypes.c_void_p] * 4 + [ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    assert g(DUMMY, NULL, NULL, DUMMY, 8, 8, DUMMY, DUMMY, 1 << 40, NULL) == QE_ERR_ARG
+    assert g(DUMMY, DUMMY, NULL, DUMMY, 0, 8, DUMMY, DUMMY, 1 << 40, NULL) == QE_ERR_ARG
+    assert g(DUMMY, DUMMY, NULL, DUMMY, 8, 8, DUMMY, DUMMY, 8, NULL) == QE_ERR_WORKSPACE
