@@ -73,28 +73,77 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+CPU_GRAM_TOKENS = 32768      # oracle Gram sample (about 10 s on 16 host threads)
+CPU_SWEEP_ROWS = 1024        # oracle sweep sample
+CPU_ONE_THREAD_ROWS = 64     # single-thread sweep sample
+
+# Child process for the single-thread figure: OpenMP's thread count is fixed
+# when the oracle library loads, so it runs in a fresh interpreter.
+_ONE_THREAD = """
+import sys, numpy as np
+sys.path.insert(0, sys.argv[1])
+import oracle
+d = sys.argv[2]
+a = {k: np.load(d + "/" + k + ".npy") for k in ("W", "S", "scale", "zero")}
+print(oracle.num_threads(), oracle.cd_sweep_timed(a["W"], a["S"], int(sys.argv[3]), a["scale"],
+                                                  a["zero"]))
+"""
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def one_thread_sweep(S, W, scale, zero, bits):
+    """Seconds of one oracle sweep over W's rows with one OpenMP thread."""
+    import subprocess
+    import tempfile
+    with tempfile.TemporaryDirectory(dir="/tmp") as d:
+        for k, v in (("W", W), ("S", S), ("scale", scale), ("zero", zero)):
+            np.save(os.path.join(d, k + ".npy"), np.ascontiguousarray(v))
+        env = dict(os.environ, OMP_NUM_THREADS="1")
+        out = subprocess.run([sys.executable, "-c", _ONE_THREAD, ROOT, d, str(bits)], env=env,
+                             capture_output=True, text=True, timeout=600, check=True).stdout
+    threads, secs = out.split()
+    assert int(threads) == 1, out
+    return float(secs)
+
+
 def cpu_baseline(spec, X_head, W, scale, zero, sweeps):
     """The oracle as it stands on the host cores, on a bounded sample of the
     same step: Gram on the first n' tokens (scaled by n/n'), one CD sweep on r
-    seeded rows (scaled by q/r rows and by the sweep count)."""
+    seeded rows (scaled by q/r rows and by the sweep count); plus the sweep on
+    fewer rows with a single thread."""
     import oracle
     q, p, n = spec.q, spec.p, spec.n
     n_s = X_head.shape[1]
     t0 = time.perf_counter()
     S = oracle.damp(oracle.gram(X_head), spec.damp)
     t_gram = time.perf_counter() - t0
-    rows = __import__("synth").row_sample(q, 256, spec.cfg)
+    rows = __import__("synth").row_sample(q, CPU_SWEEP_ROWS, spec.cfg)
     t_sweep = oracle.cd_sweep_timed(W[rows], S, spec.bits, scale[rows], zero[rows])
     t_step = t_gram * (n / n_s) + t_sweep * (q / len(rows)) * sweeps
+    r1 = rows[:CPU_ONE_THREAD_ROWS]
+    t_one = one_thread_sweep(S, W[r1], scale[r1], zero[r1], spec.bits)
     return {
         "value": p * sweeps / t_step,
         "unit": "column-updates/s",
         "cores": oracle.num_threads(),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
         "sample": (f"Gram over {n_s} of {n} tokens (x{n / n_s:.0f}), one Lemma-1 sweep over "
                    f"{len(rows)} of {q} rows (x{q / len(rows):.0f} rows, x{sweeps} sweeps); "
                    f"measured {t_gram:.2f} s + {t_sweep:.2f} s"),
         "step_s_extrapolated": t_step,
+        "one_thread_sweep": {"rows": len(r1), "seconds": t_one,
+                             "coordinate_updates_per_s": len(r1) * p / t_one,
+                             "speedup_of_all_threads": (t_one / len(r1)) / (t_sweep / len(rows))},
     }
 
 
@@ -135,7 +184,7 @@ def main():
     W_h = synth.weights(spec)
     X_h = synth.activations(spec)
     X = torch.from_numpy(X_h).to(dev)
-    X_head = np.ascontiguousarray(X_h[:, :4096])
+    X_head = np.ascontiguousarray(X_h[:, :CPU_GRAM_TOKENS])
     del X_h
     W = torch.from_numpy(W_h).to(dev)
     Sigma = torch.empty((p, p), dtype=torch.float32, device=dev)

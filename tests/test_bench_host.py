@@ -33,3 +33,21 @@ def test_more_than_one_gpu_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+def test_cpu_baseline_small():
+    """The oracle baseline on a tiny sample: the fields the bench line carries,
+    including the single-thread sweep run in a child process."""
+    import numpy as np
+    import oracle
+    import synth
+    spec = synth.CONFIGS["c1"]
+    X = synth.activations(spec)[:, :256]
+    W = synth.weights(spec)
+    sc, ze = oracle.grid_minmax(W, spec.bits)
+    r = bench.cpu_baseline(spec, np.ascontiguousarray(X), W, sc, ze, spec.sweeps)
+    assert r["kind"] == "oracle" and r["unit"] == "column-updates/s"
+    assert r["value"] > 0 and r["cores"] >= 1 and r["cpu_model"]
+    one = r["one_thread_sweep"]
+    assert one["rows"] == min(bench.CPU_ONE_THREAD_ROWS, spec.q) and one["seconds"] > 0
+    assert "256 of 2048 tokens" in r["sample"]
