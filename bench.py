@@ -154,6 +154,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-outlier", action="store_true", help="skip the outlier-aware timing")
+    ap.add_argument("--no-peaks", action="store_true",
+                    help="skip the matrix-core / copy peak checks (libqe_peak.so)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with a plain 256 MiB device copy (HBM counter calibration)")
     ap.add_argument("--configs", action="store_true",
@@ -319,6 +321,14 @@ def main():
     if not args.no_outlier:
         log("outlier-aware path")
         result["outlier"] = outlier_bench(P, torch, synth, W, Sigma, dev, block)
+
+    if not args.no_peaks:
+        log("peak checks")
+        from paper_2309_01885_amd import peaks
+        mp = peaks.measure(torch)
+        result["measured_peaks"] = mp
+        for r in result["rooflines"]:
+            r["frac_of_measured_bf16_peak"] = r["achieved"] / mp["mfma_bf16_tflops"]
 
     if not args.no_cpu:
         log("CPU oracle baseline")

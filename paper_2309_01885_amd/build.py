@@ -1,4 +1,5 @@
-"""Builds libqe.so (the HIP library behind include/qe.h) for gfx950, in-tree."""
+"""Builds libqe.so (the HIP library behind include/qe.h) and libqe_peak.so
+(peak-check probes) for gfx950, in-tree."""
 import glob
 import os
 import subprocess
@@ -23,9 +24,13 @@ def sources():
     return sorted(glob.glob(os.path.join(CSRC, "*.hip")))
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [HIPCC] + FLAGS + sources() + ["-o", tmp]
+PEAK_SRC = os.path.join(HERE, "peak", "peak.hip")
+PEAK_LIB = os.path.join(HERE, "libqe_peak.so")
+
+
+def _hipcc(srcs, out, verbose):
+    tmp = out + ".tmp"
+    cmd = [HIPCC] + FLAGS + srcs + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -33,11 +38,17 @@ def build(verbose: bool = False) -> str:
     err = "\n".join(l for l in (r.stderr or "").splitlines() if noise not in l)
     if r.returncode != 0:
         sys.stderr.write(err + "\n")
-        raise RuntimeError("hipcc failed building libqe.so")
+        raise RuntimeError(f"hipcc failed building {os.path.basename(out)}")
     if verbose and err.strip():
         sys.stderr.write(err + "\n")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """libqe.so (the C ABI of include/qe.h) and libqe_peak.so (peak checks)."""
+    _hipcc([PEAK_SRC], PEAK_LIB, verbose)
+    return _hipcc(sources(), LIB, verbose)
 
 
 if __name__ == "__main__":

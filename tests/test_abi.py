@@ -191,3 +191,14 @@ def test_lambda_and_objective_argument_errors(lib):
     assert g(DUMMY, NULL, NULL, DUMMY, 8, 8, DUMMY, DUMMY, 1 << 40, NULL) == QE_ERR_ARG
     assert g(DUMMY, DUMMY, NULL, DUMMY, 0, 8, DUMMY, DUMMY, 1 << 40, NULL) == QE_ERR_ARG
     assert g(DUMMY, DUMMY, NULL, DUMMY, 8, 8, DUMMY, DUMMY, 8, NULL) == QE_ERR_WORKSPACE
+
+
+def test_peak_library_exports_and_argument_errors():
+    """libqe_peak.so (peak checks) loads and rejects bad arguments before any launch."""
+    from paper_2309_01885_amd import peaks
+    L = peaks.load()
+    assert L.qpk_mfma_bf16(None, 512, 10, None) == 1
+    assert L.qpk_mfma_f32(DUMMY, 0, 10, None) == 1
+    assert L.qpk_clock(DUMMY, None, 512, 10, None) == 1
+    assert L.qpk_copy(DUMMY, ctypes.c_void_p(4100), 16, 64, None) == 1    # misaligned
+    assert L.qpk_copy(DUMMY, DUMMY, 0, 64, None) == 1
