@@ -260,6 +260,19 @@ def main():
     e1.record(stream)
     torch.cuda.synchronize()
     t_steps = e0.elapsed_time(e1) * 1e-3
+    # one sweep per call from W = What: events around each of sweeps 2..K
+    # (with its objective, as in the step), median
+    per_sweep = []
+    for k in range(sweeps):
+        a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a0.record(stream)
+        P.cd_sweep(W, Sigma, bits, scale, zero, Wh, codes, R, 1, block=block,
+                   flags=P.QE_INIT_FROM_W if k == 0 else P.QE_R_VALID | P.QE_CODES_VALID,
+                   obj=obj[k:], ws=ws_cd, check=False)
+        a1.record(stream)
+        per_sweep.append((a0, a1))
+    torch.cuda.synchronize()
+    sweep_median_2_k = float(np.median([a.elapsed_time(b) * 1e-3 for a, b in per_sweep[1:]]))
     launches = sweeps * (nb + 1)
     cd_flops_per_launch = 2.0 * q * p * p / (nb + 1)      # 2qp^2 per sweep over nb + 1 launches
     cd_avg = t_steps / launches
@@ -312,7 +325,10 @@ def main():
                         "cd_10_sweeps": float(np.median(phase["cd"])),
                         "exact_objective": float(np.median(phase["exact"]))},
         "sweep_time_s": sweep_t,
+        "sweep_time_median_2_to_k_s": sweep_median_2_k,
         "cd_column_updates_per_s": p / sweep_t,
+        "coordinate_updates_per_s": q * value,           # q * p * sweeps per step time
+        "cd_coordinate_updates_per_s": q * p / sweep_t,
         "layer_time_s": ms_per_step / 1e3,
         "objective_per_sweep": [float(x) for x in f_sweeps],
         "rel_calibration_error": float(exact[0] / exact[1]),

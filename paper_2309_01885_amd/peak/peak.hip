@@ -8,8 +8,8 @@
 //     products (v_mfma_f32_32x32x2f32) use, four independent accumulators per
 //     wave, two waves per SIMD; the caller times the launch.  Flops per launch:
 //     blocks * 4 waves * iters * 16 MFMAs * (2 * 32 * 32 * K), K = 16 or 2.
-//   qpk_copy: dst = src over n 16-byte elements, grid-stride, non-temporal
-//     (HBM stream).
+//   qpk_copy: dst = src over n 16-byte elements, grid-stride or one contiguous
+//     range per workgroup (HBM stream).
 //   qpk_clock: per-wave shader-clock and constant-rate (100 MHz) counter
 //     deltas across the bf16 loop, from which the engine clock under matrix
 //     load follows.
@@ -101,19 +101,30 @@ __global__ __launch_bounds__(kThreads, 2) void clock_kernel(float* out, uint64_t
     }
 }
 
-// Four independent 16-byte loads in flight per thread per pass.
+// Grid-stride copy, one 16-byte element per thread per pass.
 __global__ __launch_bounds__(kThreads) void copy_kernel(const f32x4* __restrict__ src,
                                                         f32x4* __restrict__ dst, size_t n)
 {
     const size_t stride = (size_t)gridDim.x * kThreads;
-    for (size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += 4 * stride) {
+    for (size_t i = (size_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += stride) dst[i] = src[i];
+}
+
+// Each workgroup copies one contiguous range of `per` elements, four 16-byte
+// loads in flight per thread.
+__global__ __launch_bounds__(kThreads) void copy_chunk_kernel(const f32x4* __restrict__ src,
+                                                              f32x4* __restrict__ dst, size_t n,
+                                                              size_t per)
+{
+    const size_t b0 = (size_t)blockIdx.x * per;
+    const size_t b1 = b0 + per < n ? b0 + per : n;
+    for (size_t i = b0 + threadIdx.x; i < b1; i += 4 * kThreads) {
         f32x4 v[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-            if (i + u * stride < n) v[u] = __builtin_nontemporal_load(src + i + u * stride);
+            if (i + u * kThreads < b1) v[u] = src[i + u * kThreads];
 #pragma unroll
         for (int u = 0; u < 4; ++u)
-            if (i + u * stride < n) __builtin_nontemporal_store(v[u], dst + i + u * stride);
+            if (i + u * kThreads < b1) dst[i + u * kThreads] = v[u];
     }
 }
 
@@ -150,13 +161,18 @@ int qpk_clock(float* out, uint64_t* clk, int blocks, int iters, void* stream)
     return launched();
 }
 
-// src, dst: n16 16-byte elements each, 16-byte aligned, not overlapping.
-int qpk_copy(const void* src, void* dst, size_t n16, int blocks, void* stream)
+// src, dst: n16 16-byte elements each, 16-byte aligned, not overlapping;
+// chunked = 0: grid-stride, else one contiguous range per workgroup.
+int qpk_copy(const void* src, void* dst, size_t n16, int blocks, int chunked, void* stream)
 {
     if (!src || !dst || n16 == 0 || blocks <= 0) return 1;
     if (((uintptr_t)src | (uintptr_t)dst) & 15) return 1;
-    hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(kThreads), 0, (hipStream_t)stream,
-                       (const f32x4*)src, (f32x4*)dst, n16);
+    if (chunked)
+        hipLaunchKernelGGL(copy_chunk_kernel, dim3(blocks), dim3(kThreads), 0, (hipStream_t)stream,
+                           (const f32x4*)src, (f32x4*)dst, n16, (n16 + blocks - 1) / blocks);
+    else
+        hipLaunchKernelGGL(copy_kernel, dim3(blocks), dim3(kThreads), 0, (hipStream_t)stream,
+                           (const f32x4*)src, (f32x4*)dst, n16);
     return launched();
 }
 

@@ -10,7 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libqe_peak.so")
 
 BLOCKS = 512            # two 256-thread workgroups per CU on 256 CUs
-COPY_BLOCKS = (1024, 2048, 4096)
+COPY_SHAPES = ((1024, 0), (2048, 0), (4096, 1), (16384, 1))   # (workgroups, chunked)
 _lib = None
 
 
@@ -23,7 +23,7 @@ def load():
         vp, i = ctypes.c_void_p, ctypes.c_int
         for f, args in (("qpk_mfma_bf16", [vp, i, i, vp]), ("qpk_mfma_f32", [vp, i, i, vp]),
                         ("qpk_clock", [vp, vp, i, i, vp]),
-                        ("qpk_copy", [vp, vp, ctypes.c_size_t, i, vp])):
+                        ("qpk_copy", [vp, vp, ctypes.c_size_t, i, i, vp])):
             getattr(lib, f).argtypes = args
             getattr(lib, f).restype = ctypes.c_int
         _lib = lib
@@ -69,9 +69,9 @@ def measure(torch, bf16_iters=4000, f32_iters=2000, copy_bytes=1 << 30):
     n16 = copy_bytes // 16
     src = torch.ones(n16 * 4, dtype=torch.float32, device=dev)
     dst = torch.empty_like(src)
-    t_cp = min(_timed(torch, lambda: _ok(lib.qpk_copy(src.data_ptr(), dst.data_ptr(), n16, b, st),
-                                         "qpk_copy"))
-               for b in COPY_BLOCKS)
+    t_cp = min(_timed(torch, lambda: _ok(lib.qpk_copy(src.data_ptr(), dst.data_ptr(), n16, b, ch,
+                                                      st), "qpk_copy"))
+               for b, ch in COPY_SHAPES)
     ok = bool(torch.equal(src, dst))
     del src, dst
     return {"mfma_bf16_tflops": bf_tf, "mfma_f32_tflops": f32_tf,
@@ -79,5 +79,5 @@ def measure(torch, bf16_iters=4000, f32_iters=2000, copy_bytes=1 << 30):
             "copy_checked": ok,
             "method": (f"register-only v_mfma_f32_32x32x16_bf16 / v_mfma_f32_32x32x2f32 loops, "
                        f"{BLOCKS} workgroups of 4 waves, 4 accumulators a wave; clock from "
-                       f"s_memtime over s_memrealtime; non-temporal copy of {copy_bytes >> 20} MiB, "
-                       f"best of {COPY_BLOCKS} workgroups; best of 3")}
+                       f"s_memtime over s_memrealtime; copy of {copy_bytes >> 20} MiB, best of "
+                       f"(workgroups, chunked) in {COPY_SHAPES}; best of 3")}

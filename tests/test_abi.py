@@ -200,5 +200,5 @@ def test_peak_library_exports_and_argument_errors():
     assert L.qpk_mfma_bf16(None, 512, 10, None) == 1
     assert L.qpk_mfma_f32(DUMMY, 0, 10, None) == 1
     assert L.qpk_clock(DUMMY, None, 512, 10, None) == 1
-    assert L.qpk_copy(DUMMY, ctypes.c_void_p(4100), 16, 64, None) == 1    # misaligned
-    assert L.qpk_copy(DUMMY, DUMMY, 0, 64, None) == 1
+    assert L.qpk_copy(DUMMY, ctypes.c_void_p(4100), 16, 64, 0, None) == 1    # misaligned
+    assert L.qpk_copy(DUMMY, DUMMY, 0, 64, 1, None) == 1
