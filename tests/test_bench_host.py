@@ -51,3 +51,12 @@ def test_cpu_baseline_small():
     one = r["one_thread_sweep"]
     assert one["rows"] == min(bench.CPU_ONE_THREAD_ROWS, spec.q) and one["seconds"] > 0
     assert "256 of 2048 tokens" in r["sample"]
+
+
+def test_help_lists_the_switches():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--help"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0
+    for flag in ("--gpus", "--steps", "--warmup", "--no-cpu", "--no-outlier", "--no-peaks",
+                 "--calib-copy", "--configs"):
+        assert flag in r.stdout, flag
