@@ -453,7 +453,7 @@ def outlier_bench(P, torch, synth, W, Sigma, dev, block):
            "support_nnz": int(nnz.cpu().item()),
            "g_after_cd": [float(x) for x in g[0::2]], "g_after_iht": [float(x) for x in g[1::2]]}
 
-    # structured outliers (Sec. 5.3): floor(s / q) whole columns
+    # structured outliers (Sec. 4.3): floor(s / q) whole columns
     ncols = s // q
     sup = torch.zeros(s, dtype=torch.int64, device=dev)
 

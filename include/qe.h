@@ -3,9 +3,9 @@
  *
  * QuantEase (arXiv 2309.01885) quantizes one linear layer at a time by
  * minimising f(What) = ||W X - What X||_F^2 over a per-output-channel uniform
- * b-bit grid (Sec. 3, problem (1)), with cyclic coordinate descent (Sec. 4)
+ * b-bit grid (Sec. 2.1, problem (1)), with cyclic coordinate descent (Sec. 3)
  * and, optionally, a sparse full-precision outlier matrix H chosen by
- * iterative hard thresholding (Sec. 5).
+ * iterative hard thresholding (Sec. 4).
  *
  * Conventions shared by every entry point:
  *  - Matrices are dense, row-major, contiguous fp32 in DEVICE memory (HBM)
@@ -52,12 +52,12 @@ typedef int qe_status;
 #define QE_GRAM_FP32 0x100    /* products on the fp32 matrix cores instead of the split bf16 ones */
 
 /* Flags for qe_cd_sweep / qe_cd_outlier_sweep. */
-#define QE_INIT_FROM_W 0x1u   /* start from What = W (Sec. 4.1) or What = W - H (Sec. 5.3);
+#define QE_INIT_FROM_W 0x1u   /* start from What = W (Sec. 3.1) or What = W - H (Sec. 4.3);
                                  R (or E) is set to 0; codes are not yet valid */
 #define QE_R_VALID     0x2u   /* R (or E) already holds (What [+ H] - W) Sigma: resume */
 #define QE_CODES_VALID 0x4u   /* codes hold What's grid codes: the keep-current tie rule of the
-                                 modified CD (Sec. 4.3) applies from the first sweep */
-/* Relaxed sweeps (Sec. 4.2, "Initialization": some iterations skip the
+                                 modified CD (Sec. 3.3) applies from the first sweep */
+/* Relaxed sweeps (Sec. 3.2, "Initialization": some iterations skip the
  * quantization).  With period k in [1, 255], sweeps k, 2k, ... of a call
  * (counted from 1) write the unconstrained minimiser beta of Lemma 1 instead
  * of q_i(beta); the last sweep of a call is never relaxed.  After a relaxed
@@ -66,7 +66,7 @@ typedef int qe_status;
 #define QE_RELAX_PERIOD(k) ((((uint32_t)(k)) & 0xffu) << 8)
 #define QE_RELAX_MASK      0xff00u
 /* qe_cd_outlier_sweep only: structured outliers ("Structured Outliers",
- * Sec. 5.3): the projection keeps the floor(s / q) whole columns of largest
+ * Sec. 4.3): the projection keeps the floor(s / q) whole columns of largest
  * l2 norm instead of the s largest entries (see qe_topk_columns). */
 #define QE_OUTLIER_COLUMNS 0x10u
 /* Block-update and residual products on the fp32 matrix cores instead of the
@@ -84,8 +84,8 @@ int qe_version(void);
 qe_status qe_sync_status(void* ws, void* stream);
 
 /* ------------------------------------------------------------------------
- * Gram matrix.  Lemma 1 (Sec. 4.2) works with Sigma = X X^T, whose size is
- * independent of the token count n (Sec. 4.2, "Memory Footprint").
+ * Gram matrix.  Lemma 1 (Sec. 3.2) works with Sigma = X X^T, whose size is
+ * independent of the token count n (Sec. 3.2, "Memory Footprint").
  *   Sigma (+)= X X^T; then, if damp > 0, Sigma_jj += damp * mean_j(Sigma_jj).
  * X: p x n (QE_LAYOUT_PN) or n x p (QE_LAYOUT_NP), fp32, device.
  * Sigma: p x p fp32, device; overwritten (accumulate = 0) or added to
@@ -105,23 +105,23 @@ qe_status qe_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma
 
 /* ------------------------------------------------------------------------
  * Per-row uniform grid Q_i = { scale_i (k - zero_i) : k = 0 .. 2^bits - 1 }
- * (Sec. 3: uniformly spaced levels per output channel).  Asymmetric min/max
+ * (Sec. 2.1: uniformly spaced levels per output channel).  Asymmetric min/max
  * reading: lo = min(0, min_j W_ij), hi = max(0, max_j W_ij), an all-zero row
  * uses [-1, 1]; scale = (hi - lo) / (2^bits - 1), zero = rint(-lo / scale),
  * all in fp32.  Entries with H_ij != 0 are excluded (outlier-aware grid,
- * Sec. 5.3); H may be NULL.
+ * Sec. 4.3); H may be NULL.
  * W, H: q x p device.  scale, zero: q floats each, device, written.
  * ------------------------------------------------------------------------ */
 qe_status qe_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, int bits,
                          float* scale, float* zero, void* stream);
 
 /* ------------------------------------------------------------------------
- * Blocked cyclic coordinate descent (Sec. 4; Lemma 1; the rank-1 identity of
- * Sec. 4.2; Algorithm "QuantEase").
+ * Blocked cyclic coordinate descent (Sec. 3; Lemma 1; the rank-1 identity of
+ * Sec. 3.2; Algorithm "QuantEase").
  * Residual form: R = (What - W) Sigma.  For each column j in order, for all
  * rows i at once:  beta = What_ij - R_ij / Sigma_jj;  What_ij <- q_i(beta)
  * (nearest grid level, half to even, a valid equally-near current level is
- * kept, Sec. 4.3);  R += (What_new - What_old)_{:,j} Sigma_{j,:}.
+ * kept, Sec. 3.3);  R += (What_new - What_old)_{:,j} Sigma_{j,:}.
  * Columns are processed in blocks of `block` (0 = 128; one of 16, 32, 64,
  * 128): inside a block the rank-1 updates touch only the block's columns;
  * the accumulated block update is then applied to every column as one
@@ -136,7 +136,7 @@ qe_status qe_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, i
  * sweeps: >= 0 full passes over the columns.
  * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_PERIOD(k).
  *         Without QE_INIT_FROM_W and without QE_R_VALID, R is first
- *         computed as (What - W) Sigma (warm start from any What, Sec. 4.1).
+ *         computed as (What - W) Sigma (warm start from any What, Sec. 3.1).
  * obj:    NULL, or device array of `sweeps` doubles receiving
  *         f_k = <What - W, R> = ||(W - What) X||_F^2 after sweep k.
  * ------------------------------------------------------------------------ */
@@ -147,7 +147,7 @@ qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, 
                       void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * Outlier-aware QuantEase (Sec. 5, Algorithm "Outlier-Aware QuantEase").
+ * Outlier-aware QuantEase (Sec. 4, Algorithm "Outlier-Aware QuantEase").
  * Per iteration: one CD sweep on What with H fixed (linear term from
  * W - H, residual E = (What + H - W) Sigma), then one iterative-hard-
  * thresholding step  H <- P_s(H - eta grad_H g),  grad_H g = 2E,
@@ -161,7 +161,7 @@ qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, 
  *           indices of H's nonzeros.  support_nnz: device int64, in/out.
  * s:        outlier budget, 0 <= s <= q*p.  lambda_max > 0 (qe_lambda_max).
  * flags:    QE_INIT_FROM_W: What = W - H (H and support as given, e.g. from
- *           qe_topk_abs on W, Sec. 5.3 initialisation), E = 0.
+ *           qe_topk_abs on W, Sec. 4.3 initialisation), E = 0.
  *           QE_R_VALID: E already valid.  QE_CODES_VALID as above.
  *           QE_OUTLIER_COLUMNS: structured outliers (whole columns); start
  *           from qe_topk_columns on W.
@@ -179,7 +179,7 @@ qe_status qe_cd_outlier_sweep(const float* W, const float* Sigma, int64_t q, int
                               void* stream);
 
 /* ------------------------------------------------------------------------
- * P_s of Sec. 5.3 on a dense array: keep the s entries largest in absolute
+ * P_s of Sec. 4.3 on a dense array: keep the s entries largest in absolute
  * value (ties: lower index first; exact zeros never kept).
  * V: `count` floats, device.  out: `count` floats, device: P_s(V).
  * support: device int64[s]: kept indices, ascending.  nnz: device int64.
@@ -189,7 +189,7 @@ qe_status qe_topk_abs(const float* V, int64_t count, int64_t s, float* out, int6
                       int64_t* nnz, void* ws, size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * Structured projection ("Structured Outliers", Sec. 5.3): keep the c whole
+ * Structured projection ("Structured Outliers", Sec. 4.3): keep the c whole
  * columns of the q x p matrix V with the largest l2 norm, zero elsewhere.
  * Selection key of column j: sum_i V_ij^2 accumulated in fp64, rounded to
  * fp32; ties go to the lower column; all-zero columns are never kept.
@@ -205,7 +205,7 @@ qe_status qe_topk_columns(const float* V, int64_t q, int64_t p, int64_t c, float
                           size_t ws_bytes, void* stream);
 
 /* ------------------------------------------------------------------------
- * Exact objective and its normaliser (Sec. 3 problem (1); Sec. 4.4 relative
+ * Exact objective and its normaliser (Sec. 2.1 problem (1); Sec. 3.4 relative
  * calibration error), recomputed from scratch, independent of R:
  *   out[0] = <D, D Sigma> = ||(What + H - W) X||_F^2,  D = What + H - W,
  *   out[1] = <W, W Sigma> = ||W X||_F^2.
@@ -218,7 +218,7 @@ qe_status qe_objective(const float* W, const float* W_hat, const float* H, const
                        void* stream);
 
 /* ------------------------------------------------------------------------
- * lambda_max(Sigma) by the power method (Sec. 5.3: matrix-vector products
+ * lambda_max(Sigma) by the power method (Sec. 4.3: matrix-vector products
  * only, O(p^2) per iteration).  Start vector 1/sqrt(p); the estimate is the
  * Rayleigh quotient; the result is that of the first iteration whose quotient
  * changed by at most tol (relative) from the previous one, else of iteration
@@ -231,7 +231,7 @@ qe_status qe_lambda_max(const float* Sigma, int64_t p, int max_iters, float tol,
 
 /* ------------------------------------------------------------------------
  * Export for serving.  The paper leaves serving kernels out of scope
- * (Sec. 5.3, "Structured Outliers"); these layouts are this library's.
+ * (Sec. 4.3, "Structured Outliers"); these layouts are this library's.
  *
  * qe_pack_codes: each row of the q x p codes (device uint8, values < 2^bits,
  * bits in [1, 8]) becomes one little-endian bit stream of

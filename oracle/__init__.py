@@ -44,7 +44,15 @@ def _load():
     if not os.path.exists(_LIB_PATH):
         from . import build as _build
         _build.build()
-    lib = ctypes.CDLL(_LIB_PATH)
+    _lib = bind(_LIB_PATH)
+    return _lib
+
+
+def bind(path: str) -> ctypes.CDLL:
+    """Loads a build of qe_oracle.c from ``path`` and declares its signatures
+    (the tests also bind deliberately broken copies of the source, to show
+    that the pins catch each such mistake)."""
+    lib = ctypes.CDLL(path)
     lib.qeo_gram.argtypes = [_f32p, _i64, _i64, ctypes.c_int, _f64p]
     lib.qeo_gram.restype = None
     lib.qeo_gram_entries.argtypes = [_f32p, _i64, _i64, ctypes.c_int, _i64p, _i64p, _i64, _f64p]
@@ -64,7 +72,6 @@ def _load():
     lib.qeo_topk_abs.restype = _i64
     lib.qeo_num_threads.argtypes = []
     lib.qeo_num_threads.restype = ctypes.c_int
-    _lib = lib
     return lib
 
 
@@ -167,7 +174,7 @@ def dequant(codes: np.ndarray, scale: np.ndarray, zero: np.ndarray) -> np.ndarra
 
 # --------------------------------------------------------------------------
 # Export for serving: bit-packed codes and the outliers in CSR form.  The
-# paper leaves serving kernels out of scope (Sec. 5.3, "Structured
+# paper leaves serving kernels out of scope (Sec. 4.3, "Structured
 # Outliers"); the layout here is this library's: each row of codes is one
 # little-endian bit stream, code j in bits [j*bits, (j+1)*bits), bytes
 # filled from their least significant bit; rows start on a byte boundary.
@@ -205,7 +212,7 @@ def outliers_csr(H: np.ndarray, support: np.ndarray):
 
 
 # --------------------------------------------------------------------------
-# Objective (problem (1) of Sec. 3) and relative calibration error (Sec. 4.4)
+# Objective (problem (1) of Sec. 2.1) and relative calibration error (Sec. 3.4)
 # --------------------------------------------------------------------------
 def objective(W, What, Sigma, H=None) -> float:
     """f = ||W X - (What + H) X||_F^2 written through Sigma = X X^T:
@@ -225,7 +232,7 @@ def rel_error(W, What, Sigma, H=None) -> float:
 
 
 # --------------------------------------------------------------------------
-# Coordinate descent (Sec. 4)
+# Coordinate descent (Sec. 3)
 # --------------------------------------------------------------------------
 @dataclass
 class CDResult:
@@ -244,7 +251,7 @@ def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
     """Cyclic CD sweeps of QuantEase.
 
     W: q x p weights; Sigma: p x p (used as given, promoted to fp64);
-    scale, zero: the per-row grid; W0: initial What (default W, Sec. 4.1);
+    scale, zero: the per-row grid; W0: initial What (default W, Sec. 3.1);
     codes0/codes_valid: grid codes of W0 when W0 is on the grid.
     form: 'lemma1' (direct closed form), 'alg1' (rank-1 bookkeeping),
     'alg2' (accelerated partial update).  target: the matrix whose product
@@ -313,7 +320,7 @@ def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
 
 
 # --------------------------------------------------------------------------
-# Outlier-aware QuantEase (Sec. 5, Algorithm "Outlier-Aware QuantEase")
+# Outlier-aware QuantEase (Sec. 4, Algorithm "Outlier-Aware QuantEase")
 # --------------------------------------------------------------------------
 def topk_abs(V: np.ndarray, s: int):
     """P_s(V): the s entries largest in |V| (ties: lower linear index first;
@@ -340,7 +347,7 @@ def column_keys(V: np.ndarray) -> np.ndarray:
 
 
 def topk_columns(V: np.ndarray, c: int):
-    """Structured P (Sec. 5.3, "Structured Outliers"): keep the c columns of V
+    """Structured P (Sec. 4.3, "Structured Outliers"): keep the c columns of V
     with the largest l2 norm (ties: lower column index first; all-zero
     columns never kept), zero elsewhere.  Returns (kept columns ascending,
     support as ascending linear indices of every entry of those columns,
@@ -375,7 +382,7 @@ class OutlierResult:
 
 
 def outlier_init(W, s: int, structured: bool = False):
-    """H = P_s(W), What = W - H (Sec. 5.3, initialisation).  structured: the
+    """H = P_s(W), What = W - H (Sec. 4.3, initialisation).  structured: the
     column projection with floor(s / q) columns instead of P_s."""
     Wd = np.asarray(W, np.float64)
     if structured:
@@ -387,11 +394,11 @@ def outlier_init(W, s: int, structured: bool = False):
 
 def outlier(W, Sigma, bits: int, scale, zero, s: int, lam: float, sweeps: int,
             record: bool = True, structured: bool = False) -> OutlierResult:
-    """Block coordinate descent of Sec. 5.3: per iteration, one CD sweep on
+    """Block coordinate descent of Sec. 4.3: per iteration, one CD sweep on
     What with H fixed (target W - H), then one IHT step
     H <- P_s(H - eta grad_H g), grad_H g = 2 (H + What - W) Sigma, eta = 1/(2 lam).
     structured: P_s is replaced by the column projection keeping the
-    floor(s / q) columns of largest l2 norm ("Structured Outliers", Sec. 5.3).
+    floor(s / q) columns of largest l2 norm ("Structured Outliers", Sec. 4.3).
     ``scale``/``zero`` must be the outlier-aware grid (outliers of W excluded)."""
     W = np.asarray(W)
     Wd = W.astype(np.float64)

@@ -6,7 +6,7 @@
  * leg may load this library; the product path never does.  It shares no source,
  * header, table or helper with the HIP library.
  *
- * Notation follows the paper (Sec. 3, "Problem Formulation: Layerwise Quantization"):
+ * Notation follows the paper (Sec. 2.1, "Problem Formulation: Layerwise Quantization"):
  *   W  (q x p)  layer weights, row-major;  X (p x n) layer input;
  *   Sigma = X X^T (p x p);  What = the quantized weights;
  *   per-row grid Q_i = { s_i (k - z_i) : k = 0 .. 2^b - 1 }.
@@ -60,12 +60,12 @@ void qeo_gram_entries(const float* X, int64_t p, int64_t n, int layout,
 }
 
 /* ------------------------------------------------------------------------- */
-/* Per-row uniform grid (Sec. 3: levels uniformly spaced, per output channel). */
+/* Per-row uniform grid (Sec. 2.1: levels uniformly spaced, per output channel). */
 /* The paper does not print the formula; the reading used is the asymmetric     */
 /* min/max grid: lo = min(0, min_j W_ij), hi = max(0, max_j W_ij) over the      */
 /* entries not excluded, scale = (hi - lo) / (2^b - 1), zero = rint(-lo/scale); */
 /* an all-zero row uses lo = -1, hi = +1.  Entries with H_ij != 0 are left out  */
-/* (outlier-aware grid, Sec. 5.3: the top-s weights are removed from the pool). */
+/* (outlier-aware grid, Sec. 4.3: the top-s weights are removed from the pool). */
 /* Computed in fp32 on purpose (see the file header).                           */
 /* ------------------------------------------------------------------------- */
 void qeo_grid_minmax(const float* W, int64_t q, int64_t p, int bits, const float* H,
@@ -89,8 +89,8 @@ void qeo_grid_minmax(const float* W, int64_t q, int64_t p, int bits, const float
 }
 
 /* ------------------------------------------------------------------------- */
-/* The quantizer q_i (Sec. 3, eq. quant) with the modified-CD tie rule          */
-/* (Sec. 4.3): the coordinate moves only if the move strictly decreases f.      */
+/* The quantizer q_i (Sec. 2.1, eq. quant) with the modified-CD tie rule          */
+/* (Sec. 3.3): the coordinate moves only if the move strictly decreases f.      */
 /* t is the unconstrained minimiser expressed in grid units, t = beta/s + z.    */
 /* The 1-D objective is proportional to (s (k - z) - beta)^2 = s^2 (k - t)^2,    */
 /* so the nearest grid code is the exact minimiser over Q_i; ties between two   */
@@ -125,12 +125,12 @@ static double boundary_margin(double t, int maxq)
 /* One cyclic CD sweep in the direct form of Lemma 1:                           */
 /*   beta = -[ sum_{k != j} Sigma_jk What_ik - T_ij ] / Sigma_jj,               */
 /*   What_ij <- q_i(beta),                                                      */
-/* for j = 1..p in order, all rows i (rows are independent, Sec. 4.2).          */
+/* for j = 1..p in order, all rows i (rows are independent, Sec. 3.2).          */
 /* T = W Sigma for the basic problem, T = (W - H) Sigma for the outlier-aware    */
-/* CD step (Sec. 5.3 / Algorithm "Outlier-Aware QuantEase").                     */
+/* CD step (Sec. 4.3 / Algorithm "Outlier-Aware QuantEase").                     */
 /* valid[i*p+j] != 0 means What_ij currently sits on grid code codes[i*p+j].    */
 /* relax != 0 writes beta unquantized (the paper's occasional unquantized pass, */
-/* Sec. 4.2 "Initialization") and marks the codes invalid.                      */
+/* Sec. 3.2 "Initialization") and marks the codes invalid.                      */
 /* margin (nullable) receives boundary_margin(t) of every decision.             */
 /* Returns 0, or 1 if some Sigma_jj <= 0 (Lemma 1 footnote).                    */
 /* ------------------------------------------------------------------------- */
@@ -240,7 +240,7 @@ void qeo_cd_sweep_alg2(const double* P, const double* N, int64_t q, int64_t p, i
 }
 
 /* ------------------------------------------------------------------------- */
-/* P_s (Sec. 5.3, eq. iht-update): keep the s entries of V largest in absolute  */
+/* P_s (Sec. 4.3, eq. iht-update): keep the s entries of V largest in absolute  */
 /* value, zero the rest.  Ties in |V| go to the lower linear index i*p+j;       */
 /* entries equal to zero are never part of the support.                         */
 /* Writes the support as ascending linear indices; returns its size.            */

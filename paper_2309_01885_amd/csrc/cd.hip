@@ -1,9 +1,9 @@
 // Blocked cyclic coordinate descent of QuantEase on gfx950.
 //
 // State: What (q x p), codes (q x p, uint8) and the residual R = (What - W) Sigma.
-// Lemma 1 (Sec. 4.2) in residual form: for column j and every row i,
+// Lemma 1 (Sec. 3.2) in residual form: for column j and every row i,
 //     beta = What_ij - R_ij / Sigma_jj,   What_ij <- q_i(beta),
-// and the rank-1 identity of Sec. 4.2 (both halves fused, as the paper's
+// and the rank-1 identity of Sec. 3.2 (both halves fused, as the paper's
 // acceleration note suggests) keeps R exact:  R += delta_{:,j} Sigma_{j,:}.
 //
 // Columns are taken in blocks J of width B (the panel width), grouped into
@@ -59,7 +59,7 @@ __global__ void grid_prep_kernel(const float* __restrict__ scale, const float* _
     }
 }
 
-// What = W - H (H may be null), R = 0 (Sec. 4.1 / Sec. 5.3 initialisation).
+// What = W - H (H may be null), R = 0 (Sec. 3.1 / Sec. 4.3 initialisation).
 __global__ void init_from_w_kernel(const float* __restrict__ W, const float* __restrict__ H,
                                    float* Wh, float* R, int64_t count, const int* status)
 {
@@ -178,8 +178,8 @@ struct StepArgs {
     int sbw, psbw;        // their widths (<= S)
     int S;                // super-block width = row stride of dcur / dprev
     float maxq;
-    int codes_valid;      // current codes may be kept on an exact tie (Sec. 4.3)
-    int relax;            // write beta unquantized (relaxed sweep, Sec. 4.2)
+    int codes_valid;      // current codes may be kept on an exact tie (Sec. 3.3)
+    int relax;            // write beta unquantized (relaxed sweep, Sec. 3.2)
     int fp32;             // GEMM role on the fp32 matrix cores (else the split bf16 ones)
     int n_panel;          // workgroups [0, n_panel) run the panel
     int64_t tiles_n;      // GEMM column tiles

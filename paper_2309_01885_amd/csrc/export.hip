@@ -1,5 +1,5 @@
 // Export of a quantized layer for serving: bit-packed codes and the outliers
-// in CSR form.  The paper leaves serving kernels out of scope (Sec. 5.3,
+// in CSR form.  The paper leaves serving kernels out of scope (Sec. 4.3,
 // "Structured Outliers"); the layouts are this library's (see qe.h).
 #include "qe_internal.h"
 

@@ -5,7 +5,7 @@
 // (gram_x3_kernel, see nt_x3.h); with QE_GRAM_FP32 on the fp32 matrix cores
 // (gram_kernel).  Both share the work split and the reductions below.
 //
-// Lemma 1 (Sec. 4.2) needs X only through Sigma, a p x p statistic whose size
+// Lemma 1 (Sec. 3.2) needs X only through Sigma, a p x p statistic whose size
 // does not grow with the token count n.  Work split: 128 x 128 tiles of the
 // upper triangle (ti <= tj) x token splits of at most kSplitTokensMax tokens,
 // their count chosen to fill the last round of workgroups (gram_splits).

@@ -5,10 +5,10 @@
 namespace qe {
 
 // ---------------------------------------------------------------- grid
-// Per-row asymmetric min/max grid (Sec. 3: uniformly spaced levels per output
+// Per-row asymmetric min/max grid (Sec. 2.1: uniformly spaced levels per output
 // channel; the paper does not print the formula, see qe.h): one workgroup per
 // row, min/max reductions (exact in any order), then the scale and zero point
-// in fp32.  Entries with H != 0 are excluded (outlier-aware grid, Sec. 5.3).
+// in fp32.  Entries with H != 0 are excluded (outlier-aware grid, Sec. 4.3).
 __global__ __launch_bounds__(256) void grid_minmax_kernel(const float* __restrict__ W,
                                                           const float* __restrict__ H, int64_t p,
                                                           float maxq, float* scale, float* zero)
@@ -235,7 +235,7 @@ qe_status launch_objective(const float* W, const float* Wh, const float* H, cons
 }
 
 // ---------------------------------------------------------------- lambda_max
-// Power method (Sec. 5.3): v_k = y_{k-1} / ||y_{k-1}|| (v_0 = 1/sqrt(p)),
+// Power method (Sec. 4.3): v_k = y_{k-1} / ||y_{k-1}|| (v_0 = 1/sqrt(p)),
 // y_k = Sigma v_k, lambda_k = v_k . y_k (Rayleigh quotient of the unit v_k).
 // One kernel per iteration: every workgroup first forms 1/||y_{k-1}|| from the
 // previous iteration's per-workgroup partials (same fixed-order sum in every

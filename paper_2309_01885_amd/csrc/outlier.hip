@@ -1,7 +1,7 @@
-// Outlier-aware QuantEase (Sec. 5) on gfx950: P_s by radix select, the IHT
+// Outlier-aware QuantEase (Sec. 4) on gfx950: P_s by radix select, the IHT
 // step and the sparse residual update.
 //
-// P_s (Sec. 5.3) keeps the s entries of largest |v|.  |v| of an fp32 value is
+// P_s (Sec. 4.3) keeps the s entries of largest |v|.  |v| of an fp32 value is
 // ordered exactly like its bit pattern with the sign cleared, so the s-th
 // largest key tau is found by a 3-pass radix select (digits of 11, 11 and 10
 // bits; per-workgroup LDS histograms merged with integer atomics, so counts
@@ -10,7 +10,7 @@
 // zeros.  Compaction keeps index order (per-workgroup counts, a scan, then
 // wavefront ballots inside each workgroup), so the support comes out sorted.
 //
-// IHT step (Sec. 5.3, Lemma 3): V = H - E / lambda_max, H+ = P_s(V), then
+// IHT step (Sec. 4.3, Lemma 3): V = H - E / lambda_max, H+ = P_s(V), then
 // E += (H+ - H) Sigma.  The old and new supports are merged into one list
 // sorted by linear index (an entry in both carries new - old); the sparse
 // product walks each row's stretch of that list in ascending index.
@@ -357,7 +357,7 @@ qe_status launch_topk(const float* V, int64_t count, int64_t s, float* out, int6
 }
 
 // ---------------------------------------------------------------- IHT step
-// V = H - E / lambda (Sec. 5.3: eta = 1 / (2 lambda_max), gradient 2E), and
+// V = H - E / lambda (Sec. 4.3: eta = 1 / (2 lambda_max), gradient 2E), and
 // the first-digit histogram of |V| for the radix select in the same pass.
 __global__ __launch_bounds__(256) void iht_target_kernel(const float* __restrict__ H,
                                                          const float* __restrict__ E,
@@ -619,7 +619,7 @@ __global__ __launch_bounds__(256) void spmm_delta_kernel(const int64_t* __restri
 }
 
 // ---------------------------------------------------------------- structured projection
-// "Structured Outliers" (Sec. 5.3): keep the floor(s / q) whole columns of V
+// "Structured Outliers" (Sec. 4.3): keep the floor(s / q) whole columns of V
 // with the largest l2 norm.  Key of column j: sum_i V_ij^2 in fp64 (row
 // chunks summed in a fixed order), rounded to fp32; the columns are then
 // chosen by the radix select above (ties: lower column first; all-zero

@@ -6,7 +6,7 @@ paper's workloads; it contains none of the method's arithmetic (no Gram
 matrix, no grid, no quantization).
 
 The paper calibrates on 128 sequences x 2048 tokens of C4 pushed through OPT,
-BLOOM and Falcon layers (Sec. 6, experimental setup); neither the dataset nor
+BLOOM and Falcon layers (Sec. 5, experimental set-up); neither the dataset nor
 the weights exist here, so these generators stand in for them with layers of
 the same shapes: Gaussian weights with a sprinkle of large entries, and
 heavy-tailed (Student-t, nu = 4) activations with a few outlier channels.

@@ -1,4 +1,4 @@
-"""GPU parity of qe_cd_sweep (Sec. 4: Lemma 1, the rank-1 identity, blocked)
+"""GPU parity of qe_cd_sweep (Sec. 3: Lemma 1, the rank-1 identity, blocked)
 against the fp64 oracle, on the same seeded fp32 inputs.
 
 Bar (per sweep, parity.check_row_sampled_sweeps over all rows): rows whose
@@ -214,7 +214,7 @@ def test_hand_fixture(qe):
 @pytest.mark.parametrize("fp32", [False, True])
 @pytest.mark.parametrize("q,p", [(120, 200), (256, 384)])
 def test_warm_start_from_arbitrary_what(qe, oracle, q, p, fp32):
-    # Sec. 4.1: CD may start from any What (e.g. another quantizer's output);
+    # Sec. 3.1: CD may start from any What (e.g. another quantizer's output);
     # the residual is then formed by a full product (R = (What - W) Sigma)
     W, X = layer(q, p, 1024, 25, corr=0.9)
     S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)

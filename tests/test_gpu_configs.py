@@ -4,7 +4,7 @@
   exact objective) against the oracle on every entry.
 * c3 (11008 x 4096 and 4096 x 11008, 3-bit, 10 sweeps): CD on all rows; the
   oracle replays a seeded row sample with the same Sigma (rows are
-  independent, Sec. 4.2).  The down-projection Gram is also checked at its
+  independent, Sec. 3.2).  The down-projection Gram is also checked at its
   full 11008 x 262144 size on sampled entries.
 * c4 (4096 x 4096, 3-bit, s = 1% outliers, 10 iterations): the whole CD + IHT
   run against the oracle's whole run.  g must agree within 1e-4 after every
@@ -218,7 +218,7 @@ def test_c5_cd_row_sampled(qe, oracle):
 
 
 def test_c4_structured_outlier_run(qe, oracle):
-    """The outlier-aware configuration with structured outliers (Sec. 5.3):
+    """The outlier-aware configuration with structured outliers (Sec. 4.3):
     floor(s / q) = 40 whole columns, 4 iterations against the oracle."""
     spec = synth.CONFIGS["c4"]
     q, p, bits, s = spec.q, spec.p, spec.bits, spec.s_budget

@@ -5,7 +5,7 @@ launch configuration the benchmark times (block width 128).
   a seeded 128 x 128 grid of entries (outlier channels included) against
   the oracle's one-by-one dot products; relative Frobenius <= 1e-5.
 * CD sweeps on all 4096 rows; the oracle replays a seeded sample of 64 rows
-  with the same Sigma (rows are independent, Sec. 4.2, so the comparison is
+  with the same Sigma (rows are independent, Sec. 3.2, so the comparison is
   exact): identical codes and objective within 1e-4 over the rows whose
   trajectories never split, every split at a near tie and followed by
   descent, at most max(2, 1e-6 x decisions) split rows

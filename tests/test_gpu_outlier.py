@@ -1,4 +1,4 @@
-"""GPU parity of the outlier-aware path (Sec. 5): P_s, lambda_max and the
+"""GPU parity of the outlier-aware path (Sec. 4): P_s, lambda_max and the
 full CD + IHT iteration, against the fp64 oracle.
 
 P_s on the same fp32 V is an integer decision taken in the same precision by
@@ -138,7 +138,7 @@ def test_zero_budget_equals_plain_cd(qe, oracle):
     assert not np.any(g["H"])
 
 
-# ---- structured (column) outliers, Sec. 5.3 "Structured Outliers"
+# ---- structured (column) outliers, Sec. 4.3 "Structured Outliers"
 @pytest.mark.parametrize("q,p,c", [(64, 300, 7), (512, 512, 5), (33, 70, 0), (40, 50, 60)])
 def test_topk_columns_identical(qe, oracle, q, p, c):
     V = synth.gaussian((q, p), seed=41)

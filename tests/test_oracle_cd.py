@@ -1,4 +1,4 @@
-"""Pins for the oracle's coordinate descent (Sec. 4).
+"""Pins for the oracle's coordinate descent (Sec. 3).
 
 What fixes the oracle here, other than the oracle itself:
 * eq. (cd-highlevel) solved by brute force -- every grid value of a coordinate
@@ -7,7 +7,7 @@ What fixes the oracle here, other than the oracle itself:
 * Lemma 2 (convergence to a coordinate-wise minimum), checked by enumeration;
 * exhaustive search over all (2^b)^p codes of a row (rows are independent):
   CD can never beat the optimum;
-* monotone f after the first feasible iterate (Sec. 4.1);
+* monotone f after the first feasible iterate (Sec. 3.1);
 * closed-form special cases: weights already on the grid, diagonal Sigma
   (round-to-nearest), exact ties, and unquantized sweeps (Gauss-Seidel on
   What Sigma = W Sigma, whose solution is What = W);
@@ -183,6 +183,25 @@ def test_on_grid_weights_are_a_fixed_point(oracle):
     assert np.array_equal(res.codes, rng)
     assert np.array_equal(res.What, W.astype(np.float64))
     assert all(f == 0.0 for f in res.obj)
+
+
+def test_iterates_stay_on_the_grid(oracle):
+    """Problem (1) is feasible only on Q_i: after every quantized sweep each
+    code lies in [0, 2^b - 1] and What equals its grid level, also when the
+    grid is too narrow for W (half the min/max step), so that Lemma 1's
+    minimiser often falls outside the grid and must be clamped to its end."""
+    W, X = small_layer(12, 20, 60, 61, 0.9)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    bits = 2
+    scale, zero = oracle.grid_minmax(W, bits)
+    scale = (scale * np.float32(0.5)).astype(np.float32)
+    res = oracle.cd(W, S, bits, scale, zero, 3)
+    t0 = W.astype(np.float64) / scale[:, None] + zero[:, None]
+    assert np.any(t0 > 2 ** bits - 1) and np.any(t0 < 0)      # the clamp is exercised
+    for k in range(3):
+        c = res.codes_hist[k]
+        assert c.min() >= 0 and c.max() <= 2 ** bits - 1
+        assert np.array_equal(res.what_hist[k], oracle.dequant(c, scale, zero))
 
 
 def test_diagonal_sigma_is_round_to_nearest(oracle):

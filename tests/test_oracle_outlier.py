@@ -1,8 +1,8 @@
-"""Pins for the oracle's outlier-aware path (Sec. 5).
+"""Pins for the oracle's outlier-aware path (Sec. 4).
 
 * P_s against an independent selection (numpy lexsort on (-|v|, index));
 * Lemma 3: the IHT step never increases g (H sparse, ||H||_0 <= s);
-* s = 0 reduces to the plain CD of Sec. 4;
+* s = 0 reduces to the plain CD of Sec. 3;
 * Sigma = c I: V = H - E/c = W - What in closed form, so H+ = P_s(W - What);
 * lambda_max on a matrix with known eigenvalues (Householder-rotated diagonal);
 * the initialisation H = P_s(W), What = W - H keeps What + H = W exactly.
@@ -105,6 +105,40 @@ def test_identity_sigma_closed_form(oracle):
     assert np.array_equal(r.H, Hp)
 
 
+def test_identity_sigma_step_size(oracle):
+    """With Sigma = c I and eta = 1/(2c), V = H - eta 2 (What + H - W) c is
+    W - What whatever H is.  The grid's zero point is moved half a step, so
+    0 is not a level and every kept entry carries a rounding residue: a
+    wrong step size then changes V's values on the support."""
+    W, _ = _layer(12, 16, 10, 7)
+    c = 4.0
+    S = c * np.eye(16)
+    s = 20
+    sup0, H0, _ = oracle.outlier_init(W, s)
+    sc, ze = oracle.grid_minmax(W, 3, H0)
+    ze = (ze + np.float32(0.5)).astype(np.float32)
+    r = oracle.outlier(W, S, 3, sc, ze, s, c, 1)
+    V = W.astype(np.float64) - r.What
+    sup, Hp = oracle.topk_abs(V, s)
+    assert np.array_equal(r.support, sup)
+    assert np.allclose(r.H, Hp, rtol=1e-12, atol=0)
+    assert np.min(np.abs(r.What.reshape(-1)[sup])) > 0.25 * np.min(sc)
+
+
+def test_topk_budget_cuts_a_tie_group(oracle):
+    """The budget ends inside a group of equal |V|: the lower linear indices
+    of the group are kept (ties: lower index first)."""
+    V = synth.uniform((20, 30), seed=9, lo=-0.4, hi=0.4)
+    V.reshape(-1)[::6] = 0.5             # 100 tied entries, alternating sign
+    V.reshape(-1)[3::12] = -0.5
+    V.reshape(-1)[1::60] = 1.0           # 10 entries above the group
+    s = 60
+    sup, _ = oracle.topk_abs(V, s)
+    assert np.array_equal(sup, lexsort_topk(V, s))
+    tied = np.nonzero(np.abs(V.reshape(-1)) == 0.5)[0]
+    assert np.array_equal(np.intersect1d(sup, tied), tied[:s - 10])
+
+
 def test_lambda_max_known_spectrum(oracle):
     p = 40
     lam = np.linspace(0.5, 7.25, p)
@@ -115,7 +149,7 @@ def test_lambda_max_known_spectrum(oracle):
     assert oracle.lambda_max(S) == pytest.approx(7.25, rel=1e-13)
 
 
-# ---- structured (column) outliers, Sec. 5.3 "Structured Outliers"
+# ---- structured (column) outliers, Sec. 4.3 "Structured Outliers"
 def lexsort_columns(V, c):
     V = np.asarray(V, np.float64)
     key = np.sum(V * V, axis=0).astype(np.float32)
