@@ -124,6 +124,23 @@ def gram(X: np.ndarray, layout: int = 0) -> np.ndarray:
     return out
 
 
+def gram_blas(X: np.ndarray, layout: int = 0, chunk: int = 8192, out=None,
+              row_block: int = 8192) -> np.ndarray:
+    """Sigma = X X^T in fp64 through the library product (numpy's BLAS), one
+    token chunk at a time: Sigma = sum_c X_c X_c^T, each chunk promoted to
+    fp64 (and, for very wide layers, row_block output rows per product).
+    The same definition as ``gram``; for layers too large for the plain
+    loops.  ``out`` (p x p fp64), if given, is accumulated into."""
+    X = np.asarray(X)
+    p, n = (X.shape if layout == 0 else X.shape[::-1])
+    S = np.zeros((p, p), np.float64) if out is None else out
+    for t0 in range(0, n, chunk):
+        Xc = (X[:, t0:t0 + chunk] if layout == 0 else X[t0:t0 + chunk].T).astype(np.float64)
+        for r0 in range(0, p, row_block):
+            S[r0:r0 + row_block] += Xc[r0:r0 + row_block] @ Xc.T
+    return S
+
+
 def gram_entries(X: np.ndarray, ia, ib, layout: int = 0) -> np.ndarray:
     """Entries (ia[e], ib[e]) of X X^T, each a single fp64 dot product."""
     X = _c(X, np.float32)
@@ -247,7 +264,7 @@ class CDResult:
 
 def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
        codes_valid: bool = False, form: str = "lemma1", target=None,
-       relax_period: int = 0, record: bool = True, obj_H=None) -> CDResult:
+       relax_period: int = 0, record: bool = True, obj_H=None, T=None) -> CDResult:
     """Cyclic CD sweeps of QuantEase.
 
     W: q x p weights; Sigma: p x p (used as given, promoted to fp64);
@@ -259,6 +276,8 @@ def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
     CD step).  relax_period k > 0: sweeps k, 2k, ... (1-based) write beta
     unquantized; the last sweep is always quantized.
     obj_H: H added to What in the recorded objective (outlier variant).
+    T: the product target @ Sigma (fp64), if the caller already holds it
+    (several calls on the same layer); formed here otherwise.
     """
     lib = _load()
     W = np.asarray(W)
@@ -273,7 +292,7 @@ def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
     res = CDResult(What=Wh, codes=codes, valid=valid)
 
     if form == "lemma1" or form == "alg1":
-        T = _c(tgt @ S, np.float64)
+        T = _c(tgt @ S if T is None else T, np.float64)
     elif form == "alg2":
         d = np.diag(S).copy()
         N = S / d[None, :]                     # Sigma^norm_{:,j} = Sigma_{:,j} / Sigma_jj

@@ -1,6 +1,39 @@
-"""Comparison helpers shared by the GPU parity tests (no method arithmetic)."""
+"""Comparison helpers shared by the GPU parity tests (no method arithmetic:
+every number they compare comes from the HIP library or from the oracle).
+
+CD parity protocol.  CD visits the coordinates of a row in a fixed order, so
+two correct runs hold the same codes until one of them meets a tie of the
+grid distance (Lemma 1's t half-way between two levels, to within the
+rounding of the arithmetic) and takes the other, equally near level; from
+there on both rows follow valid but different CD paths, and several results
+are correct.  Two checks follow from that:
+
+* ``teacher_forced`` (binding; the per-sweep bar).  For every sweep k the
+  oracle runs that one sweep from the GPU's own state after sweep k - 1
+  (What, codes; codes valid after the first sweep), so a divergence cannot
+  carry over from one sweep to the next.  Asserted after every sweep, whether
+  or not any row splits: at most 0.1% of the sample's codes differ from the
+  oracle's; in every row the first differing code sits at an oracle tie
+  (|frac(t) - 1/2| <= 1e-4 grid units); the GPU's objective over the sample
+  agrees with the oracle's within 1e-4 relative.
+* ``free_running`` (reported; partly asserted).  The oracle runs all sweeps
+  on its own from the common start.  Asserted: each row's first divergence
+  sits at an oracle tie; rows that never split agree on the objective within
+  1e-4; split rows keep descending.  Reported: the fraction of differing
+  codes after each sweep and the number of split rows.
+
+With ``QE_PARITY_STATS`` set, both checks append their figures as one JSON
+line to that file.
+"""
+import json
+import os
+
 import numpy as np
 import torch
+
+OBJ_RTOL = 1e-4
+CODE_FRAC = 1e-3
+TIE_MARGIN = 1e-4
 
 
 def dev(a, dtype=None):
@@ -20,6 +53,13 @@ def rel_fro(a, b):
     return float(np.linalg.norm(a - b) / np.linalg.norm(b))
 
 
+def log_stats(record):
+    path = os.environ.get("QE_PARITY_STATS")
+    if path:
+        with open(path, "a") as f:
+            f.write(json.dumps(record) + "\n")
+
+
 def first_divergence(codes_gpu_hist, codes_ref_hist):
     """For each row, the (sweep, column) of the first code that differs
     between the two sweep histories, scanning sweeps in order and columns in
@@ -34,49 +74,108 @@ def first_divergence(codes_gpu_hist, codes_ref_hist):
     return out
 
 
-def check_row_sampled_sweeps(W_rows, S64, whats, Rs, codes_hist, ref, obj_rtol=1e-4,
-                             tie_margin=1e-4, max_split_rate=1e-6):
-    """Per-sweep comparison of a row sample against the oracle's replay.
+def gpu_row_objective(W_rows, what, R):
+    """f_i = <What_i - W_i, R_i> per row from the GPU's own residual (fp64 sum)."""
+    return np.sum((np.asarray(what, np.float64) - np.asarray(W_rows, np.float64))
+                  * np.asarray(R, np.float64), axis=1)
 
-    CD visits the coordinates of a row in a fixed order, so two correct runs
-    share every code until one of them meets an exact tie of the grid
-    distance and takes the other, equally near level; from there on both rows
-    are valid but different CD paths (several results are correct).  So:
-    rows that never split must hold identical codes after every sweep and
-    their objective must agree within obj_rtol; every split must start at an
-    oracle tie (margin <= tie_margin grid units); split rows must stay valid
-    CD paths (their objective never increases); splits must be rare (fp32
-    rounding of t reaches ~1e-6 grid units, so about one decision in a
-    million sits that close to a tie: at most max(2, max_split_rate x the
-    number of decisions) splits).  Returns the number of split rows."""
+
+def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs, *,
+                   W0=None, codes0=None, codes_valid0=False, T=None, gpu_obj=None,
+                   label="", obj_rtol=OBJ_RTOL, code_frac=CODE_FRAC, tie_margin=TIE_MARGIN):
+    """Per-sweep teacher-forced comparison of a GPU run with the oracle.
+
+    W_rows, scale, zero: the rows compared (all rows of the layer, or a
+    seeded sample: rows are independent, so a sample is exact).  codes_hist,
+    whats, Rs: the GPU's codes, What and R of those rows after each sweep.
+    W0/codes0/codes_valid0: the state the GPU's first sweep started from
+    (default: What = W, codes not valid).  gpu_obj: optional per-sweep
+    objective the library reported for exactly these rows.  Returns the
+    per-sweep figures."""
     W64 = np.asarray(W_rows, np.float64)
+    if T is None:
+        T = W64 @ S64
+    sweeps = len(codes_hist)
+    stats = []
+    for k in range(sweeps):
+        if k == 0:
+            start_w = W64 if W0 is None else np.asarray(W0, np.float64)
+            start_c = None if codes0 is None else np.asarray(codes0, np.int32)
+            valid = codes_valid0
+        else:
+            start_w = np.asarray(whats[k - 1], np.float64)
+            start_c = np.asarray(codes_hist[k - 1], np.int32)
+            valid = True
+        ref = oracle.cd(W_rows, S64, bits, scale, zero, 1, W0=start_w, codes0=start_c,
+                        codes_valid=valid, T=T)
+        g = np.asarray(codes_hist[k])
+        diff = g != ref.codes
+        frac = float(diff.mean())
+        split_rows = np.nonzero(diff.any(axis=1))[0]
+        margins = [float(ref.margin_hist[0][i, int(np.argmax(diff[i]))]) for i in split_rows]
+        f_ref = ref.obj[0]
+        f_gpu = float(np.sum(gpu_row_objective(W_rows, whats[k], Rs[k])))
+        rec = {"sweep": k + 1, "code_diff_frac": frac, "split_rows": int(len(split_rows)),
+               "max_first_margin": max(margins) if margins else 0.0,
+               "obj_rel_err": abs(f_gpu - f_ref) / abs(f_ref) if f_ref else abs(f_gpu)}
+        if gpu_obj is not None:
+            rec["reported_obj_rel_err"] = (abs(gpu_obj[k] - f_ref) / abs(f_ref) if f_ref
+                                           else abs(gpu_obj[k]))
+        stats.append(rec)
+        where = f"{label} sweep {k + 1}"
+        assert frac <= code_frac, f"{where}: {frac:.3e} of codes differ (teacher-forced)"
+        for i, m in zip(split_rows, margins):
+            assert m <= tie_margin, \
+                f"{where}: row {i} first differs at column {int(np.argmax(diff[i]))}, " \
+                f"oracle margin {m:.3e} grid units (not a tie)"
+        assert rec["obj_rel_err"] <= obj_rtol, \
+            f"{where}: objective {f_gpu!r} vs oracle {f_ref!r} (teacher-forced)"
+        if gpu_obj is not None:
+            assert rec["reported_obj_rel_err"] <= obj_rtol, \
+                f"{where}: reported objective {gpu_obj[k]!r} vs oracle {f_ref!r}"
+    log_stats({"check": "teacher_forced", "label": label, "rows": int(W64.shape[0]),
+               "cols": int(W64.shape[1]), "sweeps": stats})
+    return stats
+
+
+def free_running(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs, *, W0=None,
+                 codes0=None, codes_valid0=False, T=None, label="", obj_rtol=OBJ_RTOL,
+                 tie_margin=TIE_MARGIN):
+    """End-to-end comparison: the oracle runs every sweep on its own from the
+    common start.  Asserts what stays unique (first divergences at ties,
+    identical rows agreeing on the objective, split rows descending) and
+    returns the per-sweep code-difference fractions."""
+    W64 = np.asarray(W_rows, np.float64)
+    sweeps = len(codes_hist)
+    ref = oracle.cd(W_rows, S64, bits, scale, zero, sweeps,
+                    W0=None if W0 is None else np.asarray(W0, np.float64),
+                    codes0=None if codes0 is None else np.asarray(codes0, np.int32),
+                    codes_valid=codes_valid0, T=T)
     splits = first_divergence(codes_hist, ref.codes_hist)
     same = np.array([d is None for d in splits])
-    decisions = codes_hist[0].size * len(codes_hist)
-    assert (~same).sum() <= max(2, max_split_rate * decisions), \
-        f"{int((~same).sum())} of {len(same)} rows split over {decisions} decisions"
-    f_prev = None
-    for k in range(len(codes_hist)):
-        f_gpu = np.sum((whats[k].astype(np.float64) - W64) * Rs[k], axis=1)
+    fracs, f_prev = [], None
+    for k in range(sweeps):
+        fracs.append(float(np.mean(np.asarray(codes_hist[k]) != ref.codes_hist[k])))
+        f_gpu = gpu_row_objective(W_rows, whats[k], Rs[k])
         D = ref.what_hist[k] - W64
         f_ref = np.sum((D @ S64) * D, axis=1)
         if same.any():
-            assert np.array_equal(codes_hist[k][same], ref.codes_hist[k][same]), f"sweep {k + 1}"
-            assert np.sum(f_gpu[same]) == pytest_approx(np.sum(f_ref[same]), obj_rtol), \
-                f"sweep {k + 1}: objective over the {int(same.sum())} rows that never split"
+            a, b = float(np.sum(f_gpu[same])), float(np.sum(f_ref[same]))
+            assert abs(a - b) <= obj_rtol * abs(b) + 1e-300, \
+                f"{label} sweep {k + 1}: objective over the {int(same.sum())} rows that never split"
         if f_prev is not None and not same.all():
-            split_rows = ~same
-            assert np.all(f_gpu[split_rows] <= f_prev[split_rows] * (1 + 1e-6) + 1e-9), \
-                f"sweep {k + 1}: a split row's objective went up"
+            assert np.all(f_gpu[~same] <= f_prev[~same] * (1 + 1e-6) + 1e-12), \
+                f"{label} sweep {k + 1}: a split row's objective went up"
         f_prev = f_gpu
     for i, d in enumerate(splits):
         if d is not None:
-            assert ref.margin_hist[d[0]][i, d[1]] <= tie_margin, \
-                f"row {i} splits at sweep {d[0] + 1}, column {d[1]} away from a tie " \
-                f"(margin {ref.margin_hist[d[0]][i, d[1]]:.3e})"
-    return int((~same).sum())
-
-
-def pytest_approx(value, rtol):
-    import pytest
-    return pytest.approx(value, rel=rtol)
+            m = ref.margin_hist[d[0]][i, d[1]]
+            assert m <= tie_margin, \
+                f"{label}: row {i} splits at sweep {d[0] + 1}, column {d[1]} away from a tie " \
+                f"(margin {m:.3e})"
+    rec = {"check": "free_running", "label": label, "rows": int(W64.shape[0]),
+           "cols": int(W64.shape[1]), "split_rows": int((~same).sum()),
+           "split_sweeps": sorted(int(d[0]) + 1 for d in splits if d is not None),
+           "code_diff_frac": fracs}
+    log_stats(rec)
+    return rec

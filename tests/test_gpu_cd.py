@@ -1,17 +1,18 @@
 """GPU parity of qe_cd_sweep (Sec. 3: Lemma 1, the rank-1 identity, blocked)
 against the fp64 oracle, on the same seeded fp32 inputs.
 
-Bar (per sweep, parity.check_row_sampled_sweeps over all rows): rows whose
-codes never differ from the oracle's hold identical codes and agree on the
-objective within 1e-4 relative; a row may split from the oracle only where
-the oracle's t lies within 1e-4 grid units of a rounding boundary (before
-that point both rows hold identical codes, so only rounding separates the
-two t values), after which it must stay a descending CD path; splits are
-rare (at most two per case here).  Without splits the whole objective must
-agree within 1e-4 and at most 0.1% of codes may differ.  Exact cases (weights on the grid, diagonal Sigma, constructed
-ties) must match bit for bit.  The block-update products run on the split
-bf16 matrix cores by default; the main parity cases also run with
-QE_CD_FP32 (fp32 matrix cores)."""
+Bar (tests/parity.py), on every row of each case:
+* teacher-forced, after every sweep: the oracle runs that sweep from the
+  GPU's state after the previous one; at most 0.1% of codes differ, every
+  row's first difference sits at an oracle tie (within 1e-4 grid units of a
+  rounding boundary), and the objective -- the library's reported value and
+  <What - W, R> from the GPU's residual -- agrees within 1e-4 relative;
+* free-running: first divergences only at ties, identical rows agree on the
+  objective, split rows keep descending.
+Exact cases (weights on the grid, diagonal Sigma, constructed ties) must
+match bit for bit.  The block-update products run on the split bf16 matrix
+cores by default; the main parity cases also run with QE_CD_FP32 (fp32
+matrix cores)."""
 import json
 import os
 
@@ -20,14 +21,11 @@ import pytest
 import torch
 
 import synth
-from parity import check_row_sampled_sweeps, dev, host
+from parity import dev, free_running, host, teacher_forced
 
 pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
-OBJ_RTOL = 1e-4
-CODE_FRAC = 1e-3
-TIE_MARGIN = 1e-4
 
 
 def gpu_cd(qe, W, S32, bits, scale, zero, sweeps, block=0, per_sweep=True, W0=None, codes0=None,
@@ -77,24 +75,20 @@ def layer(q, p, n, seed, corr=0.0, bits=4, damp=0.01, spec="c1"):
     return W, X
 
 
-def compare_sweeps(W, S32, g, ref, sweeps):
-    """Split-aware per-sweep comparison of a GPU run (per_sweep=True) with the
-    oracle's run on the same inputs."""
-    splits = check_row_sampled_sweeps(W, S32.astype(np.float64), g["whats"], g["Rs"], g["hist"],
-                                      ref, obj_rtol=OBJ_RTOL, tie_margin=TIE_MARGIN,
-                                      max_split_rate=0.0)
-    if splits == 0:
-        for k in range(sweeps):
-            assert g["obj"][k] == pytest.approx(ref.obj[k], rel=OBJ_RTOL), f"objective, sweep {k + 1}"
-            frac = np.mean(g["hist"][k] != ref.codes_hist[k])
-            assert frac <= CODE_FRAC, f"sweep {k + 1}: {frac:.2e} of codes differ"
-    return splits
+def compare_sweeps(oracle, W, S32, bits, scale, zero, g, label, W0=None, codes0=None,
+                   codes_valid0=False):
+    """Teacher-forced and free-running comparison of a per-sweep GPU run over
+    all rows of the layer."""
+    S64 = S32.astype(np.float64)
+    T = W.astype(np.float64) @ S64
+    kw = dict(W0=W0, codes0=codes0, codes_valid0=codes_valid0, T=T, label=label)
+    teacher_forced(oracle, W, S64, bits, scale, zero, g["hist"], g["whats"], g["Rs"],
+                   gpu_obj=g["obj"], **kw)
+    return free_running(oracle, W, S64, bits, scale, zero, g["hist"], g["whats"], g["Rs"], **kw)
 
 
-def check_parity(oracle, W, S32, bits, scale, zero, g, sweeps):
-    ref = oracle.cd(W, S32.astype(np.float64), bits, scale, zero, sweeps)
-    compare_sweeps(W, S32, g, ref, sweeps)
-    return ref
+def check_parity(oracle, W, S32, bits, scale, zero, g, label):
+    return compare_sweeps(oracle, W, S32, bits, scale, zero, g, label)
 
 
 @pytest.mark.parametrize("fp32", [False, True])
@@ -112,7 +106,7 @@ def test_cd_matches_oracle(qe, oracle, q, p, corr, bits, fp32):
     scale, zero = oracle.grid_minmax(W, bits)
     sweeps = 5
     g = gpu_cd(qe, W, S32, bits, scale, zero, sweeps, extra=qe.QE_CD_FP32 if fp32 else 0)
-    check_parity(oracle, W, S32, bits, scale, zero, g, sweeps)
+    check_parity(oracle, W, S32, bits, scale, zero, g, f"cd {q}x{p} corr={corr} b={bits} fp32={fp32}")
 
 
 @pytest.mark.parametrize("block", [16, 32, 64, 128])
@@ -121,7 +115,7 @@ def test_block_width_invariance(qe, oracle, block):
     S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
     scale, zero = oracle.grid_minmax(W, 4)
     g = gpu_cd(qe, W, S32, 4, scale, zero, 4, block=block)
-    check_parity(oracle, W, S32, 4, scale, zero, g, 4)
+    check_parity(oracle, W, S32, 4, scale, zero, g, f"block {block}")
 
 
 def test_multi_sweep_call_equals_resumed_calls(qe, oracle):
@@ -223,9 +217,8 @@ def test_warm_start_from_arbitrary_what(qe, oracle, q, p, fp32):
     W0 = oracle.dequant(codes0, scale, zero).astype(np.float32)
     g = gpu_cd(qe, W, S32, 4, scale, zero, 3, W0=W0, codes0=codes0,
                extra=qe.QE_CD_FP32 if fp32 else 0)
-    ref = oracle.cd(W, S32.astype(np.float64), 4, scale, zero, 3, W0=W0, codes0=codes0,
-                    codes_valid=True)
-    compare_sweeps(W, S32, g, ref, 3)
+    compare_sweeps(oracle, W, S32, 4, scale, zero, g, f"warm start {q}x{p} fp32={fp32}", W0=W0,
+                   codes0=codes0, codes_valid0=True)
 
 
 def test_zero_diagonal_reports_error(qe):

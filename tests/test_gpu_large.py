@@ -1,65 +1,114 @@
-"""Full-size parity at the 4096 x 4096 attention-projection workload, in the
-launch configuration the benchmark times (block width 128).
+"""Full-size parity on the 4096-channel layers, on the workload's own inputs,
+in the launch configuration the benchmark times (block width 128).
 
-* Gram over the full 4096 x 262144 heavy-tailed X: all diagonal entries and
-  a seeded 128 x 128 grid of entries (outlier channels included) against
-  the oracle's one-by-one dot products; relative Frobenius <= 1e-5.
-* CD sweeps on all 4096 rows; the oracle replays a seeded sample of 64 rows
-  with the same Sigma (rows are independent, Sec. 3.2, so the comparison is
-  exact): identical codes and objective within 1e-4 over the rows whose
-  trajectories never split, every split at a near tie and followed by
-  descent, at most max(2, 1e-6 x decisions) split rows
-  (parity.check_row_sampled_sweeps).  Sigma comes from the oracle's Gram of the
-  first 2048 tokens, damped, so the oracle finishes in seconds."""
+The activations are the attention-projection workload's: 4096 x 262144
+heavy-tailed tokens (128 x 2048, Student-t nu = 4, 1% outlier channels x30).
+The MLP up-projection (11008 x 4096) draws the very same X, so both layers
+share Sigma.
+
+* Gram: the whole 4096 x 4096 Sigma against the oracle's fp64 Gram of all
+  262144 tokens (relative Frobenius <= 1e-5), exactly symmetric.
+* CD on all rows of each layer, Sigma = the oracle's damped Gram of all
+  262144 tokens cast to fp32 (Lemma 1: Sigma = X X^T over the calibration
+  set); the oracle replays seeded row samples (512 rows of the attention
+  projection, 128 of the up-projection; rows are independent, Sec. 3.2, so
+  the sample is exact) teacher-forced after every sweep and free-running
+  (tests/parity.py)."""
 import numpy as np
 import pytest
 import torch
 
 import synth
-from parity import check_row_sampled_sweeps, dev, host
+from parity import dev, free_running, host, rel_fro, teacher_forced
 
 pytestmark = pytest.mark.gpu
 
 SPEC = synth.CONFIGS["c2"]
 
 
-def test_gram_full_size_sampled(qe, oracle):
-    X = synth.activations(SPEC)
-    Xd = dev(X)
+@pytest.fixture(scope="module")
+def c2_x():
+    print(f"[c2] drawing X {SPEC.p}x{SPEC.n}", flush=True)
+    return synth.activations(SPEC)
+
+
+@pytest.fixture(scope="module")
+def c2_sigma64(c2_x, oracle):
+    """The oracle's undamped fp64 Gram of all tokens."""
+    print("[c2] oracle Gram of all tokens (fp64)", flush=True)
+    return oracle.gram_blas(c2_x)
+
+
+@pytest.mark.timeout(900)
+def test_gram_full_size_full_matrix(qe, c2_x, c2_sigma64):
+    Xd = dev(c2_x)
     S = host(qe.gram(Xd))
     del Xd
     torch.cuda.empty_cache()
-    idx = synth.entry_sample(SPEC.p, 128, SPEC.cfg, must=synth.outlier_channels(SPEC)[:16])
-    ia, ib = np.meshgrid(idx, idx, indexing="ij")
-    ia = np.concatenate([ia.reshape(-1), np.arange(SPEC.p)])
-    ib = np.concatenate([ib.reshape(-1), np.arange(SPEC.p)])
-    ref = oracle.gram_entries(X, ia, ib)
-    got = S[ia, ib].astype(np.float64)
-    assert np.linalg.norm(got - ref) / np.linalg.norm(ref) <= 1e-5
     assert np.array_equal(S, S.T)
+    err = rel_fro(S, c2_sigma64)
+    print(f"[c2] Gram relative Frobenius error {err:.3e}", flush=True)
+    assert err <= 1e-5
+    # the diagonal (the CD step's divisors) entry by entry
+    d, dref = np.diag(S).astype(np.float64), np.diag(c2_sigma64)
+    assert np.max(np.abs(d - dref) / dref) <= 1e-5
 
 
-def test_cd_full_size_row_sampled(qe, oracle):
-    q, p, bits, sweeps = SPEC.q, SPEC.p, SPEC.bits, SPEC.sweeps
-    W = synth.weights(SPEC)
-    X = synth.activations(SPEC, n=2048)
-    S32 = oracle.damp(oracle.gram(X), SPEC.damp).astype(np.float32)
-    scale, zero = oracle.grid_minmax(W, bits)
-    rows = synth.row_sample(q, 64, SPEC.cfg)
-
+def cd_rows_on_gpu(qe, W, S32, bits, sweeps, rows, block=128):
+    """All rows on the GPU, one sweep per call from What = W; the sampled
+    rows' codes, What and R after every sweep."""
+    q, p = W.shape
+    scale, zero = qe.grid_minmax(dev(W), bits)
     Wd, Sd = dev(W), dev(S32)
     Wh = torch.empty_like(Wd)
     codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
     R = torch.empty_like(Wd)
     flags = qe.QE_INIT_FROM_W
     hist, whats, Rs = [], [], []
+    rows_d = torch.as_tensor(rows, device="cuda")
     for _ in range(sweeps):
-        qe.cd_sweep(Wd, Sd, bits, dev(scale), dev(zero), Wh, codes, R, 1, block=128, flags=flags)
+        qe.cd_sweep(Wd, Sd, bits, scale, zero, Wh, codes, R, 1, block=block, flags=flags)
         flags = qe.QE_R_VALID | qe.QE_CODES_VALID
-        hist.append(host(codes[rows]).astype(np.int32))
-        whats.append(host(Wh[rows]))
-        Rs.append(host(R[rows]))
+        hist.append(host(codes[rows_d]).astype(np.int32))
+        whats.append(host(Wh[rows_d]))
+        Rs.append(host(R[rows_d]))
+    sc, ze = host(scale), host(zero)
+    del Wd, Sd, Wh, codes, R
+    torch.cuda.empty_cache()
+    return sc, ze, hist, whats, Rs
 
-    S64 = S32.astype(np.float64)
-    ref = oracle.cd(W[rows], S64, bits, scale[rows], zero[rows], sweeps)
-    check_row_sampled_sweeps(W[rows], S64, whats, Rs, hist, ref)
+
+def row_sampled_parity(qe, oracle, spec, W, S64, rows, label):
+    S32 = oracle.damp(S64, spec.damp).astype(np.float32)
+    sc, ze, hist, whats, Rs = cd_rows_on_gpu(qe, W, S32, spec.bits, spec.sweeps, rows)
+    # the grid is an exact fp32 decision on both sides
+    scale, zero = oracle.grid_minmax(W, spec.bits)
+    assert np.array_equal(sc, scale) and np.array_equal(ze, zero)
+    Sc = S32.astype(np.float64)
+    T = W[rows].astype(np.float64) @ Sc
+    print(f"[{label}] teacher-forced oracle over {len(rows)} rows x {spec.sweeps} sweeps",
+          flush=True)
+    tf = teacher_forced(oracle, W[rows], Sc, spec.bits, scale[rows], zero[rows], hist, whats, Rs,
+                        T=T, label=label)
+    print(f"[{label}] free-running oracle", flush=True)
+    fr = free_running(oracle, W[rows], Sc, spec.bits, scale[rows], zero[rows], hist, whats, Rs,
+                      T=T, label=label)
+    print(f"[{label}] teacher-forced code differences per sweep "
+          f"{[r['code_diff_frac'] for r in tf]}; free-running {fr['code_diff_frac']} "
+          f"({fr['split_rows']} split rows)", flush=True)
+
+
+@pytest.mark.timeout(900)
+def test_cd_full_size_own_sigma(qe, oracle, c2_sigma64):
+    W = synth.weights(SPEC)
+    rows = synth.row_sample(SPEC.q, 512, SPEC.cfg)
+    row_sampled_parity(qe, oracle, SPEC, W, c2_sigma64, rows, "c2 own Sigma")
+
+
+@pytest.mark.timeout(900)
+def test_c3_up_projection_own_sigma(qe, oracle, c2_sigma64):
+    spec = synth.CONFIGS["c3up"]
+    assert spec.x_cfg == SPEC.cfg and spec.p == SPEC.p       # the same activations
+    W = synth.weights(spec)
+    rows = synth.row_sample(spec.q, 128, spec.cfg)
+    row_sampled_parity(qe, oracle, spec, W, c2_sigma64, rows, "c3-up own Sigma")

@@ -26,6 +26,17 @@ def test_gram_matches_blas_product(oracle, layout):
     assert np.array_equal(S, S.T)
 
 
+@pytest.mark.parametrize("layout", [0, 1])
+def test_gram_blas_equals_plain_loops(oracle, layout):
+    X = synth.gaussian((45, 1000), seed=11)
+    Xin = X if layout == 0 else np.ascontiguousarray(X.T)
+    S = oracle.gram_blas(Xin, layout, chunk=96, row_block=16)   # ragged last chunk and block
+    assert np.allclose(S, oracle.gram(Xin, layout), rtol=1e-13, atol=1e-11)
+    S2 = oracle.gram_blas(Xin[:, :300] if layout == 0 else Xin[:300], layout)
+    oracle.gram_blas(Xin[:, 300:] if layout == 0 else Xin[300:], layout, out=S2)
+    assert np.allclose(S2, S, rtol=1e-13, atol=1e-11)
+
+
 def test_gram_closed_forms(oracle):
     # rows of a Sylvester-Hadamard matrix are orthogonal: X X^T = n I
     H = np.array([[1.0]])
