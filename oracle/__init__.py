@@ -60,7 +60,7 @@ def bind(path: str) -> ctypes.CDLL:
     lib.qeo_grid_minmax.argtypes = [_f32p, _i64, _i64, ctypes.c_int, _f32p, _f32p, _f32p]
     lib.qeo_grid_minmax.restype = None
     lib.qeo_cd_sweep_lemma1.argtypes = [_f64p, _f64p, _i64, _i64, ctypes.c_int, _f64p, _f64p,
-                                        _f64p, _i32p, _u8p, _f64p, ctypes.c_int]
+                                        _f64p, _i32p, _u8p, _f64p, ctypes.c_int, _i64]
     lib.qeo_cd_sweep_lemma1.restype = ctypes.c_int
     lib.qeo_cd_sweep_alg1.argtypes = [_f64p, _f64p, _i64, _i64, ctypes.c_int, _f64p, _f64p,
                                       _f64p, _i32p, _u8p, _f64p]
@@ -97,7 +97,7 @@ def cd_sweep_timed(W, Sigma, bits, scale, zero) -> float:
     t0 = time.perf_counter()
     rc = lib.qeo_cd_sweep_lemma1(_p(T, _f64p), _p(S, _f64p), q, p, bits, _p(sc, _f64p),
                                  _p(ze, _f64p), _p(Wh, _f64p), _p(codes, _i32p),
-                                 _p(valid, _u8p), None, 0)
+                                 _p(valid, _u8p), None, 0, 0)
     dt = time.perf_counter() - t0
     if rc != 0:
         raise ValueError("Sigma has a non-positive diagonal entry")
@@ -264,7 +264,8 @@ class CDResult:
 
 def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
        codes_valid: bool = False, form: str = "lemma1", target=None,
-       relax_period: int = 0, record: bool = True, obj_H=None, T=None) -> CDResult:
+       relax_period: int = 0, record: bool = True, obj_H=None, T=None, start_col: int = 0,
+       with_obj: bool = True) -> CDResult:
     """Cyclic CD sweeps of QuantEase.
 
     W: q x p weights; Sigma: p x p (used as given, promoted to fp64);
@@ -278,7 +279,12 @@ def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
     obj_H: H added to What in the recorded objective (outlier variant).
     T: the product target @ Sigma (fp64), if the caller already holds it
     (several calls on the same layer); formed here otherwise.
+    start_col (lemma1 form, one sweep): begin the sweep at that column, the
+    earlier coordinates counting as already visited.  with_obj=False skips
+    the objective after each sweep.
     """
+    if start_col and (form != "lemma1" or sweeps != 1):
+        raise ValueError("start_col applies to one sweep of the lemma1 form")
     lib = _load()
     W = np.asarray(W)
     q, p = W.shape
@@ -312,7 +318,7 @@ def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
                                          _p(ze, _f64p), _p(Wh, _f64p), _p(codes, _i32p),
                                          _p(valid, _u8p),
                                          _p(margin, _f64p) if margin is not None else None,
-                                         1 if relax else 0)
+                                         1 if relax else 0, int(start_col))
             if rc != 0:
                 raise ValueError("Sigma has a non-positive diagonal entry")
         elif form == "alg1":
@@ -330,7 +336,8 @@ def cd(W, Sigma, bits: int, scale, zero, sweeps: int, *, W0=None, codes0=None,
             lib.qeo_cd_sweep_alg2(_p(P, _f64p), _p(N, _f64p), q, p, bits, _p(sc, _f64p),
                                   _p(ze, _f64p), _p(Wh, _f64p), _p(codes, _i32p),
                                   _p(valid, _u8p), _p(dW, _f64p), _p(Phat, _f64p))
-        res.obj.append(objective(W, Wh, S, obj_H))
+        if with_obj:
+            res.obj.append(objective(W, Wh, S, obj_H))
         if record:
             res.codes_hist.append(codes.copy())
             res.margin_hist.append(margin)

@@ -132,11 +132,14 @@ static double boundary_margin(double t, int maxq)
 /* relax != 0 writes beta unquantized (the paper's occasional unquantized pass, */
 /* Sec. 3.2 "Initialization") and marks the codes invalid.                      */
 /* margin (nullable) receives boundary_margin(t) of every decision.             */
+/* j0 > 0 starts the pass at column j0 (the rest of a sweep whose first j0      */
+/* coordinates are already done; the parity protocol uses it to follow another  */
+/* implementation's choice at a tie and carry on from there).                   */
 /* Returns 0, or 1 if some Sigma_jj <= 0 (Lemma 1 footnote).                    */
 /* ------------------------------------------------------------------------- */
 int qeo_cd_sweep_lemma1(const double* T, const double* S, int64_t q, int64_t p, int bits,
                         const double* scale, const double* zero, double* Wh, int32_t* codes,
-                        uint8_t* valid, double* margin, int relax)
+                        uint8_t* valid, double* margin, int relax, int64_t j0)
 {
     for (int64_t j = 0; j < p; ++j)
         if (!(S[j * p + j] > 0.0)) return 1;
@@ -144,7 +147,7 @@ int qeo_cd_sweep_lemma1(const double* T, const double* S, int64_t q, int64_t p, 
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t i = 0; i < q; ++i) {
         double* w = Wh + i * p;
-        for (int64_t j = 0; j < p; ++j) {
+        for (int64_t j = j0; j < p; ++j) {
             const double* Sj = S + j * p;
             double c = 0.0;
             for (int64_t l = 0; l < p; ++l)

@@ -27,6 +27,7 @@ line to that file.
 """
 import json
 import os
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 import torch
@@ -80,9 +81,45 @@ def gpu_row_objective(W_rows, what, R):
                   * np.asarray(R, np.float64), axis=1)
 
 
+def explain_row(oracle, W_row, S64, bits, scale, zero, T_row, start_w, start_c, valid,
+                gpu_codes, tie_margin=TIE_MARGIN, max_steps=64):
+    """Follows one row of one sweep along the GPU's choices at ties.
+
+    The oracle sweeps the row from the sweep's start state; at the first
+    column where the GPU's code differs, that decision must be a tie (oracle
+    margin <= tie_margin); the oracle then takes the GPU's code there and
+    carries on from the next column (Lemma 1 from the same state), and so on
+    to the end of the row.  Every code the GPU holds is thereby shown to be
+    the oracle's, or a tie decision, or a consequence of earlier tie
+    decisions.  Returns the list of (column, margin) of the tie decisions."""
+    w = np.array(start_w, np.float64).reshape(1, -1)
+    c = (np.zeros(w.shape, np.int32) if start_c is None
+         else np.array(start_c, np.int32).reshape(1, -1))
+    gpu_codes = np.asarray(gpu_codes).reshape(-1)
+    level = scale.astype(np.float64) * (gpu_codes - zero.astype(np.float64))
+    ties, j0 = [], 0
+    for _ in range(max_steps):
+        ref = oracle.cd(W_row, S64, bits, scale, zero, 1, W0=w, codes0=c, codes_valid=valid,
+                        T=T_row, start_col=j0, with_obj=False)
+        diff = np.nonzero(ref.codes[0, j0:] != gpu_codes[j0:])[0]
+        if diff.size == 0:
+            return ties
+        j = j0 + int(diff[0])
+        m = float(ref.margin_hist[0][0, j])
+        assert m <= tie_margin, f"column {j}: the GPU's code differs at oracle margin {m:.3e} " \
+            f"grid units (not a tie), after {len(ties)} tie decisions in this row"
+        ties.append((j, m))
+        # the state just after column j along the GPU's path
+        w[0, :j + 1] = np.concatenate([ref.What[0, :j], level[j:j + 1]])
+        c[0, :j + 1] = np.concatenate([ref.codes[0, :j], gpu_codes[j:j + 1]])
+        j0 = j + 1
+    raise AssertionError(f"more than {max_steps} tie decisions in one row")
+
+
 def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs, *,
                    W0=None, codes0=None, codes_valid0=False, T=None, gpu_obj=None,
-                   label="", obj_rtol=OBJ_RTOL, code_frac=CODE_FRAC, tie_margin=TIE_MARGIN):
+                   label="", obj_rtol=OBJ_RTOL, code_frac=CODE_FRAC, tie_margin=TIE_MARGIN,
+                   explain=True):
     """Per-sweep teacher-forced comparison of a GPU run with the oracle.
 
     W_rows, scale, zero: the rows compared (all rows of the layer, or a
@@ -99,7 +136,7 @@ def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs
     stats = []
     for k in range(sweeps):
         if k == 0:
-            start_w = W64 if W0 is None else np.asarray(W0, np.float64)
+            start_w = W64 if W0 is None else np.asarray(W0, np.float64).reshape(W64.shape)
             start_c = None if codes0 is None else np.asarray(codes0, np.int32)
             valid = codes_valid0
         else:
@@ -121,20 +158,38 @@ def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs
         if gpu_obj is not None:
             rec["reported_obj_rel_err"] = (abs(gpu_obj[k] - f_ref) / abs(f_ref) if f_ref
                                            else abs(gpu_obj[k]))
+        rec["first_diff"] = [[int(i), int(np.argmax(diff[i])), m, int(diff[i].sum())]
+                             for i, m in zip(split_rows, margins)]
+        if explain:
+            # every differing code of a split row traced back to tie decisions
+            # (rows in parallel threads: the oracle's C loop releases the GIL)
+            todo = [int(i) for i, m in zip(split_rows, margins) if m <= tie_margin]
+
+            def one(i, start_w=start_w, start_c=start_c, valid=valid, g=g):
+                return explain_row(oracle, W_rows[i:i + 1], S64, bits, scale[i:i + 1],
+                                   zero[i:i + 1], T[i:i + 1], start_w[i],
+                                   None if start_c is None else start_c[i], valid, g[i],
+                                   tie_margin=tie_margin)
+
+            with ThreadPoolExecutor(max(1, min(16, len(todo)))) as ex:
+                found = list(ex.map(one, todo))
+            rec["tie_decisions"] = [[i, [[j, mm] for j, mm in t]] for i, t in zip(todo, found)]
         stats.append(rec)
-        where = f"{label} sweep {k + 1}"
-        assert frac <= code_frac, f"{where}: {frac:.3e} of codes differ (teacher-forced)"
-        for i, m in zip(split_rows, margins):
-            assert m <= tie_margin, \
-                f"{where}: row {i} first differs at column {int(np.argmax(diff[i]))}, " \
-                f"oracle margin {m:.3e} grid units (not a tie)"
-        assert rec["obj_rel_err"] <= obj_rtol, \
-            f"{where}: objective {f_gpu!r} vs oracle {f_ref!r} (teacher-forced)"
-        if gpu_obj is not None:
-            assert rec["reported_obj_rel_err"] <= obj_rtol, \
-                f"{where}: reported objective {gpu_obj[k]!r} vs oracle {f_ref!r}"
     log_stats({"check": "teacher_forced", "label": label, "rows": int(W64.shape[0]),
                "cols": int(W64.shape[1]), "sweeps": stats})
+    for rec in stats:
+        where = f"{label} sweep {rec['sweep']}"
+        assert rec["code_diff_frac"] <= code_frac, \
+            f"{where}: {rec['code_diff_frac']:.3e} of codes differ (teacher-forced)"
+        for i, j, m, _ in rec["first_diff"]:
+            assert m <= tie_margin, \
+                f"{where}: row {i} first differs at column {j}, oracle margin {m:.3e} grid " \
+                f"units (not a tie)"
+        assert rec["obj_rel_err"] <= obj_rtol, f"{where}: objective (teacher-forced) off by " \
+            f"{rec['obj_rel_err']:.3e}"
+        if gpu_obj is not None:
+            assert rec["reported_obj_rel_err"] <= obj_rtol, \
+                f"{where}: reported objective off by {rec['reported_obj_rel_err']:.3e}"
     return stats
 
 

@@ -16,12 +16,16 @@ layers on their own Sigma are in test_gpu_large.py).
 * c5 (14848 x 59392, 4-bit, 5 sweeps): the Gram over 262144 device-drawn
   tokens streamed in 8192-token chunks, on every diagonal entry and a seeded
   256 x 256 block, against the oracle's fp64 sums of the same numbers; CD
-  on all rows against a seeded 64-row sample, teacher-forced.
+  on all rows against a seeded 64-row sample, teacher-forced and
+  free-running, on a Sigma with the workload's coupling; and a stress case on
+  a rank-deficient Sigma (see the two tests).
 
 The CD inputs at c3-down, c4 and c5 use a Sigma the oracle forms from a
 token prefix (2048 tokens; 256 at c5, whose fp64 Gram of all tokens would
-take the host the better part of an hour), so no GPU output feeds the
-oracle."""
+take the host about half an hour), so no GPU output feeds the oracle.  With
+fewer tokens than channels these Sigmas are more strongly coupled than the
+workloads' own (off-diagonal entries about n^-1/2 of the diagonal), which
+makes them the harder parity inputs."""
 import numpy as np
 import pytest
 import torch
@@ -37,7 +41,8 @@ def host_sigma(oracle, spec, tokens):
     return oracle.damp(oracle.gram_blas(X), spec.damp)
 
 
-def cd_row_sampled(qe, oracle, W, S32, bits, sweeps, rows, label, block=128, free=True):
+def cd_row_sampled(qe, oracle, W, S32, bits, sweeps, rows, label, block=128, free=True,
+                   code_frac=1e-3):
     """All rows on the GPU, the sampled rows in the oracle, both on the same
     fp32 Sigma and the same grid; teacher-forced (and free-running) checks."""
     q, p = W.shape
@@ -63,7 +68,7 @@ def cd_row_sampled(qe, oracle, W, S32, bits, sweeps, rows, label, block=128, fre
     T = W[rows].astype(np.float64) @ S64
     print(f"[{label}] teacher-forced oracle over {len(rows)} rows", flush=True)
     teacher_forced(oracle, W[rows], S64, bits, scale[rows], zero[rows], hist, whats, Rs, T=T,
-                   label=label)
+                   label=label, code_frac=code_frac)
     if free:
         print(f"[{label}] free-running oracle", flush=True)
         free_running(oracle, W[rows], S64, bits, scale[rows], zero[rows], hist, whats, Rs, T=T,
@@ -223,18 +228,51 @@ def test_c5_gram_full_size_streamed_sampled(qe, oracle):
     assert np.max(np.abs(diag - ref_diag) / ref_diag) <= 1e-5
 
 
+C5_PREFIX = 256          # tokens of the c5 CD parity Sigma
+
+
+def c5_prefix_gram(oracle, spec):
+    X = synth.activation_chunk(spec, 0, tokens=C5_PREFIX)
+    print(f"[c5] oracle Gram of a {C5_PREFIX}-token prefix", flush=True)
+    return oracle.gram_blas(X, row_block=4096)
+
+
 @pytest.mark.timeout(1200)
 def test_c5_cd_row_sampled(qe, oracle):
+    """c5 CD with the workload's coupling.  The fp64 Gram of all 262144
+    tokens at p = 59392 would take the host about half an hour, so Sigma comes
+    from a 256-token prefix; alone, that Gram has rank 256 and off-diagonal
+    entries 1/16 of the diagonal (the workload's: 1/512 = n^-1/2, full rank,
+    condition number about 8).  Damping by sqrt(262144 / 256) - 1 = 31 times
+    the mean diagonal restores the workload's ratio of off-diagonal to
+    diagonal entries and a condition number of about 10; the full bar
+    applies."""
     spec = synth.CONFIGS["c5"]
     W = synth.weights(spec)
-    X = synth.activation_chunk(spec, 0, tokens=256)
-    print("[c5] oracle Sigma of a 256-token prefix", flush=True)
-    S64 = oracle.gram_blas(X, row_block=4096)
-    del X
-    S32 = oracle.damp(S64, spec.damp).astype(np.float32)
+    S64 = c5_prefix_gram(oracle, spec)
+    S32 = oracle.damp(S64, np.sqrt(spec.n / C5_PREFIX) - 1.0).astype(np.float32)
     del S64
     cd_row_sampled(qe, oracle, W, S32, spec.bits, spec.sweeps,
-                   synth.row_sample(spec.q, 64, spec.cfg), "c5", free=False)
+                   synth.row_sample(spec.q, 64, spec.cfg), "c5")
+
+
+@pytest.mark.timeout(1200)
+def test_c5_cd_stress_rank_deficient_sigma(qe, oracle):
+    """Stress case: the 256-token prefix Gram with the workload's 0.01
+    damping -- rank 256 of 59392, condition number about 26000, 32 times the
+    workload's coupling.  A tie decision then moves a long stretch of the
+    rest of its row (measured: about 10000 of 59392 codes), so the 0.1% cap,
+    which presumes rare ties with short consequences, does not describe this
+    input.  What is unique is checked instead: every code in which the GPU
+    differs from the teacher-forced oracle is a tie decision or follows from
+    earlier tie decisions of its row (parity.explain_row), and the objective
+    agrees within 1e-4 after every sweep."""
+    spec = synth.CONFIGS["c5"]
+    W = synth.weights(spec)
+    S32 = oracle.damp(c5_prefix_gram(oracle, spec), spec.damp).astype(np.float32)
+    cd_row_sampled(qe, oracle, W, S32, spec.bits, spec.sweeps,
+                   synth.row_sample(spec.q, 64, spec.cfg), "c5 stress", free=False,
+                   code_frac=1.0)
 
 
 @pytest.mark.timeout(900)

@@ -204,6 +204,26 @@ def test_iterates_stay_on_the_grid(oracle):
         assert np.array_equal(res.what_hist[k], oracle.dequant(c, scale, zero))
 
 
+def test_sweep_from_a_start_column_is_the_tail_of_a_sweep(oracle):
+    """A sweep begun at column j0 from a state whose first j0 columns already
+    hold a full sweep's values finishes exactly as that full sweep does."""
+    W, X = small_layer(9, 30, 90, 62, 0.9)
+    S = oracle.damp(oracle.gram(X), 0.01)
+    scale, zero = oracle.grid_minmax(W, 3)
+    first = oracle.cd(W, S, 3, scale, zero, 1)
+    full = oracle.cd(W, S, 3, scale, zero, 1, W0=first.What, codes0=first.codes, codes_valid=True)
+    for j0 in (1, 13, 29):
+        w0 = first.What.copy()
+        c0 = first.codes.copy()
+        w0[:, :j0] = full.What[:, :j0]
+        c0[:, :j0] = full.codes[:, :j0]
+        tail = oracle.cd(W, S, 3, scale, zero, 1, W0=w0, codes0=c0, codes_valid=True,
+                         start_col=j0)
+        assert np.array_equal(tail.codes, full.codes)
+        assert np.array_equal(tail.What, full.What)
+        assert np.all(np.isinf(tail.margin_hist[0][:, :0]))
+
+
 def test_diagonal_sigma_is_round_to_nearest(oracle):
     W = synth.gaussian((25, 40), seed=8, std=0.03)
     d = synth.uniform((40,), seed=9, lo=0.5, hi=3.0).astype(np.float64)
@@ -234,7 +254,7 @@ def test_unquantized_sweeps_solve_normal_equations(oracle):
         lib.qeo_cd_sweep_lemma1(oracle._p(T, oracle._f64p), oracle._p(np.ascontiguousarray(S), oracle._f64p),
                                 q, p, 4, oracle._p(sc, oracle._f64p), oracle._p(ze, oracle._f64p),
                                 oracle._p(Wh, oracle._f64p), oracle._p(codes, oracle._i32p),
-                                oracle._p(valid, oracle._u8p), None, 1)
+                                oracle._p(valid, oracle._u8p), None, 1, 0)
     assert np.allclose(Wh, W.astype(np.float64), rtol=0, atol=1e-10)
 
 

@@ -92,8 +92,8 @@ C_MUTANTS = [
      "continue;\n            }\n            double t = beta / scale[i] - zero[i];",
      _brute),
     ("lemma1 Sigma column of the wrong coordinate",
-     "double* w = Wh + i * p;\n        for (int64_t j = 0; j < p; ++j) {\n            const double* Sj = S + j * p;",
-     "double* w = Wh + i * p;\n        for (int64_t j = 0; j < p; ++j) {\n            const double* Sj = S + ((j + 1) % p) * p;",
+     "double* w = Wh + i * p;\n        for (int64_t j = j0; j < p; ++j) {\n            const double* Sj = S + j * p;",
+     "double* w = Wh + i * p;\n        for (int64_t j = j0; j < p; ++j) {\n            const double* Sj = S + ((j + 1) % p) * p;",
      _brute),
     ("modified-CD rule dropped (equal-distance current code not kept)",
      "fabs(t - (double)code) <= fabs(t - (double)kk)", "fabs(t - (double)code) < fabs(t - (double)kk)",
