@@ -45,6 +45,7 @@ typedef int qe_status;
 #define QE_ERR_WORKSPACE   4  /* workspace null or smaller than the size query */
 #define QE_ERR_HIP         5  /* a HIP runtime call failed */
 #define QE_ERR_UNSUPPORTED 6  /* a valid request this library does not implement */
+#define QE_ERR_TOO_LARGE   7  /* qe_cd_sweep_noalloc: the sizes need more than its fixed scratch */
 
 /* Layouts of X for qe_gram, optionally or-ed with QE_GRAM_FP32. */
 #define QE_LAYOUT_PN 0        /* X is p x n: each channel's n tokens contiguous */
@@ -145,6 +146,32 @@ qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, 
                       const float* scale, const float* zero, float* W_hat, uint8_t* codes,
                       float* R, int sweeps, int block, uint32_t flags, double* obj,
                       void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------
+ * qe_cd_sweep without allocation or workspace, for callers that cannot
+ * allocate device memory: code under stream/graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc.  Arguments and results as for
+ * qe_cd_sweep, except:
+ *  - the scratch (the status word, 1/Sigma_jj, 1/scale, the two delta
+ *    buffers of q x max(256, block) floats, fp64 partial sums) lives in a
+ *    library-owned device array of QE_NOALLOC_SCRATCH_BYTES per GPU, held
+ *    until the process ends; the call needs qe_cd_workspace_size(q, p, block)
+ *    bytes of it and returns QE_ERR_TOO_LARGE, with nothing enqueued, when
+ *    that is more (q up to about 30000 rows at the default block);
+ *  - status: NULL, or a device int that receives, in stream order at the
+ *    end of the call, the call's data-error status (QE_OK, QE_ERR_DIAG,
+ *    QE_ERR_SCALE), as qe_sync_status would report it;
+ *  - every call on one GPU uses that GPU's one scratch array: calls that
+ *    overlap on one GPU (different streams, host threads) race and must be
+ *    serialised by the caller.  Each call clears what it needs cleared.
+ * No hipMalloc, hipFree or allocating routine is called; the scratch's
+ * device address is looked up once per GPU, on the first call there.
+ * ------------------------------------------------------------------------ */
+#define QE_NOALLOC_SCRATCH_BYTES (64u << 20)
+qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
+                              const float* scale, const float* zero, float* W_hat,
+                              uint8_t* codes, float* R, int sweeps, int block, uint32_t flags,
+                              double* obj, int* status, void* stream);
 
 /* ------------------------------------------------------------------------
  * Outlier-aware QuantEase (Sec. 4, Algorithm "Outlier-Aware QuantEase").

@@ -1,6 +1,7 @@
 // C ABI of libqe: argument validation, workspace checks and launch sequencing.
 // Every argument error is detected on the host before anything is enqueued.
 #include <cmath>
+#include <mutex>
 
 #include "qe_internal.h"
 
@@ -31,6 +32,56 @@ qe_status clear_status(void* ws, hipStream_t s)
     return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
 }
 
+qe_status cd_arg_error(const float* W, const float* Sigma, const float* scale, const float* zero,
+                       const float* W_hat, const uint8_t* codes, const float* R, int64_t q,
+                       int64_t p, int bits, int sweeps, int block, uint32_t flags)
+{
+    if (!W || !Sigma || !scale || !zero || !W_hat || !codes || !R) return QE_ERR_ARG;
+    if (bad_dims(q, p) || bad_bits(bits) || bad_block(block) || sweeps < 0) return QE_ERR_ARG;
+    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_MASK | QE_CD_FP32))
+        return QE_ERR_ARG;
+    return QE_OK;
+}
+
+// ---- scratch of qe_cd_sweep_noalloc
+// One copy per GPU, held until the process ends.  In host code `scratch` only
+// names the symbol; its device address comes from hipGetSymbolAddress, taken
+// once per device with that device current.
+static __device__ __align__(256) unsigned char scratch[QE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+qe_status scratch_on_stream(hipStream_t s, void** out)
+{
+    int dev = 0;
+    if (s) {
+        if (hipStreamGetDevice(s, &dev) != hipSuccess) return QE_ERR_HIP;
+    } else if (hipGetDevice(&dev) != hipSuccess) {
+        return QE_ERR_HIP;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return QE_ERR_UNSUPPORTED;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        int cur = 0;
+        if (hipGetDevice(&cur) != hipSuccess) return QE_ERR_HIP;
+        if (cur != dev && hipSetDevice(dev) != hipSuccess) return QE_ERR_HIP;
+        void* ptr = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+        if (cur != dev && hipSetDevice(cur) != hipSuccess) return QE_ERR_HIP;
+        if (e != hipSuccess || !ptr) return QE_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return QE_OK;
+}
+
+__global__ void status_copy_kernel(const int* from, int* to)
+{
+    if (threadIdx.x == 0) *to = *from;
+}
+
 }  // namespace
 
 extern "C" {
@@ -45,6 +96,7 @@ const char* qe_status_string(qe_status s)
         case QE_ERR_WORKSPACE: return "workspace missing or too small";
         case QE_ERR_HIP: return "HIP runtime error";
         case QE_ERR_UNSUPPORTED: return "unsupported request";
+        case QE_ERR_TOO_LARGE: return "request needs more than the fixed scratch of qe_cd_sweep_noalloc";
         default: return "unknown status";
     }
 }
@@ -104,15 +156,40 @@ qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, 
                       float* R, int sweeps, int block, uint32_t flags, double* obj, void* ws,
                       size_t ws_bytes, void* stream)
 {
-    if (!W || !Sigma || !scale || !zero || !W_hat || !codes || !R) return QE_ERR_ARG;
-    if (bad_dims(q, p) || bad_bits(bits) || bad_block(block) || sweeps < 0) return QE_ERR_ARG;
-    if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_MASK | QE_CD_FP32))
-        return QE_ERR_ARG;
+    const qe_status bad = cd_arg_error(W, Sigma, scale, zero, W_hat, codes, R, q, p, bits, sweeps,
+                                       block, flags);
+    if (bad != QE_OK) return bad;
     if (!ws || ws_bytes < cd_ws_bytes(q, p, block)) return QE_ERR_WORKSPACE;
     hipStream_t s = as_stream(stream);
     if (clear_status(ws, s) != QE_OK) return QE_ERR_HIP;
     return launch_cd(W, Sigma, q, p, bits, scale, zero, W_hat, codes, R, nullptr, sweeps, block,
                      flags, obj, 1, ws, s);
+}
+
+qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
+                              const float* scale, const float* zero, float* W_hat,
+                              uint8_t* codes, float* R, int sweeps, int block, uint32_t flags,
+                              double* obj, int* status, void* stream)
+{
+    const qe_status bad = cd_arg_error(W, Sigma, scale, zero, W_hat, codes, R, q, p, bits, sweeps,
+                                       block, flags);
+    if (bad != QE_OK) return bad;
+    if (cd_ws_bytes(q, p, block) > QE_NOALLOC_SCRATCH_BYTES) return QE_ERR_TOO_LARGE;
+    hipStream_t s = as_stream(stream);
+    void* ws = nullptr;
+    qe_status st = scratch_on_stream(s, &ws);
+    if (st != QE_OK) return st;
+    // the previous call's status word is still there
+    if (clear_status(ws, s) != QE_OK) return QE_ERR_HIP;
+    st = launch_cd(W, Sigma, q, p, bits, scale, zero, W_hat, codes, R, nullptr, sweeps, block,
+                   flags, obj, 1, ws, s);
+    if (st != QE_OK) return st;
+    if (status) {
+        hipLaunchKernelGGL(status_copy_kernel, dim3(1), dim3(64), 0, s,
+                           static_cast<const int*>(ws), status);
+        if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+    }
+    return QE_OK;
 }
 
 // ------------------------------------------------------------------ outlier-aware CD

@@ -23,6 +23,8 @@ QE_ERR_SCALE = 3
 QE_ERR_WORKSPACE = 4
 QE_ERR_HIP = 5
 QE_ERR_UNSUPPORTED = 6
+QE_ERR_TOO_LARGE = 7
+QE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 QE_LAYOUT_PN = 0
 QE_LAYOUT_NP = 1
@@ -57,6 +59,8 @@ SIGNATURES = {
     "qe_cd_workspace_size": (_sz, [_i64, _i64, _int]),
     "qe_cd_sweep": (_int, [_vp, _vp, _i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _int, _int,
                            ctypes.c_uint32, _vp, _vp, _sz, _vp]),
+    "qe_cd_sweep_noalloc": (_int, [_vp, _vp, _i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _int,
+                                   _int, ctypes.c_uint32, _vp, _vp, _vp]),
     "qe_outlier_workspace_size": (_sz, [_i64, _i64, _int, _i64]),
     "qe_cd_outlier_sweep": (_int, [_vp, _vp, _i64, _i64, _int, _vp, _vp, _vp, _vp, _vp, _vp,
                                    _i64, _f32, _vp, _vp, _int, _int, ctypes.c_uint32, _vp, _vp,
@@ -203,6 +207,28 @@ def cd_sweep(W, Sigma, bits, scale, zero, W_hat, codes, R, sweeps, block: int = 
                            _ptr(obj, torch.float64, "obj") if obj is not None else _vp(None),
                            _vp(ws.data_ptr()), ws.numel(), _stream(stream)), "qe_cd_sweep")
     _finish(ws, check, "qe_cd_sweep", stream)
+    return W_hat, codes, R
+
+
+def cd_sweep_noalloc(W, Sigma, bits, scale, zero, W_hat, codes, R, sweeps, block: int = 0,
+                     flags: int = QE_INIT_FROM_W, obj: Optional[torch.Tensor] = None,
+                     status: Optional[torch.Tensor] = None, stream=None):
+    """qe_cd_sweep_noalloc: as cd_sweep, with the library's fixed scratch in
+    place of a workspace (nothing is allocated).  status: None or an int32
+    device tensor of one element receiving the call's data-error status in
+    stream order.  Calls that overlap on one GPU race (one shared scratch)."""
+    lib = load()
+    q, p = W.shape
+    if obj is not None and (obj.dtype != torch.float64 or obj.numel() < sweeps):
+        raise ValueError("obj must be a float64 device tensor with >= sweeps entries")
+    _check(lib.qe_cd_sweep_noalloc(
+        _ptr(W, torch.float32, "W"), _ptr(Sigma, torch.float32, "Sigma", p * p), q, p, bits,
+        _ptr(scale, torch.float32, "scale", q), _ptr(zero, torch.float32, "zero", q),
+        _ptr(W_hat, torch.float32, "W_hat", q * p), _ptr(codes, torch.uint8, "codes", q * p),
+        _ptr(R, torch.float32, "R", q * p), sweeps, block, flags,
+        _ptr(obj, torch.float64, "obj") if obj is not None else _vp(None),
+        _ptr(status, torch.int32, "status", 1) if status is not None else _vp(None),
+        _stream(stream)), "qe_cd_sweep_noalloc")
     return W_hat, codes, R
 
 

@@ -61,9 +61,9 @@ def test_status_strings_and_version(lib):
     L, _ = lib
     L.qe_status_string.restype = ctypes.c_char_p
     L.qe_status_string.argtypes = [ctypes.c_int]
-    texts = [L.qe_status_string(c).decode() for c in range(7)]
+    texts = [L.qe_status_string(c).decode() for c in range(8)]
     assert texts[0] == "ok"
-    assert len(set(texts)) == 7 and all(texts)
+    assert len(set(texts)) == 8 and all(texts)
     assert L.qe_status_string(99).decode() == "unknown status"
     assert L.qe_version() == 1
 
@@ -171,6 +171,31 @@ def test_cd_sweep_argument_errors(lib):
     assert _cd(L, flags=0x10) == QE_ERR_ARG       # QE_OUTLIER_COLUMNS belongs to the outlier call
     assert _cd(L, ws=NULL) == QE_ERR_WORKSPACE
     assert _cd(L, ws_bytes=1024) == QE_ERR_WORKSPACE
+
+
+def test_cd_sweep_noalloc_argument_errors(lib):
+    """The allocation-free variant checks its arguments like qe_cd_sweep and
+    rejects sizes whose scratch exceeds the fixed array (64 MiB) before any
+    HIP call."""
+    L, _ = lib
+    f = L.qe_cd_sweep_noalloc
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p]
+
+    def call(W=DUMMY, q=64, p=64, bits=4, block=0):
+        return f(W, DUMMY, q, p, bits, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 1, block, 0, NULL, NULL,
+                 NULL)
+    assert call(W=NULL) == QE_ERR_ARG
+    assert call(bits=9) == QE_ERR_ARG
+    assert call(block=48) == QE_ERR_ARG
+    L.qe_cd_workspace_size.restype = ctypes.c_size_t
+    L.qe_cd_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
+    assert L.qe_cd_workspace_size(40000, 4096, 0) > (64 << 20)
+    assert call(q=40000, p=4096) == 7                  # QE_ERR_TOO_LARGE
+    assert L.qe_cd_workspace_size(14848, 59392, 0) <= (64 << 20)   # the largest workload fits
 
 
 def test_lambda_and_objective_argument_errors(lib):
