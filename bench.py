@@ -3,11 +3,17 @@
 One step = one layer of the 4096 x 4096 attention-projection workload, 4-bit,
 inputs resident in HBM:  Sigma = X X^T + 0.01 mean(diag) I over 128 x 2048
 heavy-tailed tokens -> per-row grid -> 10 CD sweeps (objective after each)
--> exact objective.  value = column updates per second of the whole step
-(p x 10 per step).  The outlier-aware path (3-bit, 1% outliers: lambda_max,
-P_s(W), outlier grid, 10 CD + IHT iterations) is timed in the same run and
-reported under "outlier"; the CPU oracle is timed on a bounded sample under
-"cpu_baseline".
+-> exact objective.  value = CD column updates per second of sweep time
+(p x 10 / the 10 sweeps' time, HIP events); the whole step's rate is
+layer_column_updates_per_s.  The headline roofline is the CD step kernel
+(the block-update GEMM with the next panel), the Gram's is under
+"rooflines"; each counts the method's own flops (2qp^2 per sweep,
+p(p+1)n per Gram) against the peak of the matrix-core type the kernels
+issue (bf16: the fp32 products are exact three-way bf16 splits).  The
+outlier-aware path (3-bit, 1% outliers: lambda_max, P_s(W), outlier grid, 10
+CD + IHT iterations) is timed in the same run under "outlier"; the CPU
+oracle is timed under "cpu_baseline" (all sweeps on every row; its Gram on a
+token sample, scaled).
 
     python bench.py [--gpus 1] [--steps K] [--warmup W]
 """
@@ -29,6 +35,8 @@ FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 SPLIT_PRODUCTS = 6             # bf16 products per fp32 product (exact three-way split)
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_c2_4096x4096.md")
+LAUNCH_PROFILE = os.path.join(ROOT, "profiles", "kernel_trace_gram_cd_step_c2_4096x4096.md")
+PARITY_RECORD = os.path.join(ROOT, "profiles", "parity_c2_4096x4096.md")
 CALIB_COPY_BYTES = 256 << 20
 
 
@@ -52,29 +60,49 @@ def kernel_source_hash(kernel):
     return h.hexdigest()
 
 
+def _json_block(path):
+    try:
+        with open(path) as f:
+            text = f.read()
+    except OSError:
+        return None
+    m = re.search(r"```json\n(.*?)\n```", text, re.S)
+    return json.loads(m.group(1)) if m else None
+
+
 def measured_traffic():
     """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE summary
     (copy-calibrated), keyed by kernel; a kernel is left out when its sources
     changed since the counters were taken."""
-    try:
-        with open(TRAFFIC_PROFILE) as f:
-            text = f.read()
-    except OSError:
+    data = _json_block(TRAFFIC_PROFILE)
+    if not data:
         return {}
-    m = re.search(r"```json\n(.*?)\n```", text, re.S)
-    if not m:
-        return {}
-    data = json.loads(m.group(1))
     return {k: v["hbm_bytes_per_launch"] for k, v in data["kernels"].items()
             if k in KERNEL_SOURCES and v.get("source_sha256") == kernel_source_hash(k)}
+
+
+def profiled_panel_launch():
+    """Mean duration of the panel-only launch (the first step launch of each
+    sweep) from the committed kernel trace, or None when the step kernel's
+    sources changed since the trace was taken."""
+    data = _json_block(LAUNCH_PROFILE)
+    if not data or data.get("source_sha256") != kernel_source_hash("cd_step_kernel"):
+        return None
+    return data
+
+
+def parity_record():
+    """CD parity figures of the c2 workload from the committed record of the
+    GPU parity tests (teacher-forced and free-running, 512 seeded rows)."""
+    return _json_block(PARITY_RECORD)
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-CPU_GRAM_TOKENS = 32768      # oracle Gram sample (about 10 s on 16 host threads)
-CPU_SWEEP_ROWS = 1024        # oracle sweep sample
+CPU_GRAM_TOKENS = 8192       # oracle Gram sample (about 2 s on 16 host threads)
+CPU_SWEEP_ROWS = 1024        # oracle sweep sample with --oracle-sample
 CPU_ONE_THREAD_ROWS = 64     # single-thread sweep sample
 
 # Child process for the single-thread figure: OpenMP's thread count is fixed
@@ -115,35 +143,47 @@ def one_thread_sweep(S, W, scale, zero, bits):
     return float(secs)
 
 
-def cpu_baseline(spec, X_head, W, scale, zero, sweeps):
+def cpu_baseline(spec, X_head, W, scale, zero, sweeps, full=False):
     """The oracle as it stands on the host cores, on a bounded sample of the
-    same step: Gram on the first n' tokens (scaled by n/n'), one CD sweep on r
-    seeded rows (scaled by q/r rows and by the sweep count); plus the sweep on
-    fewer rows with a single thread."""
+    same step: one CD sweep on r seeded rows, scaled by q/r rows (the cost is
+    exactly linear in the rows, which are independent) -- or, with full, all
+    sweeps on every row, unscaled -- and the Gram on the first n' tokens
+    (scaled by n/n'); plus the sweep on fewer rows with a single thread.
+    value: column updates per second of sweeping, as the GPU's value."""
     import oracle
     q, p, n = spec.q, spec.p, spec.n
     n_s = X_head.shape[1]
     t0 = time.perf_counter()
     S = oracle.damp(oracle.gram(X_head), spec.damp)
     t_gram = time.perf_counter() - t0
-    rows = __import__("synth").row_sample(q, CPU_SWEEP_ROWS, spec.cfg)
-    t_sweep = oracle.cd_sweep_timed(W[rows], S, spec.bits, scale[rows], zero[rows])
-    t_step = t_gram * (n / n_s) + t_sweep * (q / len(rows)) * sweeps
+    if full:
+        rows = np.arange(q)
+        t_sweeps = oracle.cd_sweep_timed(W, S, spec.bits, scale, zero, sweeps)
+        sweep_all = t_sweeps / sweeps
+        how = f"all {sweeps} sweeps over all {q} rows (not scaled)"
+        measured = t_sweeps
+    else:
+        rows = __import__("synth").row_sample(q, CPU_SWEEP_ROWS, spec.cfg)
+        t_sweep = oracle.cd_sweep_timed(W[rows], S, spec.bits, scale[rows], zero[rows])
+        sweep_all = t_sweep * (q / len(rows))
+        how = f"one Lemma-1 sweep over {len(rows)} of {q} rows (x{q / len(rows):.0f} rows)"
+        measured = t_sweep
+    t_step = t_gram * (n / n_s) + sweep_all * sweeps
     r1 = rows[:CPU_ONE_THREAD_ROWS]
     t_one = one_thread_sweep(S, W[r1], scale[r1], zero[r1], spec.bits)
     return {
-        "value": p * sweeps / t_step,
+        "value": p / sweep_all,
         "unit": "column-updates/s",
         "cores": oracle.num_threads(),
         "cpu_model": cpu_model(),
         "kind": "oracle",
-        "sample": (f"Gram over {n_s} of {n} tokens (x{n / n_s:.0f}), one Lemma-1 sweep over "
-                   f"{len(rows)} of {q} rows (x{q / len(rows):.0f} rows, x{sweeps} sweeps); "
-                   f"measured {t_gram:.2f} s + {t_sweep:.2f} s"),
-        "step_s_extrapolated": t_step,
+        "sample": (f"{how}, measured {measured:.2f} s; Gram over {n_s} of {n} tokens "
+                   f"(x{n / n_s:.0f}), measured {t_gram:.2f} s"),
+        "sweep_s": sweep_all,
+        "layer_s": t_step,
+        "layer_column_updates_per_s": p * sweeps / t_step,
         "one_thread_sweep": {"rows": len(r1), "seconds": t_one,
-                             "coordinate_updates_per_s": len(r1) * p / t_one,
-                             "speedup_of_all_threads": (t_one / len(r1)) / (t_sweep / len(rows))},
+                             "coordinate_updates_per_s": len(r1) * p / t_one},
     }
 
 
@@ -156,6 +196,9 @@ def main():
     ap.add_argument("--no-outlier", action="store_true", help="skip the outlier-aware timing")
     ap.add_argument("--no-peaks", action="store_true",
                     help="skip the matrix-core / copy peak checks (libqe_peak.so)")
+    ap.add_argument("--oracle-sample", action="store_true",
+                    help="time one oracle sweep on a 1024-row sample (scaled) instead of all "
+                         "sweeps on every row (about 20 s on 16 host threads)")
     ap.add_argument("--calib-copy", action="store_true",
                     help="end with a plain 256 MiB device copy (HBM counter calibration)")
     ap.add_argument("--configs", action="store_true",
@@ -244,7 +287,8 @@ def main():
         st = P.sync_status(w)
         assert st == 0, f"device status {st}"
     ms_per_step = wall / args.steps * 1e3
-    value = p * sweeps / (wall / args.steps)
+    cd_phase_t = float(np.median(phase["cd"]))           # the 10 sweeps of a step
+    value = p * sweeps / cd_phase_t                      # column updates per second of sweeping
     f_sweeps = obj.cpu().numpy()
     exact = exact.cpu().numpy()
 
@@ -274,35 +318,47 @@ def main():
     torch.cuda.synchronize()
     sweep_median_2_k = float(np.median([a.elapsed_time(b) * 1e-3 for a, b in per_sweep[1:]]))
     launches = sweeps * (nb + 1)
-    cd_flops_per_launch = 2.0 * q * p * p / (nb + 1)      # 2qp^2 per sweep over nb + 1 launches
     cd_avg = t_steps / launches
-    cd_tflops = cd_flops_per_launch / cd_avg / 1e12
-    cd_mfma_flops = SPLIT_PRODUCTS * cd_flops_per_launch
-    cd_bf16_tflops = cd_mfma_flops / cd_avg / 1e12
     gram_t = float(np.median(phase["gram"]))
-    gram_flops = float(p) * (p + 1) * n                      # fp32 products (symmetric half)
-    gram_tflops = gram_flops / gram_t / 1e12
-    gram_mfma_flops = SPLIT_PRODUCTS * gram_flops            # the split algorithm's bf16 flops
-    gram_bf16_tflops = gram_mfma_flops / gram_t / 1e12
-    sweep_t = float(np.median(phase["cd"])) / sweeps
+    sweep_t = cd_phase_t / sweeps
     traffic = measured_traffic()
-    roof_cd = {"kernel": "cd_step_kernel<8>", "bound": "mfma", "achieved": cd_bf16_tflops,
-               "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-               "frac": cd_bf16_tflops / BF16_MFMA_PEAK_TFLOPS,
-               "traffic": traffic.get("cd_step_kernel"),
-               "avg_launch_s": cd_avg, "flops_per_launch": cd_mfma_flops,
-               "products": "bf16, 6 per fp32 product (exact 3-way split)",
-               "fp32_equivalent_tflops": cd_tflops,
-               "fp32_equivalent_frac": cd_tflops / FP32_MFMA_PEAK_TFLOPS}
-    roof_gram = {"kernel": "gram_x3w_kernel", "bound": "mfma", "achieved": gram_bf16_tflops,
-                 "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                 "frac": gram_bf16_tflops / BF16_MFMA_PEAK_TFLOPS,
-                 "traffic": traffic.get("gram_x3w_kernel"),
-                 "call_s": gram_t, "flops_per_call": gram_mfma_flops,
-                 "products": "bf16, 6 per fp32 product (exact 3-way split)",
-                 "fp32_equivalent_tflops": gram_tflops,
-                 "fp32_equivalent_frac": gram_tflops / FP32_MFMA_PEAK_TFLOPS}
-    dominant = roof_gram if gram_t > sweeps * sweep_t else roof_cd
+
+    def roofline(kernel, flops, seconds, extra):
+        """The method's own flops (fp32 multiply-adds x 2) per launch over the
+        launch time, against the peak of the matrix-core type issued (bf16);
+        the six-product issue rate and the fp32-equivalent fraction are
+        separate fields."""
+        achieved = flops / seconds / 1e12
+        r = {"kernel": kernel, "bound": "mfma", "achieved": achieved,
+             "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+             "frac": achieved / BF16_MFMA_PEAK_TFLOPS,
+             "traffic": traffic.get(kernel.split("<")[0]),
+             "flops_per_launch": flops,
+             "flops_counted": "the method's: fp32 products of the algorithm, 2 flops each",
+             "issued": "bf16 matrix cores, 6 exact bf16 products per fp32 product",
+             "issued_bf16_tflops": SPLIT_PRODUCTS * achieved,
+             "issued_frac_of_bf16_peak": SPLIT_PRODUCTS * achieved / BF16_MFMA_PEAK_TFLOPS,
+             "fp32_equivalent_frac": achieved / FP32_MFMA_PEAK_TFLOPS,
+             "frac_of_split_ceiling": achieved / (BF16_MFMA_PEAK_TFLOPS / SPLIT_PRODUCTS)}
+        r.update(extra)
+        return r
+
+    # 2qp^2 per sweep over its nb + 1 launches; p(p+1)n for the Gram (symmetric half)
+    roof_cd = roofline("cd_step_kernel<8>", 2.0 * q * p * p / (nb + 1), cd_avg,
+                       {"avg_launch_s": cd_avg, "launches_per_sweep": nb + 1})
+    roof_gram = roofline("gram_x3w_kernel", float(p) * (p + 1) * n, gram_t, {"call_s": gram_t})
+
+    # the column-sequential panel: a panel-only launch (256 columns x q rows)
+    # moves 17 bytes per coordinate (R, What in; What, code, delta out)
+    panel = None
+    prof = profiled_panel_launch()
+    if prof:
+        bytes_panel = 17.0 * q * super_w
+        t_panel = prof["panel_only_launch_us"] * 1e-6
+        panel = {"launch_s": t_panel, "algorithmic_bytes": bytes_panel,
+                 "achieved_GBps": bytes_panel / t_panel / 1e9,
+                 "frac_of_hbm_peak": bytes_panel / t_panel / 1e9 / HBM_PEAK_GBS,
+                 "source": os.path.relpath(LAUNCH_PROFILE, ROOT) + " (rocprofv3 kernel trace)"}
 
     result = {
         "metric": METRIC,
@@ -319,19 +375,21 @@ def main():
         "data": "synthetic",
         "config": {"workload": spec.name, "q": q, "p": p, "n": n, "bits": bits,
                    "sweeps": sweeps, "block": block, "damp": spec.damp},
-        "roofline": dominant,
+        "roofline": roof_cd,
         "rooflines": [roof_cd, roof_gram],
+        "panel": panel,
         "breakdown_s": {"gram": gram_t, "grid": float(np.median(phase["grid"])),
-                        "cd_10_sweeps": float(np.median(phase["cd"])),
+                        "cd_10_sweeps": cd_phase_t,
                         "exact_objective": float(np.median(phase["exact"]))},
         "sweep_time_s": sweep_t,
         "sweep_time_median_2_to_k_s": sweep_median_2_k,
-        "cd_column_updates_per_s": p / sweep_t,
-        "coordinate_updates_per_s": q * value,           # q * p * sweeps per step time
-        "cd_coordinate_updates_per_s": q * p / sweep_t,
+        "cd_column_updates_per_s": value,
+        "cd_coordinate_updates_per_s": q * value,
         "layer_time_s": ms_per_step / 1e3,
+        "layer_column_updates_per_s": p * sweeps / (wall / args.steps),
         "objective_per_sweep": [float(x) for x in f_sweeps],
         "rel_calibration_error": float(exact[0] / exact[1]),
+        "parity": parity_record(),
     }
 
     if not args.no_outlier:
@@ -344,12 +402,14 @@ def main():
         mp = peaks.measure(torch)
         result["measured_peaks"] = mp
         for r in result["rooflines"]:
-            r["frac_of_measured_bf16_peak"] = r["achieved"] / mp["mfma_bf16_tflops"]
+            r["issued_frac_of_measured_bf16_peak"] = r["issued_bf16_tflops"] / mp["mfma_bf16_tflops"]
 
     if not args.no_cpu:
         log("CPU oracle baseline")
         result["cpu_baseline"] = cpu_baseline(spec, X_head, W_h, scale.cpu().numpy(),
-                                              zero.cpu().numpy(), sweeps)
+                                              zero.cpu().numpy(), sweeps,
+                                              full=not args.oracle_sample)
+        result["gpu_over_oracle"] = value / result["cpu_baseline"]["value"]
     if args.calib_copy:
         a = torch.ones(CALIB_COPY_BYTES // 4, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)

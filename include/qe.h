@@ -46,6 +46,7 @@ typedef int qe_status;
 #define QE_ERR_HIP         5  /* a HIP runtime call failed */
 #define QE_ERR_UNSUPPORTED 6  /* a valid request this library does not implement */
 #define QE_ERR_TOO_LARGE   7  /* qe_cd_sweep_noalloc: the sizes need more than its fixed scratch */
+#define QE_ERR_NONFINITE   8  /* QE_DEBUG_CHECKS found a NaN or infinity in an input */
 
 /* Layouts of X for qe_gram, optionally or-ed with QE_GRAM_FP32. */
 #define QE_LAYOUT_PN 0        /* X is p x n: each channel's n tokens contiguous */
@@ -73,6 +74,14 @@ typedef int qe_status;
 /* Block-update and residual products on the fp32 matrix cores instead of the
  * default exact three-way bf16 split (the split is described at qe_gram). */
 #define QE_CD_FP32 0x20u
+/* Checks before the sweeps (the paper asks for checks on the inputs before
+ * QuantEase runs, footnote to Lemma 1): every input of the call -- W, Sigma,
+ * scale, zero, What unless QE_INIT_FROM_W, R (or E) with QE_R_VALID, and H in
+ * the outlier-aware call -- is scanned for NaN and infinity, which sets
+ * QE_ERR_NONFINITE (reported by qe_sync_status; the rest of the call does
+ * nothing).  One extra read of those arrays (about 30 us at 4096 x 4096).
+ * Without the flag only Sigma's diagonal and the grid are checked. */
+#define QE_DEBUG_CHECKS 0x40u
 
 /* Human-readable name of a status code (static string). */
 const char* qe_status_string(qe_status s);
@@ -135,7 +144,8 @@ qe_status qe_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, i
  * W_hat:  q x p, device, in/out.  codes: q x p uint8, device, in/out.
  * R:      q x p, device, in/out: (What - W) Sigma on exit.
  * sweeps: >= 0 full passes over the columns.
- * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_PERIOD(k).
+ * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_PERIOD(k)
+ *         | QE_CD_FP32 | QE_DEBUG_CHECKS.
  *         Without QE_INIT_FROM_W and without QE_R_VALID, R is first
  *         computed as (What - W) Sigma (warm start from any What, Sec. 3.1).
  * obj:    NULL, or device array of `sweeps` doubles receiving
@@ -193,6 +203,7 @@ qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int
  *           QE_OUTLIER_COLUMNS: structured outliers (whole columns); start
  *           from qe_topk_columns on W.
  *           Without QE_INIT_FROM_W / QE_R_VALID, E = (What + H - W) Sigma.
+ *           QE_CD_FP32 and QE_DEBUG_CHECKS as for qe_cd_sweep.
  * obj:      NULL or device array of 2*sweeps doubles: obj[2k] = g after the
  *           CD sweep of iteration k, obj[2k+1] = g after its IHT step.
  * scale/zero: the outlier-aware grid (qe_grid_minmax with H excluded).

@@ -80,9 +80,9 @@ def num_threads() -> int:
     return int(_load().qeo_num_threads())
 
 
-def cd_sweep_timed(W, Sigma, bits, scale, zero) -> float:
-    """Wall seconds of one Lemma-1 sweep from What = W, clocked around the C
-    call only (T = W Sigma is formed before the clock starts)."""
+def cd_sweep_timed(W, Sigma, bits, scale, zero, sweeps: int = 1) -> float:
+    """Wall seconds of `sweeps` Lemma-1 sweeps from What = W, clocked around
+    the C calls only (T = W Sigma is formed before the clock starts)."""
     import time
     lib = _load()
     W = np.asarray(W)
@@ -94,13 +94,15 @@ def cd_sweep_timed(W, Sigma, bits, scale, zero) -> float:
     valid = np.zeros((q, p), np.uint8)
     sc = _c(scale, np.float32).astype(np.float64)
     ze = _c(zero, np.float32).astype(np.float64)
-    t0 = time.perf_counter()
-    rc = lib.qeo_cd_sweep_lemma1(_p(T, _f64p), _p(S, _f64p), q, p, bits, _p(sc, _f64p),
-                                 _p(ze, _f64p), _p(Wh, _f64p), _p(codes, _i32p),
-                                 _p(valid, _u8p), None, 0, 0)
-    dt = time.perf_counter() - t0
-    if rc != 0:
-        raise ValueError("Sigma has a non-positive diagonal entry")
+    dt = 0.0
+    for _ in range(sweeps):
+        t0 = time.perf_counter()
+        rc = lib.qeo_cd_sweep_lemma1(_p(T, _f64p), _p(S, _f64p), q, p, bits, _p(sc, _f64p),
+                                     _p(ze, _f64p), _p(Wh, _f64p), _p(codes, _i32p),
+                                     _p(valid, _u8p), None, 0, 0)
+        dt += time.perf_counter() - t0
+        if rc != 0:
+            raise ValueError("Sigma has a non-positive diagonal entry")
     return dt
 
 

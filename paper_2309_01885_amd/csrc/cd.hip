@@ -659,6 +659,16 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     float* d1 = w.take<float>((size_t)q * S);
     double* part = w.take<double>(kObjBlocks);
 
+    if (flags & QE_DEBUG_CHECKS) {
+        // every input of the call (the footnote to Lemma 1: checks before the sweeps)
+        const float* inputs[6] = {W, Sigma, scale, zero,
+                                  (flags & QE_INIT_FROM_W) ? nullptr : Wh,
+                                  (flags & QE_R_VALID) ? R : nullptr};
+        const int64_t counts[6] = {q * p, p * p, q, q, q * p, q * p};
+        for (int k = 0; k < 6; ++k)
+            if (launch_nonfinite_scan(inputs[k], counts[k], status, s) != QE_OK) return QE_ERR_HIP;
+        if (launch_nonfinite_scan(H, q * p, status, s) != QE_OK) return QE_ERR_HIP;
+    }
     hipLaunchKernelGGL(diag_prep_kernel, dim3((unsigned)cdiv(p, 256)), dim3(256), 0, s, Sigma, p,
                        inv_d, status);
     hipLaunchKernelGGL(grid_prep_kernel, dim3((unsigned)cdiv(q, 256)), dim3(256), 0, s, scale,

@@ -45,6 +45,39 @@ __global__ __launch_bounds__(256) void grid_minmax_kernel(const float* __restric
     }
 }
 
+// ---------------------------------------------------------------- input checks
+// Any NaN or infinity among `count` floats sets QE_ERR_NONFINITE.
+__global__ __launch_bounds__(256) void nonfinite_scan_kernel(const float* __restrict__ a,
+                                                             int64_t count, int vec4, int* status)
+{
+    const int64_t G = (int64_t)gridDim.x * blockDim.x;
+    const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    // exponent field all ones: infinity or NaN
+    auto bad = [](float x) { return (int)((__float_as_uint(x) & 0x7f800000u) == 0x7f800000u); };
+    int found = 0;
+    int64_t tail = 0;
+    if (vec4) {
+        const f32x4* a4 = reinterpret_cast<const f32x4*>(a);
+        const int64_t n4 = count / 4;
+        for (int64_t e = tid; e < n4; e += G) {
+            const f32x4 v = a4[e];
+            found |= bad(v[0]) | bad(v[1]) | bad(v[2]) | bad(v[3]);
+        }
+        tail = n4 * 4;
+    }
+    for (int64_t e = tail + tid; e < count; e += G) found |= bad(a[e]);
+    if (found) set_status(status, QE_ERR_NONFINITE);
+}
+
+qe_status launch_nonfinite_scan(const float* a, int64_t count, int* status, hipStream_t s)
+{
+    if (!a || count <= 0) return QE_OK;
+    const int64_t wgs = std::min<int64_t>(2048, std::max<int64_t>(1, cdiv(count / 4, 256)));
+    hipLaunchKernelGGL(nonfinite_scan_kernel, dim3((unsigned)wgs), dim3(256), 0, s, a, count,
+                       aligned16(a) ? 1 : 0, status);
+    return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
+}
+
 qe_status launch_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, int bits,
                              float* scale, float* zero, hipStream_t s)
 {

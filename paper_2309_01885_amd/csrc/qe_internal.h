@@ -437,6 +437,7 @@ qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* S
                       int accumulate, float damp, void* ws, hipStream_t s);
 qe_status launch_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, int bits,
                              float* scale, float* zero, hipStream_t s);
+qe_status launch_nonfinite_scan(const float* a, int64_t count, int* status, hipStream_t s);
 size_t objective_ws_bytes(int64_t q, int64_t p);
 qe_status launch_objective(const float* W, const float* Wh, const float* H, const float* Sigma,
                            int64_t q, int64_t p, double* out, void* ws, hipStream_t s);

@@ -24,6 +24,7 @@ QE_ERR_WORKSPACE = 4
 QE_ERR_HIP = 5
 QE_ERR_UNSUPPORTED = 6
 QE_ERR_TOO_LARGE = 7
+QE_ERR_NONFINITE = 8
 QE_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 QE_LAYOUT_PN = 0
@@ -36,6 +37,7 @@ QE_CODES_VALID = 0x4
 QE_RELAX_MASK = 0xff00
 QE_OUTLIER_COLUMNS = 0x10
 QE_CD_FP32 = 0x20
+QE_DEBUG_CHECKS = 0x40
 
 
 def QE_RELAX_PERIOD(k: int) -> int:

@@ -61,9 +61,9 @@ def test_status_strings_and_version(lib):
     L, _ = lib
     L.qe_status_string.restype = ctypes.c_char_p
     L.qe_status_string.argtypes = [ctypes.c_int]
-    texts = [L.qe_status_string(c).decode() for c in range(8)]
+    texts = [L.qe_status_string(c).decode() for c in range(9)]
     assert texts[0] == "ok"
-    assert len(set(texts)) == 8 and all(texts)
+    assert len(set(texts)) == 9 and all(texts)
     assert L.qe_status_string(99).decode() == "unknown status"
     assert L.qe_version() == 1
 
@@ -169,6 +169,8 @@ def test_cd_sweep_argument_errors(lib):
     assert _cd(L, block=48) == QE_ERR_ARG         # block widths 16, 32, 64, 128 (0 = default)
     assert _cd(L, sweeps=-1) == QE_ERR_ARG
     assert _cd(L, flags=0x10) == QE_ERR_ARG       # QE_OUTLIER_COLUMNS belongs to the outlier call
+    assert _cd(L, flags=0x80) == QE_ERR_ARG       # no such flag
+    assert _cd(L, flags=0x40, ws=NULL) == QE_ERR_WORKSPACE   # QE_DEBUG_CHECKS is accepted
     assert _cd(L, ws=NULL) == QE_ERR_WORKSPACE
     assert _cd(L, ws_bytes=1024) == QE_ERR_WORKSPACE
 

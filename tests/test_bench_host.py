@@ -51,6 +51,16 @@ def test_cpu_baseline_small():
     one = r["one_thread_sweep"]
     assert one["rows"] == min(bench.CPU_ONE_THREAD_ROWS, spec.q) and one["seconds"] > 0
     assert "256 of 2048 tokens" in r["sample"]
+    assert r["value"] == spec.p / r["sweep_s"]
+    full = bench.cpu_baseline(spec, np.ascontiguousarray(X), W[:64], sc[:64], ze[:64], 2,
+                              full=True)
+    assert "all 2 sweeps over all" in full["sample"]
+
+
+def test_profile_readers():
+    """The committed launch and parity records parse (or are absent)."""
+    for rec in (bench.profiled_panel_launch(), bench.parity_record()):
+        assert rec is None or isinstance(rec, dict)
 
 
 def test_help_lists_the_switches():
@@ -58,5 +68,5 @@ def test_help_lists_the_switches():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 0
     for flag in ("--gpus", "--steps", "--warmup", "--no-cpu", "--no-outlier", "--no-peaks",
-                 "--calib-copy", "--configs"):
+                 "--calib-copy", "--configs", "--oracle-sample"):
         assert flag in r.stdout, flag

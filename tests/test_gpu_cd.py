@@ -291,3 +291,52 @@ def test_relaxed_sweeps_match_oracle(qe, oracle, period, sweeps):
     # R stays consistent with What through relaxed sweeps
     Rex = (host(Wh).astype(np.float64) - W) @ S32.astype(np.float64)
     assert np.max(np.abs(host(R) - Rex)) <= 1e-5 * np.max(np.abs(Rex)) + 1e-7
+
+
+@pytest.mark.parametrize("where", ["W", "Sigma", "scale", "zero", "What", "R"])
+def test_debug_checks_report_nonfinite_inputs(qe, oracle, where):
+    """QE_DEBUG_CHECKS (footnote to Lemma 1: checks before the sweeps): a NaN
+    or infinity in any input of the call is reported as QE_ERR_NONFINITE and
+    the outputs are left as they were."""
+    q, p, bits = 64, 160, 4
+    W, X = layer(q, p, 512, 31, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, bits)
+    arrays = {"W": W.copy(), "Sigma": S32.copy(), "scale": scale.copy(), "zero": zero.copy()}
+    # a warm start from What with a valid R: both are inputs then
+    g = gpu_cd(qe, W, S32, bits, scale, zero, 1, per_sweep=False)
+    arrays["What"], arrays["R"] = g["What"].copy(), g["R"].copy()
+    a = arrays[where].reshape(-1)
+    a[a.size // 3] = np.nan if where in ("W", "What", "zero") else np.inf
+    Wd, Sd = dev(arrays["W"]), dev(arrays["Sigma"])
+    Wh, R = dev(arrays["What"]), dev(arrays["R"])
+    codes = dev(g["codes"].astype(np.uint8))
+    before = (host(Wh).copy(), host(R).copy())
+    flags = qe.QE_R_VALID | qe.QE_CODES_VALID | qe.QE_DEBUG_CHECKS
+    with pytest.raises(qe.QEError) as e:
+        qe.cd_sweep(Wd, Sd, bits, dev(arrays["scale"]), dev(arrays["zero"]), Wh, codes, R, 2,
+                    flags=flags)
+    assert e.value.code == qe.QE_ERR_NONFINITE
+    assert np.array_equal(host(Wh), before[0], equal_nan=True)
+    assert np.array_equal(host(R), before[1], equal_nan=True)
+
+
+def test_debug_checks_pass_clean_inputs_unchanged(qe, oracle):
+    """On finite inputs the flag changes nothing (bitwise), and an output-only
+    What (QE_INIT_FROM_W) is not scanned even when it holds NaNs."""
+    q, p, bits = 96, 250, 4
+    W, X = layer(q, p, 1024, 32, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, bits)
+    out = []
+    for flags in (qe.QE_INIT_FROM_W, qe.QE_INIT_FROM_W | qe.QE_DEBUG_CHECKS):
+        Wd = dev(W)
+        Wh = torch.full_like(Wd, float("nan"))
+        R = torch.full_like(Wd, float("nan"))
+        codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+        obj = torch.zeros(3, dtype=torch.float64, device="cuda")
+        qe.cd_sweep(Wd, dev(S32), bits, dev(scale), dev(zero), Wh, codes, R, 3, flags=flags,
+                    obj=obj)
+        out.append((host(Wh), host(codes), host(R), host(obj)))
+    for x, y in zip(*out):
+        assert np.array_equal(x, y)

@@ -191,3 +191,25 @@ def test_structured_outlier_matches_oracle(qe, oracle, q, p, ncols, corr):
                           np.nonzero(np.any(ref.H != 0, axis=0))[0])
     assert np.allclose(Hg, ref.H, rtol=1e-3, atol=1e-7)
     assert np.mean(host(codes).astype(np.int32) != ref.codes) <= 1e-3
+
+
+def test_outlier_debug_checks_scan_h(qe, oracle):
+    """QE_DEBUG_CHECKS in the outlier-aware call also scans H."""
+    q, p, bits = 48, 96, 3
+    W = synth.gaussian((q, p), seed=41, std=0.02)
+    X = synth.correlated_activations(p, 512, 0.9, 42)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    s = 40
+    H, sup, nnz = qe.topk_abs(dev(W), s)
+    Hh = host(H)
+    Hh[host(sup)[0] // p, host(sup)[0] % p] = np.inf
+    scale, zero = oracle.grid_minmax(W, bits, Hh)
+    Wd, Sd = dev(W), dev(S32)
+    Wh = torch.empty_like(Wd)
+    E = torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    lam = float(np.float32(oracle.lambda_max(S32)))
+    with pytest.raises(qe.QEError) as e:
+        qe.cd_outlier_sweep(Wd, Sd, bits, dev(scale), dev(zero), Wh, codes, dev(Hh), E, s, lam,
+                            sup, nnz, 2, flags=qe.QE_INIT_FROM_W | qe.QE_DEBUG_CHECKS)
+    assert e.value.code == qe.QE_ERR_NONFINITE
