@@ -180,6 +180,7 @@ struct StepArgs {
     float maxq;
     int codes_valid;      // current codes may be kept on an exact tie (Sec. 3.3)
     int relax;            // write beta unquantized (relaxed sweep, Sec. 3.2)
+    int intd;             // deltas as code differences k_new - k_old (see launch_cd)
     int fp32;             // GEMM role on the fp32 matrix cores (else the split bf16 ones)
     int n_panel;          // workgroups [0, n_panel) run the panel
     int64_t tiles_n;      // GEMM column tiles
@@ -196,7 +197,8 @@ struct PanelState {
     float L[SLOTS];     // residual of the lane's block columns (local copy of R_{i,J})
     float w[SLOTS];     // What_{i,J} (relaxed sweeps: updated as the block runs)
     float u[SLOTS];     // quantized: 1 / (Sigma_jj s_i); relaxed: 1 / Sigma_jj
-    float v[SLOTS];     // quantized: What_ij / s_i + z_i; relaxed: delta of owned columns
+    float v[SLOTS];     // quantized: What_ij / s_i + z_i (the code itself with code
+                        // differences); relaxed: delta of owned columns
     float k[SLOTS];     // quantized: code of the column (NaN while none is valid)
     float srow[3][SLOTS];   // Sigma rows J, J+1, J+2 (lane's columns), fetched ahead
 };
@@ -235,7 +237,7 @@ __device__ __forceinline__ void load_srow(float (&dst)[SLOTS], const float* sS, 
 // One column update (column J of the block) for all 16 rows of the workgroup.
 // FULL blocks (width == B) carry no per-column test.  The Sigma row of column
 // J + 2 is fetched from LDS while column J's dependent chain runs.
-template <int SLOTS, int J, bool FULL, bool RELAX>
+template <int SLOTS, int J, bool FULL, bool RELAX, bool INTD>
 __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* sS, int g,
                                            int width, float s, float z, float maxq)
 {
@@ -263,7 +265,10 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
         // modified CD: a valid, equally near current level is kept (NaN never is)
         const float kc = st.k[M];
         const float k = fabsf(t - kc) <= fabsf(t - kn) ? kc : kn;
-        delta = fmaf(s, k - z, -w);                  // s (k - z) - What_ij
+        if constexpr (INTD)
+            delta = s * (k - kc);                    // What on the grid: s (k_new - k_old)
+        else
+            delta = fmaf(s, k - z, -w);              // s (k - z) - What_ij
         st.k[M] = own ? k : kc;
     }
     const float db = row_bcast<O>(delta);
@@ -273,14 +278,14 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
     for (int mm = M; mm < SLOTS; ++mm) st.L[mm] = fmaf(db, st.srow[J % 3][mm], st.L[mm]);
 }
 
-template <int SLOTS, bool FULL, bool RELAX, int... Js>
+template <int SLOTS, bool FULL, bool RELAX, bool INTD, int... Js>
 __device__ __forceinline__ void panel_run(std::integer_sequence<int, Js...>,
                                           PanelState<SLOTS>& st, const float* sS, int g,
                                           int width, float s, float z, float maxq)
 {
     load_srow<SLOTS>(st.srow[0], sS, 0, g);
     if constexpr (16 * SLOTS > 1) load_srow<SLOTS>(st.srow[1], sS, 1, g);
-    (panel_step<SLOTS, Js, FULL, RELAX>(st, sS, g, width, s, z, maxq), ...);
+    (panel_step<SLOTS, Js, FULL, RELAX, INTD>(st, sS, g, width, s, z, maxq), ...);
 }
 
 // Stages Sigma[r0 + k][c0 + c] (k < kw, c < cw; else 0) into LDS with the
@@ -324,8 +329,9 @@ __device__ __forceinline__ void stage_sigma_block(const float* __restrict__ Sigm
     }
 }
 
-// L_{i,J} += D_{i, k0..k0+kw} Sigma_{r0..r0+kw, J} for the workgroup's 16 rows
-// (kw <= B), with D a q x S row-major delta buffer.
+// L_{i,J} += dscale_i D_{i, k0..k0+kw} Sigma_{r0..r0+kw, J} for the workgroup's
+// 16 rows (kw <= B), with D a q x S row-major delta buffer and dscale the row's
+// grid step when D holds code differences (else 1).
 //
 // B >= 64: on matrix cores (v_mfma_f32_16x16x4f32, 16 x 16 output tiles; wave
 // w owns block columns [B/4 w, B/4 (w+1))).  A = the 16 delta rows, fetched as
@@ -341,7 +347,7 @@ template <int SLOTS>
 __device__ __forceinline__ void add_block_update(PanelState<SLOTS>& st, const StepArgs& a,
                                                  const float* D, int64_t k0, int kw, int64_t r0,
                                                  int64_t j0, int width, int64_t i0, int lrow,
-                                                 int g, float* lds)
+                                                 int g, float* lds, float dscale)
 {
     constexpr int B = 16 * SLOTS;
     if constexpr (SLOTS >= 4) {
@@ -419,7 +425,7 @@ __device__ __forceinline__ void add_block_update(PanelState<SLOTS>& st, const St
             for (int v = 0; v < 4; ++v) sC[(4 * h + v) * B + CPW * wave + 16 * t + r] = acc[t][v];
         __syncthreads();
 #pragma unroll
-        for (int m = 0; m < SLOTS; ++m) st.L[m] += sC[lrow * B + 16 * m + g];
+        for (int m = 0; m < SLOTS; ++m) st.L[m] = fmaf(dscale, sC[lrow * B + 16 * m + g], st.L[m]);
     } else {
         float* sS = lds;            // B x B
         float* sD = lds + B * B;    // 16 x B
@@ -432,7 +438,7 @@ __device__ __forceinline__ void add_block_update(PanelState<SLOTS>& st, const St
         }
         __syncthreads();
         for (int k = 0; k < kw; ++k) {
-            const float dk = sD[lrow * B + k];
+            const float dk = dscale * sD[lrow * B + k];
 #pragma unroll
             for (int m = 0; m < SLOTS; ++m) st.L[m] = fmaf(dk, sS[k * B + g * SLOTS + m], st.L[m]);
         }
@@ -478,14 +484,18 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
                 // the current code is recovered exactly from What (|k - z| <= 255
                 // keeps the rounding error far below 1/2)
                 st.k[m] = cvalid ? rintf(st.v[m]) : __builtin_nanf("");
+                // with code differences t is taken from the code itself: What's
+                // exact level s (k - z) over s, plus z, is k
+                if (a.intd) st.v[m] = st.k[m];
             }
         }
+        const float dscale = a.intd ? s : 1.f;
         // (1) look-ahead: deltas of the previous super-block, R_{i,J} written back
         if (a.psb >= 0) {
             for (int kc = 0; kc < a.psbw; kc += B) {
                 const int kw = min(B, a.psbw - kc);
                 add_block_update<SLOTS>(st, a, a.dprev, kc, kw, a.psb + kc, j0, width, i0, lrow, g,
-                                        lds);
+                                        lds, dscale);
             }
 #pragma unroll
             for (int m = 0; m < SLOTS; ++m) {
@@ -497,20 +507,22 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
         //     written to R: the next launch's GEMM applies the whole super-block)
         for (int sp = 0; sp < sub; ++sp)
             add_block_update<SLOTS>(st, a, a.dcur, (int64_t)sp * B, B, a.sb + (int64_t)sp * B, j0,
-                                    width, i0, lrow, g, lds);
+                                    width, i0, lrow, g, lds, dscale);
         // (3) the B column updates in order
         __syncthreads();
         stage_sigma_block<SLOTS>(a.Sigma, p, j0, width, j0, width, a.sig_vec4 != 0, sS);
         __syncthreads();
+        constexpr auto cols = std::make_integer_sequence<int, B>{};
         if (a.relax)
-            panel_run<SLOTS, false, true>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s,
-                                          z, a.maxq);
+            panel_run<SLOTS, false, true, false>(cols, st, sS, g, width, s, z, a.maxq);
+        else if (a.intd && width == B)
+            panel_run<SLOTS, true, false, true>(cols, st, sS, g, width, s, z, a.maxq);
+        else if (a.intd)
+            panel_run<SLOTS, false, false, true>(cols, st, sS, g, width, s, z, a.maxq);
         else if (width == B)
-            panel_run<SLOTS, true, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width, s,
-                                          z, a.maxq);
+            panel_run<SLOTS, true, false, false>(cols, st, sS, g, width, s, z, a.maxq);
         else
-            panel_run<SLOTS, false, false>(std::make_integer_sequence<int, B>{}, st, sS, g, width,
-                                           s, z, a.maxq);
+            panel_run<SLOTS, false, false, false>(cols, st, sS, g, width, s, z, a.maxq);
 #pragma unroll
         for (int m = 0; m < SLOTS; ++m) {
             const int c = 16 * m + g;
@@ -519,8 +531,12 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
                 d = st.v[m];
                 if (rowok && c < width) a.Wh[i * p + j0 + c] = st.w[m];
             } else {
-                // the same delta the column's step broadcast
-                d = c < width ? fmaf(s, st.k[m] - z, -st.w[m]) : 0.f;
+                // the same delta the column's step broadcast (as a code
+                // difference: the GEMM and the look-ahead scale it by s)
+                if (a.intd)
+                    d = c < width ? st.k[m] - st.v[m] : 0.f;
+                else
+                    d = c < width ? fmaf(s, st.k[m] - z, -st.w[m]) : 0.f;
                 if (rowok && c < width) {
                     a.Wh[i * p + j0 + c] = s * (st.k[m] - z);
                     a.codes[i * p + j0 + c] = (uint8_t)st.k[m];
@@ -552,13 +568,24 @@ __device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t
         nt_tile(A, row0, Bo, col0, a.psbw, lds, acc);
     } else {
         // split bf16 products (nt_x3.h); Delta rows are 16-byte aligned (stride S)
-        const X3Row A{a.dprev, a.S, a.q, a.psbw};
         const X3Row Bo{a.Sigma + a.psb, a.p, a.p, a.psbw};
         uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
-        if (a.sig_vec4 && row0 + kTile <= a.q && col0 + kTile <= a.p && a.psbw % (2 * kX3KC) == 0)
-            nt_tile_x3_full(A, row0, Bo, col0, a.psbw, l32, acc);
-        else
-            nt_tile_x3_edge(A, row0, Bo, col0, a.psbw, l32, acc);
+        const bool full =
+            a.sig_vec4 && row0 + kTile <= a.q && col0 + kTile <= a.p && a.psbw % (2 * kX3KC) == 0;
+        if (a.intd) {
+            // code differences are exact in bf16: three exact products with Sigma's planes
+            const X1Row A{{a.dprev, a.S, a.q, a.psbw}};
+            if (full)
+                nt_tile_x3_full<false, 3>(A, row0, Bo, col0, a.psbw, l32, acc);
+            else
+                nt_tile_x3_edge<3>(A, row0, Bo, col0, a.psbw, l32, acc);
+        } else {
+            const X3Row A{a.dprev, a.S, a.q, a.psbw};
+            if (full)
+                nt_tile_x3_full(A, row0, Bo, col0, a.psbw, l32, acc);
+            else
+                nt_tile_x3_edge(A, row0, Bo, col0, a.psbw, l32, acc);
+        }
     }
     // R's tile is fetched before the accumulators pass through LDS, which
     // hides part of its latency
@@ -566,7 +593,9 @@ __device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t
     tile_load_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv);
     acc_to_lds(acc, lds);                                // the K loop ended with a barrier
     __syncthreads();
-    tile_add_store_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv, lds, ex0, ex1);
+    // code differences: R += s_i (D Sigma)_i
+    tile_add_store_rm(a.R, a.p, a.q, a.p, row0, col0, a.r_vec4 != 0, rv, lds, ex0, ex1,
+                      a.intd ? a.scale : nullptr);
 }
 
 template <int SLOTS>
@@ -709,6 +738,13 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
         const int k = sw + 1;
         base.relax = (period > 0 && k % period == 0 && k != sweeps) ? 1 : 0;
         base.codes_valid = ((sw > 0 || codes_valid0) && !prev_relaxed) ? 1 : 0;
+        // A quantized sweep that starts with every What_ij on its grid level
+        // moves coordinates only between levels: delta = s_i (k_new - k_old).
+        // The deltas are then handed on as the code differences (exact small
+        // integers, a single bf16 plane) and the row's s_i is applied after
+        // the product: R += s_i (D Sigma).  R then follows the exact levels
+        // s (k - z) rather than their fp32 roundings.
+        base.intd = (base.codes_valid && !base.relax) ? 1 : 0;
         prev_relaxed = base.relax != 0;
         qe_status st;
         switch (B) {

@@ -105,6 +105,22 @@ struct X3Row {
     __device__ inline void store(uint32_t* op, const X3Stage& st) const { x3_store_row8(op, st); }
 };
 
+// Row-major operand whose values are exact in bf16 (e.g. small integers: the
+// code differences of the CD block update), staged as its h plane only; it
+// pairs with the three planes of the other operand (x3_mfma_stage<3>).
+struct X1Row : X3Row {
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        u32x4 h;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            h[u] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
+                (f32x2){st.v[u >> 1][2 * (u & 1)], st.v[u >> 1][2 * (u & 1) + 1]}, bf16x2));
+        *reinterpret_cast<u32x4*>(op + x3_addr(t >> 1, t & 1, 0)) = h;
+    }
+};
+
 // Row-major composite operand P1 + P2 - P3 (P2, P3 may be null), e.g.
 // What + H - W, staged as X3Row.
 struct X3Comp {
@@ -190,10 +206,15 @@ struct X3Col {
 
 // acc[mi][ni] += A(wave rows mi) B(wave cols ni)^T over one staged K = 16 of
 // the 128 x 128 tile: waves form a 2 x 2 grid, wave (wm, wn) owns rows
-// wm * 64 + 32 mi and columns wn * 64 + 32 ni (mi, ni < 2).
+// wm * 64 + 32 mi and columns wn * 64 + 32 ni (mi, ni < 2).  NP = 6: both
+// operands split in three (the six kept products); NP = 3: A exact in bf16
+// (its h plane only), B split in three, all three products exact.
+template <int NP = 6>
 __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t* sB,
                                               f32x16 (&acc)[2][2])
 {
+    static_assert(NP == 6 || NP == 3, "six or three products");
+    constexpr int NA = NP == 6 ? 3 : 1;
     const int lane = threadIdx.x & 63;
     const int wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -201,11 +222,13 @@ __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t
     // small terms first
     constexpr int PA[6] = {2, 1, 0, 1, 0, 0};
     constexpr int PB[6] = {0, 1, 2, 0, 1, 0};
-    bf16x8 a[2][3], b[2][3];
+    constexpr int QA[3] = {0, 0, 0};
+    constexpr int QB[3] = {2, 1, 0};
+    bf16x8 a[2][NA], b[2][3];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int pl = 0; pl < 3; ++pl)
+        for (int pl = 0; pl < NA; ++pl)
             a[i][pl] = __builtin_bit_cast(
                 bf16x8, *reinterpret_cast<const u32x4*>(sA + x3_addr(wm * 64 + i * 32 + r, half, pl)));
 #pragma unroll
@@ -216,13 +239,14 @@ __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t
                 bf16x8, *reinterpret_cast<const u32x4*>(sB + x3_addr(wn * 64 + i * 32 + r, half, pl)));
     // the four accumulators interleave so that no MFMA waits on the one just issued
 #pragma unroll
-    for (int q = 0; q < 6; ++q)
+    for (int q = 0; q < NP; ++q)
 #pragma unroll
         for (int mi = 0; mi < 2; ++mi)
 #pragma unroll
             for (int ni = 0; ni < 2; ++ni)
-                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[mi][PA[q]], b[ni][PB[q]],
-                                                                      acc[mi][ni], 0, 0, 0);
+                acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    a[mi][NP == 6 ? PA[q] : QA[q % 3] % NA], b[ni][NP == 6 ? PB[q] : QB[q % 3]],
+                    acc[mi][ni], 0, 0, 0);
 }
 
 // Instruction order of one stage when INTERLEAVE is set: the operand reads,
@@ -247,7 +271,7 @@ __device__ __forceinline__ void x3_interleave()
 // stage's LDS store leaves the next stage's loads in flight.  `lds` holds
 // kX3LdsDw dwords.  Ends with a barrier.  INTERLEAVE pays off in long K loops
 // (the Gram), not in the CD block update.
-template <bool INTERLEAVE = false, class OA, class OB>
+template <bool INTERLEAVE = false, int NP = 6, class OA, class OB>
 __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                        int64_t K, uint32_t* lds, f32x16 (&acc)[2][2])
 {
@@ -270,7 +294,7 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         A.load_full(row0a, (c + 2) * kX3KC, ra0);
         B.load_full(row0b, (c + 2) * kX3KC, rb0);
         __builtin_amdgcn_sched_barrier(0);
-        x3_mfma_stage(a0, b0, acc);
+        x3_mfma_stage<NP>(a0, b0, acc);
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a1, ra1);
         B.store(b1, rb1);
@@ -280,24 +304,24 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         A.load_full(row0a, (c + 3) * kX3KC, ra1);
         B.load_full(row0b, (c + 3) * kX3KC, rb1);
         __builtin_amdgcn_sched_barrier(0);
-        x3_mfma_stage(a1, b1, acc);
+        x3_mfma_stage<NP>(a1, b1, acc);
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a0, ra0);
         B.store(b0, rb0);
         if constexpr (INTERLEAVE) x3_interleave();
         __syncthreads();
     }
-    x3_mfma_stage(a0, b0, acc);
+    x3_mfma_stage<NP>(a0, b0, acc);
     A.store(a1, ra1);
     B.store(b1, rb1);
     __syncthreads();
-    x3_mfma_stage(a1, b1, acc);
+    x3_mfma_stage<NP>(a1, b1, acc);
     __syncthreads();
 }
 
 // Any shape: guarded loads (out-of-range elements read as 0), one stage of
 // prefetch.  Ends with a barrier.
-template <class OA, class OB>
+template <int NP = 6, class OA, class OB>
 __device__ __forceinline__ void nt_tile_x3_edge(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                        int64_t K, uint32_t* lds, f32x16 (&acc)[2][2])
 {
@@ -318,7 +342,7 @@ __device__ __forceinline__ void nt_tile_x3_edge(const OA& A, int64_t row0a, cons
             A.load(row0a, (c + 1) * kX3KC, sa);
             B.load(row0b, (c + 1) * kX3KC, sb);
         }
-        x3_mfma_stage(a0, b0, acc);
+        x3_mfma_stage<NP>(a0, b0, acc);
         if (more) {
             A.store(a1, sa);
             B.store(b1, sb);
@@ -330,7 +354,7 @@ __device__ __forceinline__ void nt_tile_x3_edge(const OA& A, int64_t row0a, cons
             A.load(row0a, (c + 2) * kX3KC, sa);
             B.load(row0b, (c + 2) * kX3KC, sb);
         }
-        x3_mfma_stage(a1, b1, acc);
+        x3_mfma_stage<NP>(a1, b1, acc);
         if (more) {
             A.store(a0, sa);
             B.store(b0, sb);

@@ -297,11 +297,14 @@ __device__ inline void tile_load_rm(const float* M, int64_t ld, int64_t rows, in
 }
 
 // Writes T + (the accumulator tile staged in LDS by acc_to_lds) to M, skipping
-// elements outside rows x cols and columns in [ex0, ex1).
+// elements outside rows x cols and columns in [ex0, ex1).  rowscale (nullable,
+// indexed by M's row) multiplies each accumulator row first, in one fused
+// multiply-add; without it the sum is T + acc.
 constexpr int kAccStride = kTile + 4;
 __device__ inline void tile_add_store_rm(float* M, int64_t ld, int64_t rows, int64_t cols,
                                          int64_t row0, int64_t col0, bool vec4, const TileRM& T,
-                                         const float* accLds, int64_t ex0 = 0, int64_t ex1 = 0)
+                                         const float* accLds, int64_t ex0 = 0, int64_t ex1 = 0,
+                                         const float* rowscale = nullptr)
 {
     const int t = threadIdx.x;
     const int lr = t >> 5, lc = 4 * (t & 31);
@@ -312,7 +315,15 @@ __device__ inline void tile_add_store_rm(float* M, int64_t ld, int64_t rows, int
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const f32x4 a = *reinterpret_cast<const f32x4*>(accLds + (lr + 8 * j) * kAccStride + lc);
-            *reinterpret_cast<f32x4*>(base + 8 * j * ld) = T.v[j] + a;
+            if (rowscale) {
+                const float sc = rowscale[r0 + 8 * j];
+                f32x4 o;
+#pragma unroll
+                for (int u = 0; u < 4; ++u) o[u] = fmaf(sc, a[u], T.v[j][u]);
+                *reinterpret_cast<f32x4*>(base + 8 * j * ld) = o;
+            } else {
+                *reinterpret_cast<f32x4*>(base + 8 * j * ld) = T.v[j] + a;
+            }
         }
         return;
     }
@@ -322,8 +333,10 @@ __device__ inline void tile_add_store_rm(float* M, int64_t ld, int64_t rows, int
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
             const int64_t c = c0 + u;
-            if (r < rows && c < cols && !(c >= ex0 && c < ex1))
-                M[r * ld + c] = T.v[j][u] + accLds[(lr + 8 * j) * kAccStride + lc + u];
+            if (r < rows && c < cols && !(c >= ex0 && c < ex1)) {
+                const float a = accLds[(lr + 8 * j) * kAccStride + lc + u];
+                M[r * ld + c] = rowscale ? fmaf(rowscale[r], a, T.v[j][u]) : T.v[j][u] + a;
+            }
         }
     }
 }
