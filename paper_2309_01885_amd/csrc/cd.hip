@@ -576,7 +576,7 @@ __device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t
             // code differences are exact in bf16: three exact products with Sigma's planes
             const X1Row A{{a.dprev, a.S, a.q, a.psbw}};
             if (full)
-                nt_tile_x3_full<false, 3>(A, row0, Bo, col0, a.psbw, l32, acc);
+                nt_tile_x3_full<true, 3>(A, row0, Bo, col0, a.psbw, l32, acc);
             else
                 nt_tile_x3_edge<3>(A, row0, Bo, col0, a.psbw, l32, acc);
         } else {

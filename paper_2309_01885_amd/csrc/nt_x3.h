@@ -253,15 +253,20 @@ __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t
 // then the MFMAs, each followed by a few VALU instructions of the next stage's
 // split, then the LDS writes, so that the split runs while the matrix cores
 // work.
+template <int NP = 6>
 __device__ __forceinline__ void x3_interleave()
 {
-    __builtin_amdgcn_sched_group_barrier(0x100, 12, 0);            // DS reads
+    // operand reads: A's planes (three, or one with NP = 3) and B's three, per
+    // 32-row block; MFMAs 4 NP; LDS writes of the next stage: one or three
+    // planes of A, three of B
+    constexpr int reads = NP == 6 ? 12 : 8, writes = NP == 6 ? 6 : 4;
+    __builtin_amdgcn_sched_group_barrier(0x100, reads, 0);         // DS reads
 #pragma unroll
-    for (int i = 0; i < 24; ++i) {
+    for (int i = 0; i < 4 * NP; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);         // MFMA
         __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);         // VALU
     }
-    __builtin_amdgcn_sched_group_barrier(0x200, 6, 0);             // DS writes
+    __builtin_amdgcn_sched_group_barrier(0x200, writes, 0);        // DS writes
 }
 
 // acc += A[row0a.., 0..K) B[row0b.., 0..K)^T on the 128 x 128 tile of 256
@@ -298,7 +303,7 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a1, ra1);
         B.store(b1, rb1);
-        if constexpr (INTERLEAVE) x3_interleave();
+        if constexpr (INTERLEAVE) x3_interleave<NP>();
         __syncthreads();
         // LDS 1: stage c + 1; registers 0: stage c + 2; registers 1 take stage c + 3
         A.load_full(row0a, (c + 3) * kX3KC, ra1);
@@ -308,7 +313,7 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a0, ra0);
         B.store(b0, rb0);
-        if constexpr (INTERLEAVE) x3_interleave();
+        if constexpr (INTERLEAVE) x3_interleave<NP>();
         __syncthreads();
     }
     x3_mfma_stage<NP>(a0, b0, acc);
