@@ -348,6 +348,29 @@ def main():
                        {"avg_launch_s": cd_avg, "launches_per_sweep": nb + 1})
     roof_gram = roofline("gram_x3w_kernel", float(p) * (p + 1) * n, gram_t, {"call_s": gram_t})
 
+    # the Gram from token-major activations (n x p, as a model produces them),
+    # in one call and streamed in 32768-token chunks accumulated into Sigma
+    XT = X.t().contiguous()
+    S_np = torch.empty_like(Sigma)
+    ws_np = P.workspace(max(P.load().qe_gram_workspace_size(p, n),
+                            P.load().qe_gram_workspace_size(p, 32768)), dev)
+    tm = {}
+    for label, chunk in (("one_call_s", n), ("chunks_32768_s", 32768)):
+        times = []
+        for rep in range(3):
+            g0, g1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            g0.record(stream)
+            for c0 in range(0, n, chunk):
+                P.gram(XT[c0:c0 + chunk], layout=P.QE_LAYOUT_NP, Sigma=S_np, accumulate=c0 > 0,
+                       damp=spec.damp if c0 + chunk >= n else 0.0, ws=ws_np, check=False)
+            g1.record(stream)
+            torch.cuda.synchronize()
+            times.append(g0.elapsed_time(g1) * 1e-3)
+        tm[label] = float(np.median(times))
+    assert P.sync_status(ws_np) == 0
+    del XT, S_np, ws_np
+    torch.cuda.empty_cache()
+
     # the column-sequential panel: a panel-only launch (256 columns x q rows)
     # moves 17 bytes per coordinate (R, What in; What, code, delta out)
     panel = None
@@ -390,6 +413,7 @@ def main():
         "objective_per_sweep": [float(x) for x in f_sweeps],
         "rel_calibration_error": float(exact[0] / exact[1]),
         "parity": parity_record(),
+        "gram_token_major": tm,
     }
 
     if not args.no_outlier:

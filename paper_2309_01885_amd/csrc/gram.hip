@@ -238,8 +238,9 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
 // matrix-core work of the 128 x 128 tile (half the split work, LDS traffic
 // and L2 traffic per product), with the operand reads pipelined through three
 // LDS stage buffers (nt_tile_x3_wide).  Used when every 256-row panel lies
-// inside X (p a multiple of 256, aligned rows, token ranges multiples of 32,
-// p x n layout).  Each wave's 64 x 128 block lies in one 128 x 128 tile of the
+// inside X (p a multiple of 256, aligned rows, token ranges multiples of 32),
+// in either layout (channel-major rows through X3Row, token-major through
+// X3ColW).  Each wave's 64 x 128 block lies in one 128 x 128 tile of the
 // upper triangle, so the partials use the same slots as gram_x3_kernel and
 // the same finalize.
 constexpr int kWide = 256;
@@ -271,7 +272,7 @@ __device__ inline void band_index_wide(int64_t t, int64_t nt, int64_t& ti, int64
 // LDS-transposed symmetric writes as the two-level mode, 128 x 128 quadrant
 // by quadrant; the large-p replacement of the two-level mode for streamed
 // token chunks.
-template <bool DIRECT>
+template <bool DIRECT, bool TRANS>
 __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
     const float* __restrict__ X, int64_t p, int64_t n, int64_t ntw, int64_t tiles_w, int64_t nt,
     int64_t tiles, int64_t splits, int64_t split_len, float* __restrict__ out, int accumulate,
@@ -295,8 +296,14 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
         for (int ni = 0; ni < 4; ++ni)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
-    const X3Row op{X + k0, n, 0, K};
-    nt_tile_x3_wide(op, ti * kWide, op, tj * kWide, K, lds, acc);
+    if constexpr (TRANS) {
+        // X is n x p: element (channel r, token k) at X[k * p + r]
+        const X3ColW op{X + k0 * p, p, 0, K};
+        nt_tile_x3_wide(op, ti * kWide, op, tj * kWide, K, lds, acc);
+    } else {
+        const X3Row op{X + k0, n, 0, K};
+        nt_tile_x3_wide(op, ti * kWide, op, tj * kWide, K, lds, acc);
+    }
     // wave (wm, wn): rows 64 wm .. of the tile, columns 128 wn ..
     const int wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -433,7 +440,7 @@ static int64_t gram_splits(int64_t p, int64_t n)
     return best;
 }
 
-size_t gram_ws_bytes(int64_t p, int64_t n)
+static size_t gram_ws_one(int64_t p, int64_t n)
 {
     const int64_t nt = cdiv(p, kTile);
     const int64_t tiles = nt * (nt + 1) / 2;
@@ -441,8 +448,38 @@ size_t gram_ws_bytes(int64_t p, int64_t n)
     return kStatusBytes + align256((size_t)splits * tiles * kTileFloats * sizeof(float));
 }
 
+// Token-major X with a token count that is not a multiple of 32 is taken as
+// an aligned part on the 256 x 256 tiles and a short tail (launch_gram).
+constexpr int64_t kTokAlign = 2 * kX3KC;
+
+size_t gram_ws_bytes(int64_t p, int64_t n)
+{
+    size_t b = gram_ws_one(p, n);
+    if (n > kTokAlign && n % kTokAlign != 0)
+        b = std::max(b, std::max(gram_ws_one(p, n - n % kTokAlign), gram_ws_one(p, n % kTokAlign)));
+    return b;
+}
+
+static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layout, float* Sigma,
+                                 int accumulate, float damp, void* ws, hipStream_t s);
+
 qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma,
                       int accumulate, float damp, void* ws, hipStream_t s)
+{
+    const bool trans = (layout & ~QE_GRAM_FP32) == QE_LAYOUT_NP;
+    if (trans && !(layout & QE_GRAM_FP32) && p % kWide == 0 && n > kTokAlign &&
+        n % kTokAlign != 0) {
+        // token rows are contiguous: the tail is X's last n % 32 token rows
+        const int64_t tail = n % kTokAlign, main = n - tail;
+        const qe_status st = launch_gram_one(X, p, main, layout, Sigma, accumulate, 0.f, ws, s);
+        if (st != QE_OK) return st;
+        return launch_gram_one(X + main * p, p, tail, layout, Sigma, 1, damp, ws, s);
+    }
+    return launch_gram_one(X, p, n, layout, Sigma, accumulate, damp, ws, s);
+}
+
+static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layout, float* Sigma,
+                                 int accumulate, float damp, void* ws, hipStream_t s)
 {
     int* status = static_cast<int*>(ws);
     const int64_t nt = cdiv(p, kTile);
@@ -482,16 +519,18 @@ qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* S
     hipLaunchKernelGGL((gram_x3_kernel<T, L, F>), dim3(grid), dim3(256), 0, s, X, p, n, nt, tiles, \
                        used, split_len, dst, accumulate, status)
         const bool two = splits == 0;
-        if (full && !trans && p % kWide == 0 && (!two || n <= kSplitTokensMax)) {
+        if (full && p % kWide == 0 && (!two || n <= kSplitTokensMax)) {
             const int64_t ntw = p / kWide;
             const int64_t tiles_w = ntw * (ntw + 1) / 2;
             const dim3 grid((unsigned)(8 * cdiv(tiles_w * used, 8)));
-            if (two)
-                hipLaunchKernelGGL(gram_x3w_kernel<true>, grid, dim3(512), 0, s, X, p, n, ntw,
-                                   tiles_w, nt, tiles, (int64_t)1, n, Sigma, accumulate, status);
-            else
-                hipLaunchKernelGGL(gram_x3w_kernel<false>, grid, dim3(512), 0, s, X, p, n, ntw,
-                                   tiles_w, nt, tiles, used, split_len, parts, accumulate, status);
+#define QE_GRAM_X3W(D, T, SPLITS, LEN, OUT)                                                    \
+    hipLaunchKernelGGL((gram_x3w_kernel<D, T>), grid, dim3(512), 0, s, X, p, n, ntw, tiles_w, nt, \
+                       tiles, SPLITS, LEN, OUT, accumulate, status)
+            if (two && trans) QE_GRAM_X3W(true, true, (int64_t)1, n, Sigma);
+            else if (two) QE_GRAM_X3W(true, false, (int64_t)1, n, Sigma);
+            else if (trans) QE_GRAM_X3W(false, true, used, split_len, parts);
+            else QE_GRAM_X3W(false, false, used, split_len, parts);
+#undef QE_GRAM_X3W
         } else if (trans) {
             if (two) { if (full) QE_GRAM_X3(true, true, true); else QE_GRAM_X3(true, true, false); }
             else { if (full) QE_GRAM_X3(true, false, true); else QE_GRAM_X3(true, false, false); }

@@ -204,6 +204,41 @@ struct X3Col {
     }
 };
 
+// Transposed operand for the 512-thread 256 x 256 tile: thread t stages rows
+// 2 (t % 128) and 2 (t % 128) + 1, k = 4 (t / 128) .. +3, so that the 128
+// threads of a k group read 1024 contiguous bytes per k.
+struct X3ColW {
+    const float* base;
+    int64_t ld, rows, kvalid;
+    // whole stage inside the matrix, 8-byte aligned row pairs
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const float* src = base + (k0 + 4 * (t >> 7)) * ld + row0 + 2 * (t & 127);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const f32x2 v = *reinterpret_cast<const f32x2*>(src + u * ld);
+            st.v[0][u] = v[0];
+            st.v[1][u] = v[1];
+        }
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int kq = t >> 7;                   // k = 4 kq .. 4 kq + 3: half kq / 2
+#pragma unroll
+        for (int e = 0; e < 2; ++e) {
+            const int row = 2 * (t & 127) + e;
+            const X3Pair q0 = split3(st.v[e][0], st.v[e][1]);
+            const X3Pair q1 = split3(st.v[e][2], st.v[e][3]);
+            const int o = x3_addr(row, kq >> 1, 0) + 2 * (kq & 1);
+            *reinterpret_cast<u32x2*>(op + o) = u32x2{q0.h, q1.h};
+            *reinterpret_cast<u32x2*>(op + o + 8) = u32x2{q0.m, q1.m};
+            *reinterpret_cast<u32x2*>(op + o + 16) = u32x2{q0.l, q1.l};
+        }
+    }
+};
+
 // acc[mi][ni] += A(wave rows mi) B(wave cols ni)^T over one staged K = 16 of
 // the 128 x 128 tile: waves form a 2 x 2 grid, wave (wm, wn) owns rows
 // wm * 64 + 32 mi and columns wn * 64 + 32 ni (mi, ni < 2).  NP = 6: both

@@ -36,8 +36,10 @@ def test_gram_matches_oracle(qe, oracle, p, n, fp32):
 
 
 @pytest.mark.parametrize("fp32", [False, True])
-@pytest.mark.parametrize("p,n", [(256, 1024), (130, 77), (384, 96)])
+@pytest.mark.parametrize("p,n", [(256, 1024), (130, 77), (384, 96), (512, 2048 + 17), (256, 31)])
 def test_gram_token_major_layout(qe, oracle, p, n, fp32):
+    """(256, 1024) takes the 256 x 256 tiles; (512, 2065) an aligned part on
+    them plus a 17-token tail; the others the 128 x 128 tiles."""
     X = synth.gaussian((p, n), seed=3)
     S_pn = _gram(qe, X, 0, fp32=fp32)
     S_np = _gram(qe, np.ascontiguousarray(X.T), 1, fp32=fp32)

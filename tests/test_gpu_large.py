@@ -7,7 +7,8 @@ The MLP up-projection (11008 x 4096) draws the very same X, so both layers
 share Sigma.
 
 * Gram: the whole 4096 x 4096 Sigma against the oracle's fp64 Gram of all
-  262144 tokens (relative Frobenius <= 1e-5), exactly symmetric.
+  262144 tokens (relative Frobenius <= 1e-5), exactly symmetric -- from the
+  channel-major X in one call, and from the token-major X streamed in chunks.
 * CD on all rows of each layer, Sigma = the oracle's damped Gram of all
   262144 tokens cast to fp32 (Lemma 1: Sigma = X X^T over the calibration
   set); the oracle replays seeded row samples (512 rows of the attention
@@ -42,14 +43,49 @@ def c2_sigma64(c2_x, oracle):
 @pytest.mark.timeout(900)
 def test_gram_full_size_full_matrix(qe, c2_x, c2_sigma64):
     Xd = dev(c2_x)
-    S = host(qe.gram(Xd))
-    del Xd
+    qe.gram(Xd)                              # code objects loaded
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    Sd = qe.gram(Xd, check=False)
+    ev[1].record()
+    torch.cuda.synchronize()
+    print(f"[c2] channel-major Gram: {ev[0].elapsed_time(ev[1]):.2f} ms", flush=True)
+    S = host(Sd)
+    del Xd, Sd
     torch.cuda.empty_cache()
     assert np.array_equal(S, S.T)
     err = rel_fro(S, c2_sigma64)
     print(f"[c2] Gram relative Frobenius error {err:.3e}", flush=True)
     assert err <= 1e-5
     # the diagonal (the CD step's divisors) entry by entry
+    d, dref = np.diag(S).astype(np.float64), np.diag(c2_sigma64)
+    assert np.max(np.abs(d - dref) / dref) <= 1e-5
+
+
+@pytest.mark.timeout(900)
+def test_gram_token_major_streamed_full_size(qe, c2_x, c2_sigma64):
+    """Sec. 3.2 "Memory Footprint" (Sigma does not grow with n) and the
+    calibration set of Sec. 5: the same 262144 tokens handed over token-major
+    (n x p, the layout a model's activations come in) in chunks accumulated
+    into Sigma, the first chunk ragged (30000 tokens, not a multiple of 32).
+    The whole 4096 x 4096 Sigma against the oracle's fp64 Gram."""
+    p, n = c2_x.shape
+    cuts = [0, 30000] + list(range(30000 + 32768, n, 32768)) + [n]
+    Sigma = torch.empty((p, p), dtype=torch.float32, device="cuda")
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    t = 0.0
+    for c, (a, b) in enumerate(zip(cuts[:-1], cuts[1:])):
+        chunk = dev(np.ascontiguousarray(c2_x[:, a:b].T))
+        ev[0].record()
+        qe.gram(chunk, layout=qe.QE_LAYOUT_NP, Sigma=Sigma, accumulate=c > 0)
+        ev[1].record()
+        torch.cuda.synchronize()
+        t += ev[0].elapsed_time(ev[1]) * 1e-3
+        del chunk
+    S = host(Sigma)
+    print(f"[c2] token-major Gram in {len(cuts) - 1} chunks: {t * 1e3:.2f} ms", flush=True)
+    assert np.array_equal(S, S.T)
+    assert rel_fro(S, c2_sigma64) <= 1e-5
     d, dref = np.diag(S).astype(np.float64), np.diag(c2_sigma64)
     assert np.max(np.abs(d - dref) / dref) <= 1e-5
 
