@@ -257,10 +257,16 @@ qe_status qe_objective(const float* W, const float* W_hat, const float* H, const
 
 /* ------------------------------------------------------------------------
  * lambda_max(Sigma) by the power method (Sec. 4.3: matrix-vector products
- * only, O(p^2) per iteration).  Start vector 1/sqrt(p); the estimate is the
- * Rayleigh quotient; the result is that of the first iteration whose quotient
- * changed by at most tol (relative) from the previous one, else of iteration
- * max_iters.  Synchronises `stream` every 32 iterations.
+ * only, O(p^2) per iteration), returned as an upper bound, since the IHT step
+ * 1 / (2 lambda) of Lemma 3 needs lambda >= lambda_max.  Start vector
+ * 1/sqrt(p); iterate v_k = S v_{k-1} / |S v_{k-1}|, quotient
+ * rho_k = v_k' S v_k / v_k' v_k.  The iteration used is the first whose
+ * quotient changed by at most tol (relative) from the previous one, else
+ * iteration max_iters; the result is rho + |S v - rho v| / |v| of that
+ * iteration (an eigenvalue lies within that radius of rho; v approximates the
+ * leading eigenvector), from fp64 sums, widened by a relative 2^-30 and
+ * rounded up to fp32.
+ * Synchronises `stream` every 32 iterations.
  * lambda_out: HOST float.
  * ------------------------------------------------------------------------ */
 size_t qe_lambda_workspace_size(int64_t p);

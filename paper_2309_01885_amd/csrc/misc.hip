@@ -1,4 +1,7 @@
 // Grid, exact objective and lambda_max kernels (gfx950).
+#include <algorithm>
+#include <cmath>
+
 #include "nt_x3.h"
 #include "qe_internal.h"
 
@@ -281,18 +284,32 @@ qe_status launch_objective(const float* W, const float* Wh, const float* H, cons
 constexpr int kSymvRows = 8;
 constexpr int kLambdaCheck = 32;   // iterations per host check (the stop is still per iteration)
 
-__device__ inline void sum_pair_partials(const double* part, int n, double* sh, double& yy,
-                                         double& vy)
+// Sums the per-workgroup partials (|Sv|^2, v'Sv, |v|^2) of one iteration.
+__device__ inline void sum_partials3(const double* part, int n, double* sh, double& yy,
+                                     double& vy, double& vv)
 {
-    double a = 0.0, b = 0.0;
+    double a = 0.0, b = 0.0, c = 0.0;
     for (int e = threadIdx.x; e < n; e += blockDim.x) {
-        a += part[2 * e];
-        b += part[2 * e + 1];
+        a += part[3 * e];
+        b += part[3 * e + 1];
+        c += part[3 * e + 2];
     }
     yy = block_sum_f64(a, sh);
     vy = block_sum_f64(b, sh);
+    vv = block_sum_f64(c, sh);
 }
 
+// Quotient rho = v'Sv / v'v and squared inclusion radius |Sv - rho v|^2 / |v|^2
+// (= (|Sv|^2 - (v'Sv)^2 / v'v) / v'v) of one iteration, into lam_hist.
+__device__ inline void put_hist(double* lam_hist, int slot, double yy, double vy, double vv)
+{
+    lam_hist[2 * slot] = vv > 0.0 ? vy / vv : 0.0;
+    lam_hist[2 * slot + 1] = vv > 0.0 ? fmax(0.0, yy - vy * vy / vv) / vv : 0.0;
+}
+
+// One power iteration y = Sigma v with v = yprev / |S v_prev| (the first: all
+// ones / sqrt(p)); the products and the partial sums are fp64, y is stored in
+// fp32 for the next iteration.
 __global__ __launch_bounds__(256) void power_step_kernel(const float* __restrict__ Sigma,
                                                          int64_t p, const float* __restrict__ yprev,
                                                          const double* __restrict__ pprev,
@@ -300,17 +317,17 @@ __global__ __launch_bounds__(256) void power_step_kernel(const float* __restrict
                                                          double* part, double* lam_hist, int slot)
 {
     __shared__ double sh[256];
-    __shared__ double wpart[4][2];
+    __shared__ double wpart[4][3];
     const int nwg = (int)gridDim.x;
     // v_k = yprev * inv (the first iteration: yprev taken as all ones)
     double inv;
     if (first) {
         inv = 1.0 / sqrt((double)p);
     } else {
-        double yy, vy;
-        sum_pair_partials(pprev, nwg, sh, yy, vy);
+        double yy, vy, vv;
+        sum_partials3(pprev, nwg, sh, yy, vy, vv);
         inv = yy > 0.0 ? 1.0 / sqrt(yy) : 0.0;
-        if (blockIdx.x == 0 && threadIdx.x == 0 && slot > 0) lam_hist[slot - 1] = vy;
+        if (blockIdx.x == 0 && threadIdx.x == 0 && slot > 0) put_hist(lam_hist, slot - 1, yy, vy, vv);
     }
     auto wj = [&](int64_t j) -> float { return first ? 1.f : yprev[j]; };
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -347,43 +364,47 @@ __global__ __launch_bounds__(256) void power_step_kernel(const float* __restrict
 #pragma unroll
         for (int rr = 0; rr < RW; ++rr) acc[rr] += (double)srow[rr][j] * wv;
     }
-    double pyy = 0.0, pvy = 0.0;
+    double pyy = 0.0, pvy = 0.0, pvv = 0.0;
 #pragma unroll
     for (int rr = 0; rr < RW; ++rr) {
         double a = acc[rr];
         for (int off = 32; off > 0; off >>= 1) a += __shfl_xor(a, off, 64);
         if (!ok[rr]) continue;
-        const float yr = (float)(a * inv);
-        if (lane == 0) y[r0 + rr] = yr;
-        pyy += (double)yr * (double)yr;
-        pvy += (double)wj(r0 + rr) * inv * (double)yr;
+        const double yd = a * inv;               // (S v)_r in fp64
+        if (lane == 0) y[r0 + rr] = (float)yd;
+        const double vr = (double)wj(r0 + rr) * inv;
+        pyy += yd * yd;
+        pvy += vr * yd;
+        pvv += vr * vr;
     }
     if (lane == 0) {
         wpart[wave][0] = pyy;
         wpart[wave][1] = pvy;
+        wpart[wave][2] = pvv;
     }
     __syncthreads();
     if (threadIdx.x == 0) {
-        part[2 * blockIdx.x] = ((wpart[0][0] + wpart[1][0]) + wpart[2][0]) + wpart[3][0];
-        part[2 * blockIdx.x + 1] = ((wpart[0][1] + wpart[1][1]) + wpart[2][1]) + wpart[3][1];
+#pragma unroll
+        for (int c = 0; c < 3; ++c)
+            part[3 * blockIdx.x + c] = ((wpart[0][c] + wpart[1][c]) + wpart[2][c]) + wpart[3][c];
     }
 }
 
-// lambda of the last iteration of a batch.
+// Quotient and radius of the last iteration of a batch.
 __global__ __launch_bounds__(256) void power_last_kernel(const double* part, int nwg,
                                                          double* lam_hist, int slot)
 {
     __shared__ double sh[256];
-    double yy, vy;
-    sum_pair_partials(part, nwg, sh, yy, vy);
-    if (threadIdx.x == 0) lam_hist[slot] = vy;
+    double yy, vy, vv;
+    sum_partials3(part, nwg, sh, yy, vy, vv);
+    if (threadIdx.x == 0) put_hist(lam_hist, slot, yy, vy, vv);
 }
 
 size_t lambda_ws_bytes(int64_t p)
 {
     const int64_t nwg = cdiv(p, kSymvRows);
     return kStatusBytes + 2 * align256(sizeof(float) * p) +
-           2 * align256(sizeof(double) * 2 * nwg) + align256(sizeof(double) * kLambdaCheck);
+           2 * align256(sizeof(double) * 3 * nwg) + align256(sizeof(double) * 2 * kLambdaCheck);
 }
 
 qe_status launch_lambda(const float* Sigma, int64_t p, int max_iters, float tol, float* out,
@@ -392,10 +413,10 @@ qe_status launch_lambda(const float* Sigma, int64_t p, int max_iters, float tol,
     Ws w(ws);
     const int64_t nwg = cdiv(p, kSymvRows);
     float* y[2] = {w.take<float>(p), w.take<float>(p)};
-    double* part[2] = {w.take<double>(2 * nwg), w.take<double>(2 * nwg)};
-    double* hist = w.take<double>(kLambdaCheck);
+    double* part[2] = {w.take<double>(3 * nwg), w.take<double>(3 * nwg)};
+    double* hist = w.take<double>(2 * kLambdaCheck);      // (rho, radius^2) per iteration
     const int vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
-    double last = 0.0, prev = 0.0;
+    double last = 0.0, prev = 0.0, last_r2 = 0.0;
     int it = 0, cur = 0;
     while (it < max_iters) {
         const int batch = std::min(kLambdaCheck, max_iters - it);
@@ -410,20 +431,31 @@ qe_status launch_lambda(const float* Sigma, int64_t p, int max_iters, float tol,
                            batch - 1);
         it += batch;
         if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
-        double h[kLambdaCheck];
-        if (hipMemcpyAsync(h, hist, sizeof(double) * batch, hipMemcpyDeviceToHost, s) != hipSuccess)
+        double h[2 * kLambdaCheck];
+        if (hipMemcpyAsync(h, hist, sizeof(double) * 2 * batch, hipMemcpyDeviceToHost, s) !=
+            hipSuccess)
             return QE_ERR_HIP;
         if (hipStreamSynchronize(s) != hipSuccess) return QE_ERR_HIP;
         // the first iteration of the batch whose quotient moved by <= tol relative
         bool done = false;
         for (int b = 0; b < batch && !done; ++b) {
             prev = last;
-            last = h[b];
+            last = h[2 * b];
+            last_r2 = h[2 * b + 1];
             done = it - batch + b > 0 && last > 0.0 && fabs(last - prev) <= (double)tol * last;
         }
         if (done) break;
     }
-    *out = (float)last;
+    // Upper bound: for v and rho = v'Sv / v'v some eigenvalue of the symmetric
+    // Sigma lies within |Sv - rho v| / |v| of rho, and v approximates the
+    // leading eigenvector, so rho plus that radius bounds lambda_max from
+    // above.  Both come from fp64 sums of the fp64 product S v; a relative
+    // 2^-30 covers their rounding, and the result is rounded up to fp32.  The
+    // IHT step 1 / (2 lambda) then stays within the Lipschitz bound of Lemma 3.
+    const double bound = (last + sqrt(last_r2)) * (1.0 + 0x1p-30);
+    float f = (float)bound;
+    if ((double)f < bound) f = std::nextafter(f, INFINITY);
+    *out = f;
     return QE_OK;
 }
 

@@ -31,39 +31,49 @@ def test_topk_identical_support(qe, oracle, shape, s):
 
 
 def test_lambda_max(qe, oracle):
+    """An upper bound of the largest eigenvalue (Lemma 3 needs the step
+    1/(2 lambda) with lambda >= lambda_max), tight to 1e-3."""
     X = synth.correlated_activations(300, 2000, 0.9, 3, out_channels=6, out_mult=20.0)
-    S = oracle.damp(oracle.gram(X), 0.01)
-    lam = qe.lambda_max(dev(S.astype(np.float32)))
-    assert lam == pytest.approx(oracle.lambda_max(S), rel=1e-5)
+    S = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    lam = qe.lambda_max(dev(S))
+    ref = oracle.lambda_max(S)
+    assert ref <= lam <= ref * (1 + 1e-3)
 
 
 def _power_method(S, max_iters, tol):
     """The stop rule of qe_lambda_max in fp64: Rayleigh quotients of the unit
     iterates from 1/sqrt(p); the first one within tol (relative) of its
-    predecessor, else the last."""
+    predecessor, else the last; returned with its residual norm."""
     S = np.asarray(S, np.float64)
     v = np.full(S.shape[0], 1.0 / np.sqrt(S.shape[0]))
     prev = None
     for _ in range(max_iters):
         y = S @ v
         lam = float(v @ y)
+        res = float(np.linalg.norm(y - lam * v))
         if prev is not None and abs(lam - prev) <= tol * lam:
-            return lam
+            return lam, res
         prev = lam
         v = y / np.linalg.norm(y)
-    return lam
+    return lam, res
 
 
 @pytest.mark.parametrize("max_iters,tol", [(1, 1e-7), (3, 1e-7), (40, 1e-7), (500, 1e-2),
                                            (500, 1e-4)])
 def test_lambda_max_stop_rule(qe, max_iters, tol):
     """Iteration counts and tolerances that stop inside, at the end of and
-    across the 32-iteration host checks give the quotient of the same
-    iteration as an fp64 power method with the same rule."""
+    across the 32-iteration host checks give the bound (quotient plus
+    residual norm) of the same iteration as an fp64 power method with the
+    same rule; once the iterates have converged, never less than the largest
+    eigenvalue (early iterates bound some eigenvalue, not necessarily it)."""
     X = synth.correlated_activations(300, 2000, 0.9, 4, out_channels=6, out_mult=20.0)
     S = (X.astype(np.float64) @ X.T.astype(np.float64)).astype(np.float32)
     lam = qe.lambda_max(dev(S), max_iters=max_iters, tol=tol)
-    assert lam == pytest.approx(_power_method(S, max_iters, tol), rel=2e-6)
+    rho, res = _power_method(S, max_iters, tol)
+    assert lam == pytest.approx(rho + res, rel=2e-6)
+    if max_iters >= 40:
+        # converged iterates: the eigenvalue within the radius is the largest
+        assert lam >= np.linalg.eigvalsh(S.astype(np.float64))[-1]
 
 
 def run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, sweeps, H0, sup0, n0, block=0,
@@ -213,3 +223,22 @@ def test_outlier_debug_checks_scan_h(qe, oracle):
         qe.cd_outlier_sweep(Wd, Sd, bits, dev(scale), dev(zero), Wh, codes, dev(Hh), E, s, lam,
                             sup, nnz, 2, flags=qe.QE_INIT_FROM_W | qe.QE_DEBUG_CHECKS)
     assert e.value.code == qe.QE_ERR_NONFINITE
+
+
+def test_lemma3_descent_with_the_library_lambda(qe, oracle):
+    """The whole outlier-aware run with the step size from qe_lambda_max:
+    every IHT step keeps g from increasing (Lemma 3)."""
+    q, p, bits, s, iters = 96, 256, 3, 300, 5
+    W = synth.gaussian((q, p), seed=51, std=0.02)
+    W.reshape(-1)[::41] *= 8.0
+    X = synth.correlated_activations(p, 2048, 0.9, 52, out_channels=5, out_mult=20.0)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    lam = qe.lambda_max(dev(S32))
+    assert lam >= oracle.lambda_max(S32)
+    H0, sup0, n0 = qe.topk_abs(dev(W), s)
+    scale, zero = oracle.grid_minmax(W, bits, host(H0))
+    g = run_outlier_gpu(qe, W, S32, bits, scale, zero, s, lam, iters, H0, sup0, n0)["obj"]
+    for k in range(iters):
+        assert g[2 * k + 1] <= g[2 * k] * (1 + 1e-6), f"IHT step {k + 1}"
+        if k:
+            assert g[2 * k] <= g[2 * k - 1] * (1 + 1e-6), f"CD step {k + 1}"
