@@ -341,6 +341,7 @@ __device__ __forceinline__ void stage_sigma_block(const float* __restrict__ Sigm
 // of 16 (lane half h covers k = 4h .. 4h+3), which leaves the sum unchanged.
 // The 16 x B result passes through LDS into the panel's register layout.
 // B < 64: a VALU loop over k with Sigma staged in the panel layout.
+
 constexpr int kTStride = 128 + 4;   // transposed-Sigma LDS row stride (floats)
 
 template <int SLOTS>
@@ -445,6 +446,120 @@ __device__ __forceinline__ void add_block_update(PanelState<SLOTS>& st, const St
     }
 }
 
+// Look-ahead of a super-block: R_{I,SB(t)} += dscale_i D_{I,SB(t-1)} Sigma_{SB(t-1),SB(t)}
+// for the workgroup's 16 rows I, before its panels start (D: the deltas of the
+// previous super-block, q x S; dscale: the row's grid step when D holds code
+// differences, else 1).  One 16 x 256 x 256 product on the fp32 matrix cores
+// (v_mfma_f32_16x16x4f32; wave w owns output columns [64 w, 64 w + 64)), with
+// Sigma's block staged through LDS in K chunks of 64 -- read as rows of the
+// current super-block, the same numbers by symmetry, transposed so that k is
+// contiguous -- and the next chunk (Sigma and the delta fragments) loaded into
+// registers while the current chunk's matrix-core work runs.  The result is
+// added to R in the panel's own lane layout (lane g of row lrow: columns
+// 16 m + g), so that the panels' later loads of R are the same lanes' reads
+// of their own writes.
+constexpr int kLaK = 64;                  // K per staged chunk
+constexpr int kLaStride = kLaK + 4;       // LDS row stride (floats) of a staged chunk
+constexpr int kLaCols = 256;              // super-block columns covered
+constexpr int kLaUStride = kLaCols + 4;   // LDS row stride of the 16 x 256 result
+
+template <bool FULL>
+__device__ __forceinline__ void la_fetch(const StepArgs& a, int64_t i0, int kc, f32x4 (&v)[16],
+                                         f32x4 (&av)[4])
+{
+    const int lane = threadIdx.x & 63;
+    const int r = lane & 15, h = lane >> 4;
+#pragma unroll
+    for (int u = 0; u < 16; ++u) {
+        const int f = threadIdx.x + 256 * u;
+        const int c = f >> 4, kq = f & 15;
+        const int64_t base = (a.sb + c) * a.p + a.psb + kc + 4 * kq;
+        if constexpr (FULL) {
+            v[u] = *reinterpret_cast<const f32x4*>(a.Sigma + base);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                v[u][e] = (c < a.sbw && kc + 4 * kq + e < a.psbw) ? a.Sigma[base + e] : 0.f;
+        }
+    }
+    const int64_t ia = i0 + r;
+#pragma unroll
+    for (int kg = 0; kg < 4; ++kg) {
+        const int k = kc + 16 * kg + 4 * h;
+        if constexpr (FULL) {
+            av[kg] = *reinterpret_cast<const f32x4*>(a.dprev + ia * a.S + k);
+        } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                av[kg][e] = (ia < a.q && k + e < a.psbw) ? a.dprev[ia * a.S + k + e] : 0.f;
+        }
+    }
+}
+
+template <bool FULL>
+__device__ __forceinline__ void lookahead_k(const StepArgs& a, float* lds, int64_t i0,
+                                            f32x4 (&acc)[4])
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, h = lane >> 4;
+    f32x4 v[16], av[4], avn[4];
+    la_fetch<FULL>(a, i0, 0, v, avn);
+    for (int kc = 0; kc < a.psbw; kc += kLaK) {
+        __syncthreads();                         // the previous chunk's reads are done
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+            const int f = threadIdx.x + 256 * u;
+            *reinterpret_cast<f32x4*>(lds + (f >> 4) * kLaStride + 4 * (f & 15)) = v[u];
+        }
+#pragma unroll
+        for (int kg = 0; kg < 4; ++kg) av[kg] = avn[kg];
+        __syncthreads();
+        if (kc + kLaK < a.psbw) la_fetch<FULL>(a, i0, kc + kLaK, v, avn);   // in flight below
+#pragma unroll
+        for (int kg = 0; kg < 4; ++kg)
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+                const f32x4 bv = *reinterpret_cast<const f32x4*>(
+                    lds + (64 * wave + 16 * t + r) * kLaStride + 16 * kg + 4 * h);
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[kg][u], bv[u], acc[t], 0, 0, 0);
+            }
+    }
+}
+
+__device__ __forceinline__ void lookahead(const StepArgs& a, float* lds, int64_t i0, int lrow,
+                                          int g, bool rowok, float dscale)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int r = lane & 15, h = lane >> 4;
+    f32x4 acc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (a.sig_vec4 && a.sbw == kLaCols && a.psbw % kLaK == 0 && i0 + 16 <= a.q)
+        lookahead_k<true>(a, lds, i0, acc);
+    else
+        lookahead_k<false>(a, lds, i0, acc);
+    __syncthreads();                             // the last chunk's reads are done
+    float* sU = lds;                             // 16 x 256 result
+    // 16 x 16 output: lane holds rows 4 (lane / 16) + v, column lane % 16
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) sU[(4 * h + v) * kLaUStride + 64 * wave + 16 * t + r] = acc[t][v];
+    __syncthreads();
+    if (!rowok) return;
+    const int64_t i = i0 + lrow;
+#pragma unroll
+    for (int m = 0; m < kLaCols / 16; ++m) {
+        const int c = 16 * m + g;
+        if (c < a.sbw) {
+            float* rp = a.R + i * a.p + a.sb + c;
+            *rp = fmaf(dscale, sU[lrow * kLaUStride + c], *rp);
+        }
+    }
+}
+
 template <int SLOTS>
 __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
 {
@@ -461,6 +576,10 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
     const float z = rowok ? a.zero[i] : 0.f;
     const float inv_s = rowok ? a.inv_s[i] : 1.f;
     const int nsub = (int)cdiv(a.sbw, B);
+    const float dscale = a.intd ? s : 1.f;
+    // (1) look-ahead: the previous super-block's deltas on this one's columns
+    //     (written to R: this launch's GEMM leaves these columns out)
+    if (a.psb >= 0) lookahead(a, lds, i0, lrow, g, rowok, dscale);
 
     for (int sub = 0; sub < nsub; ++sub) {
         const int64_t j0 = a.sb + (int64_t)sub * B;
@@ -487,20 +606,6 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
                 // with code differences t is taken from the code itself: What's
                 // exact level s (k - z) over s, plus z, is k
                 if (a.intd) st.v[m] = st.k[m];
-            }
-        }
-        const float dscale = a.intd ? s : 1.f;
-        // (1) look-ahead: deltas of the previous super-block, R_{i,J} written back
-        if (a.psb >= 0) {
-            for (int kc = 0; kc < a.psbw; kc += B) {
-                const int kw = min(B, a.psbw - kc);
-                add_block_update<SLOTS>(st, a, a.dprev, kc, kw, a.psb + kc, j0, width, i0, lrow, g,
-                                        lds, dscale);
-            }
-#pragma unroll
-            for (int m = 0; m < SLOTS; ++m) {
-                const int c = 16 * m + g;
-                if (rowok && c < width) a.R[i * p + j0 + c] = st.L[m];
             }
         }
         // (2) earlier blocks of this super-block (this workgroup's own rows; not
@@ -610,6 +715,7 @@ template <int SLOTS>
 __global__ __launch_bounds__(256, 2) void cd_step_kernel(StepArgs a)
 {
     if (failed(a.status)) return;
+    static_assert(step_lds_floats<SLOTS>() >= kLaCols * kLaStride, "look-ahead staging fits");
     __shared__ __attribute__((aligned(16))) float lds[step_lds_floats<SLOTS>()];
     if ((int)blockIdx.x < a.n_panel)
         panel_role<SLOTS>(a, lds);
