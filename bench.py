@@ -225,12 +225,13 @@ def main():
     q, p, n, bits, sweeps = spec.q, spec.p, spec.n, spec.bits, spec.sweeps
     block = 128
 
-    log(f"generating inputs: W {q}x{p}, X {p}x{n}")
+    log(f"generating inputs: W {q}x{p}, X {p}x{n} (X drawn on the device, seeded)")
     W_h = synth.weights(spec)
-    X_h = synth.activations(spec)
-    X = torch.from_numpy(X_h).to(dev)
-    X_head = np.ascontiguousarray(X_h[:, :CPU_GRAM_TOKENS])
-    del X_h
+    X = torch.empty((p, n), dtype=torch.float32, device=dev)
+    chunk = 32768
+    for c in range(n // chunk):
+        X[:, c * chunk:(c + 1) * chunk] = synth.activation_chunk_device(spec, c, chunk, dev)
+    X_head = X[:, :CPU_GRAM_TOKENS].cpu().numpy()          # the oracle's token sample
     W = torch.from_numpy(W_h).to(dev)
     Sigma = torch.empty((p, p), dtype=torch.float32, device=dev)
     Wh = torch.empty_like(W)
@@ -442,13 +443,21 @@ def main():
     print(json.dumps(result), flush=True)
 
 
-def configs_bench(P, torch, synth):
+# oracle row sample per configuration for the --configs report (rows; Gram tokens)
+CONFIG_ORACLE = {"c1": (512, 2048), "c2": (256, 2048), "c3up": (256, 2048),
+                 "c3down": (128, 1024), "c5": (32, 256)}
+
+
+def configs_bench(P, torch, synth, with_oracle=True):
     """Every workload configuration at its full size: the Gram over all
     n = 262144 device-drawn tokens (one call when X fits comfortably, else
     token chunks accumulated into Sigma), damping, the per-row grid and the
     configured number of CD sweeps from What = W.  Times from HIP events on
     the library's stream (c1 timed on its second pass, after the code objects
-    are loaded)."""
+    are loaded).  With the oracle: one Lemma-1 sweep over a seeded row sample
+    on the host cores (Sigma from a token prefix of the same X; the sweep's
+    cost does not depend on Sigma's values), scaled by q / rows and by the
+    sweep count (rows are independent, so the cost is linear in them)."""
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
     out = {}
@@ -461,8 +470,11 @@ def configs_bench(P, torch, synth):
         chunk = n if p * n * 4 <= (16 << 30) else 32768
         Sigma = torch.empty((p, p), dtype=torch.float32, device=dev)
         gram_s = 0.0
+        head = None
         for c in range(n // chunk):
             Xc = synth.activation_chunk_device(spec, c, chunk, dev)
+            if c == 0 and with_oracle:
+                head = Xc[:, :CONFIG_ORACLE[key][1]].cpu().numpy()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             P.gram(Xc, Sigma=Sigma, accumulate=c > 0, damp=spec.damp if c == n // chunk - 1 else 0.0)
@@ -471,7 +483,8 @@ def configs_bench(P, torch, synth):
             gram_s += e0.elapsed_time(e1) * 1e-3
             del Xc
         torch.cuda.empty_cache()
-        W = torch.from_numpy(synth.weights(spec)).to(dev)
+        W_h = synth.weights(spec)
+        W = torch.from_numpy(W_h).to(dev)
         scale, zero = P.grid_minmax(W, spec.bits)
         Wh = torch.empty_like(W)
         R = torch.empty_like(W)
@@ -484,15 +497,31 @@ def configs_bench(P, torch, synth):
         e1.record(stream)
         torch.cuda.synchronize()
         cd_s = e0.elapsed_time(e1) * 1e-3
-        out[spec.name] = {"q": q, "p": p, "n": n, "bits": spec.bits, "sweeps": spec.sweeps,
-                          "gram_s": gram_s, "gram_chunks": n // chunk,
-                          "gram_fp32_equivalent_tflops": float(p) * (p + 1) * n / gram_s / 1e12,
-                          "sweep_s": cd_s / spec.sweeps,
-                          "cd_fp32_equivalent_tflops": 2.0 * q * p * p * spec.sweeps / cd_s / 1e12,
-                          "layer_s": gram_s + cd_s,
-                          "column_updates_per_s": p * spec.sweeps / (gram_s + cd_s)}
+        rec = {"q": q, "p": p, "n": n, "bits": spec.bits, "sweeps": spec.sweeps,
+               "gram_s": gram_s, "gram_chunks": n // chunk,
+               "gram_fp32_equivalent_tflops": float(p) * (p + 1) * n / gram_s / 1e12,
+               "sweep_s": cd_s / spec.sweeps,
+               "column_updates_per_s": p * spec.sweeps / cd_s,
+               "cd_fp32_equivalent_tflops": 2.0 * q * p * p * spec.sweeps / cd_s / 1e12,
+               "layer_s": gram_s + cd_s,
+               "layer_column_updates_per_s": p * spec.sweeps / (gram_s + cd_s)}
+        sc_h, ze_h = scale.cpu().numpy(), zero.cpu().numpy()
         del Sigma, W, Wh, R, codes, ws
         torch.cuda.empty_cache()
+        if with_oracle and key in CONFIG_ORACLE and head is not None:
+            import oracle
+            rows_n, _ = CONFIG_ORACLE[key]
+            S = oracle.damp(oracle.gram_blas(head, row_block=4096), spec.damp)
+            rows = synth.row_sample(q, rows_n, spec.cfg)
+            t = oracle.cd_sweep_timed(W_h[rows], S, spec.bits, sc_h[rows], ze_h[rows])
+            del S
+            sweep_oracle = t * q / len(rows)
+            rec["oracle"] = {"sweep_s": sweep_oracle, "measured_s": t, "rows": len(rows),
+                             "cores": oracle.num_threads(), "kind": "oracle",
+                             "column_updates_per_s": p / sweep_oracle,
+                             "extrapolated": len(rows) < q}
+            rec["gpu_over_oracle"] = rec["column_updates_per_s"] / rec["oracle"]["column_updates_per_s"]
+        out[spec.name] = rec
     return {"configs": out}
 
 

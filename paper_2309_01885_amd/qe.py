@@ -134,7 +134,9 @@ def _check(code: int, where: str):
 
 
 def workspace(nbytes: int, device) -> torch.Tensor:
-    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+    """A device workspace; zero-filled, so that its status word reads QE_OK
+    before any call has used it."""
+    return torch.zeros(max(int(nbytes), 256), dtype=torch.uint8, device=device)
 
 
 def sync_status(ws: torch.Tensor, stream=None) -> int:
