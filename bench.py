@@ -9,7 +9,9 @@ layer_column_updates_per_s.  The headline roofline is the CD step kernel
 (the block-update GEMM with the next panel), the Gram's is under
 "rooflines"; each counts the method's own flops (2qp^2 per sweep,
 p(p+1)n per Gram) against the peak of the matrix-core type the kernels
-issue (bf16: the fp32 products are exact three-way bf16 splits).  The
+issue (bf16: the fp32 products are exact three-way bf16 splits, and once
+the codes are valid the block update multiplies integer code differences,
+exact in one bf16 plane, by Sigma's three planes).  The
 outlier-aware path (3-bit, 1% outliers: lambda_max, P_s(W), outlier grid, 10
 CD + IHT iterations) is timed in the same run under "outlier"; the CPU
 oracle is timed under "cpu_baseline" (all sweeps on every row; its Gram on a
@@ -34,6 +36,7 @@ HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 SPLIT_PRODUCTS = 6             # bf16 products per fp32 product (exact three-way split)
+INT_DELTA_PRODUCTS = 3         # integer code difference x three bf16 planes of Sigma
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_c2_4096x4096.md")
 LAUNCH_PROFILE = os.path.join(ROOT, "profiles", "kernel_trace_gram_cd_step_c2_4096x4096.md")
 PARITY_RECORD = os.path.join(ROOT, "profiles", "parity_c2_4096x4096.md")
@@ -324,11 +327,11 @@ def main():
     sweep_t = cd_phase_t / sweeps
     traffic = measured_traffic()
 
-    def roofline(kernel, flops, seconds, extra):
+    def roofline(kernel, flops, seconds, products, issued, extra):
         """The method's own flops (fp32 multiply-adds x 2) per launch over the
         launch time, against the peak of the matrix-core type issued (bf16);
-        the six-product issue rate and the fp32-equivalent fraction are
-        separate fields."""
+        the issue rate (`products` exact bf16 products per fp32 product) and
+        the fp32-equivalent fraction are separate fields."""
         achieved = flops / seconds / 1e12
         r = {"kernel": kernel, "bound": "mfma", "achieved": achieved,
              "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -336,18 +339,26 @@ def main():
              "traffic": traffic.get(kernel.split("<")[0]),
              "flops_per_launch": flops,
              "flops_counted": "the method's: fp32 products of the algorithm, 2 flops each",
-             "issued": "bf16 matrix cores, 6 exact bf16 products per fp32 product",
-             "issued_bf16_tflops": SPLIT_PRODUCTS * achieved,
-             "issued_frac_of_bf16_peak": SPLIT_PRODUCTS * achieved / BF16_MFMA_PEAK_TFLOPS,
+             "issued": issued,
+             "bf16_products_per_fp32_product": products,
+             "issued_bf16_tflops": products * achieved,
+             "issued_frac_of_bf16_peak": products * achieved / BF16_MFMA_PEAK_TFLOPS,
              "fp32_equivalent_frac": achieved / FP32_MFMA_PEAK_TFLOPS,
-             "frac_of_split_ceiling": achieved / (BF16_MFMA_PEAK_TFLOPS / SPLIT_PRODUCTS)}
+             "frac_of_split_ceiling": achieved / (BF16_MFMA_PEAK_TFLOPS / products)}
         r.update(extra)
         return r
 
-    # 2qp^2 per sweep over its nb + 1 launches; p(p+1)n for the Gram (symmetric half)
+    # 2qp^2 per sweep over its nb + 1 launches; p(p+1)n for the Gram (symmetric half).
+    # The resumed sweeps start from valid codes, so the block update multiplies
+    # integer code differences (one exact bf16 plane) by Sigma's three planes.
     roof_cd = roofline("cd_step_kernel<8>", 2.0 * q * p * p / (nb + 1), cd_avg,
+                       INT_DELTA_PRODUCTS,
+                       "bf16 matrix cores: integer code differences (exact in bf16) times "
+                       "the three bf16 planes of Sigma, 3 products per fp32 product",
                        {"avg_launch_s": cd_avg, "launches_per_sweep": nb + 1})
-    roof_gram = roofline("gram_x3w_kernel", float(p) * (p + 1) * n, gram_t, {"call_s": gram_t})
+    roof_gram = roofline("gram_x3w_kernel", float(p) * (p + 1) * n, gram_t, SPLIT_PRODUCTS,
+                         "bf16 matrix cores, 6 exact bf16 products per fp32 product",
+                         {"call_s": gram_t})
 
     # the Gram from token-major activations (n x p, as a model produces them),
     # in one call and streamed in 32768-token chunks accumulated into Sigma
