@@ -673,19 +673,19 @@ __device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t
         nt_tile(A, row0, Bo, col0, a.psbw, lds, acc);
     } else {
         // split bf16 products (nt_x3.h); Delta rows are 16-byte aligned (stride S)
-        const X3Row Bo{a.Sigma + a.psb, a.p, a.p, a.psbw};
+        const XRowQ<256, 3> Bo{a.Sigma + a.psb, a.p, a.p, a.psbw};
         uint32_t* l32 = reinterpret_cast<uint32_t*>(lds);
         const bool full =
             a.sig_vec4 && row0 + kTile <= a.q && col0 + kTile <= a.p && a.psbw % (2 * kX3KC) == 0;
         if (a.intd) {
             // code differences are exact in bf16: three exact products with Sigma's planes
-            const X1Row A{{a.dprev, a.S, a.q, a.psbw}};
+            const XRowQ<256, 1> A{a.dprev, a.S, a.q, a.psbw};
             if (full)
                 nt_tile_x3_full<true, 3>(A, row0, Bo, col0, a.psbw, l32, acc);
             else
                 nt_tile_x3_edge<3>(A, row0, Bo, col0, a.psbw, l32, acc);
         } else {
-            const X3Row A{a.dprev, a.S, a.q, a.psbw};
+            const XRowQ<256, 3> A{a.dprev, a.S, a.q, a.psbw};
             if (full)
                 nt_tile_x3_full(A, row0, Bo, col0, a.psbw, l32, acc);
             else

@@ -121,6 +121,59 @@ struct X1Row : X3Row {
     }
 };
 
+// Row-major operand staged by four lanes per row: with NT threads, thread t
+// holds rows t / 4 and t / 4 + NT / 4 at k = 4 (t % 4) .. +3, so that each
+// 16-byte load instruction of a wave covers 16 rows of 64 contiguous bytes
+// (half as many cache lines per instruction as two lanes per row).  NT / 2
+// rows per stage; PLANES = 3 stores h, m and l, PLANES = 1 only h (values
+// exact in bf16, such as the code differences of the CD block update).
+template <int NT, int PLANES>
+struct XRowQ {
+    const float* base;
+    int64_t ld, rows, kvalid;
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const float* src = base + (row0 + (t >> 2)) * ld + k0 + 4 * (t & 3);
+        st.v[0] = *reinterpret_cast<const f32x4*>(src);
+        st.v[1] = *reinterpret_cast<const f32x4*>(src + (NT / 4) * ld);
+    }
+    __device__ inline void load(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int64_t k = k0 + 4 * (t & 3);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int64_t r = row0 + (t >> 2) + h * (NT / 4);
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                st.v[h][u] = (r < rows && k + u < kvalid) ? base[r * ld + k + u] : 0.f;
+        }
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int kq = t & 3;                    // half kq / 2, dwords 2 (kq % 2) .. +1 of it
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int o = x3_addr((t >> 2) + h * (NT / 4), kq >> 1, 0) + 2 * (kq & 1);
+            if constexpr (PLANES == 3) {
+                const X3Pair q0 = split3(st.v[h][0], st.v[h][1]);
+                const X3Pair q1 = split3(st.v[h][2], st.v[h][3]);
+                *reinterpret_cast<u32x2*>(op + o) = u32x2{q0.h, q1.h};
+                *reinterpret_cast<u32x2*>(op + o + 8) = u32x2{q0.m, q1.m};
+                *reinterpret_cast<u32x2*>(op + o + 16) = u32x2{q0.l, q1.l};
+            } else {
+                const uint32_t h0 = __builtin_bit_cast(
+                    uint32_t, __builtin_convertvector((f32x2){st.v[h][0], st.v[h][1]}, bf16x2));
+                const uint32_t h1 = __builtin_bit_cast(
+                    uint32_t, __builtin_convertvector((f32x2){st.v[h][2], st.v[h][3]}, bf16x2));
+                *reinterpret_cast<u32x2*>(op + o) = u32x2{h0, h1};
+            }
+        }
+    }
+};
+
 // Row-major composite operand P1 + P2 - P3 (P2, P3 may be null), e.g.
 // What + H - W, staged as X3Row.
 struct X3Comp {
@@ -284,17 +337,24 @@ __device__ __forceinline__ void x3_mfma_stage(const uint32_t* sA, const uint32_t
                     acc[mi][ni], 0, 0, 0);
 }
 
+// LDS store instructions of one operand's stage: the four-lanes-per-row
+// loaders store 8-byte pieces (two per plane), the others 16-byte ones.
+template <class O> struct X3Writes { static constexpr int value = 3; };
+template <> struct X3Writes<X1Row> { static constexpr int value = 1; };
+template <int NT, int PL> struct X3Writes<XRowQ<NT, PL>> { static constexpr int value = 2 * PL; };
+template <class O> constexpr int x3_writes() { return X3Writes<O>::value; }
+
 // Instruction order of one stage when INTERLEAVE is set: the operand reads,
 // then the MFMAs, each followed by a few VALU instructions of the next stage's
 // split, then the LDS writes, so that the split runs while the matrix cores
 // work.
-template <int NP = 6>
+template <int NP = 6, int WRITES = (NP == 6 ? 6 : 4)>
 __device__ __forceinline__ void x3_interleave()
 {
     // operand reads: A's planes (three, or one with NP = 3) and B's three, per
-    // 32-row block; MFMAs 4 NP; LDS writes of the next stage: one or three
-    // planes of A, three of B
-    constexpr int reads = NP == 6 ? 12 : 8, writes = NP == 6 ? 6 : 4;
+    // 32-row block; MFMAs 4 NP; LDS writes of the next stage (the operands'
+    // store instructions)
+    constexpr int reads = NP == 6 ? 12 : 8, writes = WRITES;
     __builtin_amdgcn_sched_group_barrier(0x100, reads, 0);         // DS reads
 #pragma unroll
     for (int i = 0; i < 4 * NP; ++i) {
@@ -338,7 +398,7 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a1, ra1);
         B.store(b1, rb1);
-        if constexpr (INTERLEAVE) x3_interleave<NP>();
+        if constexpr (INTERLEAVE) x3_interleave<NP, x3_writes<OA>() + x3_writes<OB>()>();
         __syncthreads();
         // LDS 1: stage c + 1; registers 0: stage c + 2; registers 1 take stage c + 3
         A.load_full(row0a, (c + 3) * kX3KC, ra1);
@@ -348,7 +408,7 @@ __device__ __forceinline__ void nt_tile_x3_full(const OA& A, int64_t row0a, cons
         if constexpr (!INTERLEAVE) __builtin_amdgcn_sched_barrier(0);
         A.store(a0, ra0);
         B.store(b0, rb0);
-        if constexpr (INTERLEAVE) x3_interleave<NP>();
+        if constexpr (INTERLEAVE) x3_interleave<NP, x3_writes<OA>() + x3_writes<OB>()>();
         __syncthreads();
     }
     x3_mfma_stage<NP>(a0, b0, acc);
