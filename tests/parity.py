@@ -14,8 +14,10 @@ are correct.  Two checks follow from that:
   carry over from one sweep to the next.  Asserted after every sweep, whether
   or not any row splits: at most 0.1% of the sample's codes differ from the
   oracle's; in every row the first differing code sits at an oracle tie
-  (|frac(t) - 1/2| <= 1e-4 grid units); the GPU's objective over the sample
-  agrees with the oracle's within 1e-4 relative.
+  (|frac(t) - 1/2| <= 1e-4 grid units), and every later difference in that
+  row follows from tie decisions (the oracle, taking the GPU's level at each
+  tie, reaches the GPU's codes); the GPU's objective over the sample agrees
+  within 1e-4 relative with the oracle's along those same tie decisions.
 * ``free_running`` (reported; partly asserted).  The oracle runs all sweeps
   on its own from the common start.  Asserted: each row's first divergence
   sits at an oracle tie; rows that never split agree on the objective within
@@ -75,6 +77,23 @@ def first_divergence(codes_gpu_hist, codes_ref_hist):
     return out
 
 
+def _obj_errors(rec, f_gpu, f_ref, f0, f_reported=None):
+    """Objective errors of one sweep against the reference value f_ref, with
+    the floor the fp32 storage of the levels sets: every What_ij is a level
+    rounded to fp32 (relative error eps <= 2^-24, taken as 2^-23), which moves
+    (W - What) X by at most eps ||W X|| and f = ||(W - What) X||^2 by at most
+    2 eps sqrt(f ||W X||^2) + eps^2 ||W X||^2 (f0 = ||W X||_F^2)."""
+    eps = 2.0 ** -23
+    rec["obj_ref"] = f_ref
+    rec["obj_atol"] = 2 * eps * np.sqrt(abs(f_ref) * f0) + eps * eps * f0
+    rec["obj_abs_err"] = abs(f_gpu - f_ref)
+    rec["obj_rel_err"] = rec["obj_abs_err"] / abs(f_ref) if f_ref else rec["obj_abs_err"]
+    if f_reported is not None:
+        rec["reported_obj_abs_err"] = abs(f_reported - f_ref)
+        rec["reported_obj_rel_err"] = (rec["reported_obj_abs_err"] / abs(f_ref) if f_ref
+                                       else rec["reported_obj_abs_err"])
+
+
 def gpu_row_objective(W_rows, what, R):
     """f_i = <What_i - W_i, R_i> per row from the GPU's own residual (fp64 sum)."""
     return np.sum((np.asarray(what, np.float64) - np.asarray(W_rows, np.float64))
@@ -127,11 +146,16 @@ def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs
     whats, Rs: the GPU's codes, What and R of those rows after each sweep.
     W0/codes0/codes_valid0: the state the GPU's first sweep started from
     (default: What = W, codes not valid).  gpu_obj: optional per-sweep
-    objective the library reported for exactly these rows.  Returns the
-    per-sweep figures."""
+    objective the library reported for exactly these rows.  The objective is
+    compared with the oracle's along the same path: in rows that split at a
+    tie (every difference traced back to tie decisions by explain_row) the
+    reference is the objective of the GPU's own levels, which the oracle
+    reaches by taking the GPU's choice at each tie.  Returns the per-sweep
+    figures."""
     W64 = np.asarray(W_rows, np.float64)
     if T is None:
         T = W64 @ S64
+    f0 = float(np.sum(W64 * T))              # ||W X||_F^2 of the sample
     sweeps = len(codes_hist)
     stats = []
     for k in range(sweeps):
@@ -153,11 +177,8 @@ def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs
         f_ref = ref.obj[0]
         f_gpu = float(np.sum(gpu_row_objective(W_rows, whats[k], Rs[k])))
         rec = {"sweep": k + 1, "code_diff_frac": frac, "split_rows": int(len(split_rows)),
-               "max_first_margin": max(margins) if margins else 0.0,
-               "obj_rel_err": abs(f_gpu - f_ref) / abs(f_ref) if f_ref else abs(f_gpu)}
-        if gpu_obj is not None:
-            rec["reported_obj_rel_err"] = (abs(gpu_obj[k] - f_ref) / abs(f_ref) if f_ref
-                                           else abs(gpu_obj[k]))
+               "max_first_margin": max(margins) if margins else 0.0}
+        _obj_errors(rec, f_gpu, f_ref, f0, None if gpu_obj is None else gpu_obj[k])
         rec["first_diff"] = [[int(i), int(np.argmax(diff[i])), m, int(diff[i].sum())]
                              for i, m in zip(split_rows, margins)]
         if explain:
@@ -174,6 +195,20 @@ def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs
             with ThreadPoolExecutor(max(1, min(16, len(todo)))) as ex:
                 found = list(ex.map(one, todo))
             rec["tie_decisions"] = [[i, [[j, mm] for j, mm in t]] for i, t in zip(todo, found)]
+            if len(todo) and len(todo) == len(split_rows):
+                # Along the GPU's tie decisions the oracle reaches exactly the
+                # GPU's codes in every split row (explain_row), so the
+                # reference objective of those rows is that of the GPU's
+                # levels: compare the objective on the same path.
+                rows = np.asarray(todo)
+                lev = (np.asarray(scale, np.float64)[rows, None]
+                       * (g[rows] - np.asarray(zero, np.float64)[rows, None]))
+                d_ref = np.asarray(ref.What, np.float64)[rows] - W64[rows]
+                d_gpu = lev - W64[rows]
+                f_tie = (f_ref - float(np.sum(d_ref * (d_ref @ S64)))
+                         + float(np.sum(d_gpu * (d_gpu @ S64))))
+                rec["obj_ref_along_ties"] = f_tie
+                _obj_errors(rec, f_gpu, f_tie, f0, None if gpu_obj is None else gpu_obj[k])
         stats.append(rec)
     log_stats({"check": "teacher_forced", "label": label, "rows": int(W64.shape[0]),
                "cols": int(W64.shape[1]), "sweeps": stats})
@@ -185,10 +220,10 @@ def teacher_forced(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs
             assert m <= tie_margin, \
                 f"{where}: row {i} first differs at column {j}, oracle margin {m:.3e} grid " \
                 f"units (not a tie)"
-        assert rec["obj_rel_err"] <= obj_rtol, f"{where}: objective (teacher-forced) off by " \
-            f"{rec['obj_rel_err']:.3e}"
+        assert rec["obj_abs_err"] <= obj_rtol * abs(rec["obj_ref"]) + rec["obj_atol"], \
+            f"{where}: objective (teacher-forced) off by {rec['obj_rel_err']:.3e}"
         if gpu_obj is not None:
-            assert rec["reported_obj_rel_err"] <= obj_rtol, \
+            assert rec["reported_obj_abs_err"] <= obj_rtol * abs(rec["obj_ref"]) + rec["obj_atol"], \
                 f"{where}: reported objective off by {rec['reported_obj_rel_err']:.3e}"
     return stats
 
@@ -201,6 +236,8 @@ def free_running(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs, 
     identical rows agreeing on the objective, split rows descending) and
     returns the per-sweep code-difference fractions."""
     W64 = np.asarray(W_rows, np.float64)
+    if T is None:
+        T = W64 @ S64
     sweeps = len(codes_hist)
     ref = oracle.cd(W_rows, S64, bits, scale, zero, sweeps,
                     W0=None if W0 is None else np.asarray(W0, np.float64),
@@ -216,7 +253,9 @@ def free_running(oracle, W_rows, S64, bits, scale, zero, codes_hist, whats, Rs, 
         f_ref = np.sum((D @ S64) * D, axis=1)
         if same.any():
             a, b = float(np.sum(f_gpu[same])), float(np.sum(f_ref[same]))
-            assert abs(a - b) <= obj_rtol * abs(b) + 1e-300, \
+            rec = {}
+            _obj_errors(rec, a, b, float(np.sum((W64 * T)[same])))
+            assert rec["obj_abs_err"] <= obj_rtol * abs(b) + rec["obj_atol"], \
                 f"{label} sweep {k + 1}: objective over the {int(same.sum())} rows that never split"
         if f_prev is not None and not same.all():
             assert np.all(f_gpu[~same] <= f_prev[~same] * (1 + 1e-6) + 1e-12), \

@@ -109,6 +109,45 @@ def test_cd_matches_oracle(qe, oracle, q, p, corr, bits, fp32):
     check_parity(oracle, W, S32, bits, scale, zero, g, f"cd {q}x{p} corr={corr} b={bits} fp32={fp32}")
 
 
+@pytest.mark.parametrize("bits", [1, 8])
+def test_extreme_bit_widths(qe, oracle, bits):
+    """The narrowest and widest grids the ABI takes (2 and 256 levels)."""
+    W, X = layer(128, 300, 1024, 41, corr=0.9, bits=bits)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, bits)
+    g = gpu_cd(qe, W, S32, bits, scale, zero, 4)
+    check_parity(oracle, W, S32, bits, scale, zero, g, f"bits {bits}")
+
+
+def test_degenerate_rows(qe, oracle):
+    """An all-zero row (grid [-1, 1], Sec. 2.1 reading), a constant row, a row
+    with one nonzero entry and an ordinary row: the grid bit for bit, then
+    the sweeps through the parity protocol."""
+    W, X = layer(4, 96, 512, 42, corr=0.9)
+    W[0] = 0.0
+    W[1] = 0.5
+    W[2] = 0.0
+    W[2, 17] = -0.03
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    sc_d, ze_d = qe.grid_minmax(dev(W), 4)
+    scale, zero = oracle.grid_minmax(W, 4)
+    assert np.array_equal(host(sc_d), scale) and np.array_equal(host(ze_d), zero)
+    g = gpu_cd(qe, W, S32, 4, scale, zero, 3)
+    check_parity(oracle, W, S32, 4, scale, zero, g, "degenerate rows")
+    assert np.all(g["What"][0] == 0.0)       # zero is a level of every grid
+
+
+@pytest.mark.parametrize("q,p", [(1, 1), (1, 5), (5, 1), (3, 2)])
+def test_tiny_layers(qe, oracle, q, p):
+    """Single rows and columns: one panel, a partial block, no GEMM tile
+    beyond the first."""
+    W, X = layer(q, p, 64, 43 + q + p, corr=0.5)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 3)
+    g = gpu_cd(qe, W, S32, 3, scale, zero, 3)
+    check_parity(oracle, W, S32, 3, scale, zero, g, f"tiny {q}x{p}")
+
+
 @pytest.mark.parametrize("block", [16, 32, 64, 128])
 def test_block_width_invariance(qe, oracle, block):
     W, X = layer(96, 250, 1024, 12, corr=0.9)

@@ -86,11 +86,14 @@ def test_protocol_explains_a_cascade_from_a_tie(oracle):
     gpu[i] = tail.codes[0]
     whats = [oracle.dequant(gpu, scale, zero).astype(np.float32)]
     Rs = [(whats[0].astype(np.float64) - W2) @ S]
-    stats = teacher_forced(oracle, W2, S, 3, scale, zero, [gpu], whats, Rs, code_frac=1.0,
-                           obj_rtol=1.0)
+    stats = teacher_forced(oracle, W2, S, 3, scale, zero, [gpu], whats, Rs, code_frac=1.0)
     assert stats[0]["split_rows"] == 1
     (row, ties), = stats[0]["tie_decisions"]
     assert row == i and ties[0][0] == j
+    # the objective is compared along the GPU's tie decision
+    assert stats[0]["obj_rel_err"] <= 1e-8           # fp32 levels in whats and Rs
+    assert stats[0]["obj_ref_along_ties"] == pytest.approx(
+        oracle.objective(W2, whats[0], S), rel=1e-8)
 
 
 def _t_at(oracle, W, S, scale, zero, i, j, w_ij):
