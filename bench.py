@@ -40,6 +40,7 @@ INT_DELTA_PRODUCTS = 3         # integer code difference x three bf16 planes of 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_c2_4096x4096.md")
 LAUNCH_PROFILE = os.path.join(ROOT, "profiles", "kernel_trace_gram_cd_step_c2_4096x4096.md")
 PARITY_RECORD = os.path.join(ROOT, "profiles", "parity_c2_4096x4096.md")
+CONFIG_PROFILE = os.path.join(ROOT, "profiles", "cd_step_per_configuration.md")
 CALIB_COPY_BYTES = 256 << 20
 
 
@@ -207,6 +208,8 @@ def main():
     ap.add_argument("--configs", action="store_true",
                     help="instead of the c2 step: Gram and CD timings of every workload "
                          "configuration at its full size (one JSON line)")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="leave the per-configuration report out of the line")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU: --gpus {args.gpus} is not supported "
@@ -219,7 +222,7 @@ def main():
     import synth
 
     if args.configs:
-        print(json.dumps(configs_bench(P, torch, synth)), flush=True)
+        print(json.dumps(configs_bench(P, torch, synth, with_oracle=not args.no_cpu)), flush=True)
         return
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -446,6 +449,12 @@ def main():
                                               zero.cpu().numpy(), sweeps,
                                               full=not args.oracle_sample)
         result["gpu_over_oracle"] = value / result["cpu_baseline"]["value"]
+    if not args.no_configs:
+        log("every workload configuration at full size")
+        del X, W, Sigma, Wh, R, codes
+        torch.cuda.empty_cache()
+        result["configs"] = configs_report(configs_bench(P, torch, synth,
+                                                         with_oracle=not args.no_cpu))
     if args.calib_copy:
         a = torch.ones(CALIB_COPY_BYTES // 4, dtype=torch.float32, device=dev)
         b = torch.empty_like(a)
@@ -534,6 +543,31 @@ def configs_bench(P, torch, synth, with_oracle=True):
             rec["gpu_over_oracle"] = rec["column_updates_per_s"] / rec["oracle"]["column_updates_per_s"]
         out[spec.name] = rec
     return {"configs": out}
+
+
+def configs_report(rep):
+    """Per-configuration rows for the line: the timings of configs_bench plus,
+    from the committed per-configuration kernel trace and counter profile
+    (while the step kernel's sources match), the panel-only launch as HBM
+    bandwidth (17 bytes per coordinate of a 256-column super-block) and the
+    step kernel's matrix-core busy fraction."""
+    prof = _json_block(CONFIG_PROFILE)
+    valid = bool(prof) and prof.get("source_sha256") == kernel_source_hash("cd_step_kernel")
+    rows = {}
+    for name, rec in rep["configs"].items():
+        row = dict(rec)
+        pc = prof.get("configs", {}).get(name) if valid else None
+        if pc:
+            t = pc["panel_only_launch_us"] * 1e-6
+            b = 17.0 * rec["q"] * min(256, rec["p"])
+            row["panel"] = {"launch_s": t, "achieved_GBps": b / t / 1e9,
+                            "frac_of_hbm_peak": b / t / 1e9 / HBM_PEAK_GBS}
+            row["cd_step_mfma_busy"] = pc.get("mfma_busy")
+        else:
+            row["panel"] = None
+            row["cd_step_mfma_busy"] = None
+        rows[name] = row
+    return rows
 
 
 def outlier_bench(P, torch, synth, W, Sigma, dev, block):

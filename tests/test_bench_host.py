@@ -70,3 +70,22 @@ def test_help_lists_the_switches():
     for flag in ("--gpus", "--steps", "--warmup", "--no-cpu", "--no-outlier", "--no-peaks",
                  "--calib-copy", "--configs", "--oracle-sample"):
         assert flag in r.stdout, flag
+
+
+def test_configs_report_rows(monkeypatch, tmp_path):
+    """The per-configuration rows: the timings pass through; panel bandwidth
+    and matrix-core busy come from the committed profile only while its
+    source hash matches the step kernel's sources."""
+    rep = {"configs": {"w": {"q": 4096, "p": 4096, "sweep_s": 1e-3}}}
+    prof = tmp_path / "p.md"
+    monkeypatch.setattr(bench, "CONFIG_PROFILE", str(prof))
+    prof.write_text('```json\n{"source_sha256": "%s", "configs": {"w": '
+                    '{"panel_only_launch_us": 26.0, "mfma_busy": 0.2}}}\n```\n'
+                    % bench.kernel_source_hash("cd_step_kernel"))
+    row = bench.configs_report(rep)["w"]
+    assert row["sweep_s"] == 1e-3 and row["cd_step_mfma_busy"] == 0.2
+    assert abs(row["panel"]["achieved_GBps"] - 17.0 * 4096 * 256 / 26e-6 / 1e9) < 1e-6
+    prof.write_text('```json\n{"source_sha256": "0", "configs": {"w": '
+                    '{"panel_only_launch_us": 26.0, "mfma_busy": 0.2}}}\n```\n')
+    row = bench.configs_report(rep)["w"]
+    assert row["panel"] is None and row["cd_step_mfma_busy"] is None
