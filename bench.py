@@ -312,13 +312,17 @@ def main():
     torch.cuda.synchronize()
     t_steps = e0.elapsed_time(e1) * 1e-3
     # one sweep per call from W = What: events around each of sweeps 2..K
-    # (with its objective, as in the step), median
+    # (with its objective, carried from call to call as inside the step's
+    # multi-sweep call), median
     per_sweep = []
     for k in range(sweeps):
+        if k > 0:
+            obj[k].copy_(obj[k - 1])                     # the incoming objective
         a0, a1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a0.record(stream)
         P.cd_sweep(W, Sigma, bits, scale, zero, Wh, codes, R, 1, block=block,
-                   flags=P.QE_INIT_FROM_W if k == 0 else P.QE_R_VALID | P.QE_CODES_VALID,
+                   flags=(P.QE_INIT_FROM_W if k == 0
+                          else P.QE_R_VALID | P.QE_CODES_VALID | P.QE_OBJ_IN),
                    obj=obj[k:], ws=ws_cd, check=False)
         a1.record(stream)
         per_sweep.append((a0, a1))

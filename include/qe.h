@@ -82,6 +82,11 @@ typedef int qe_status;
  * nothing).  One extra read of those arrays (about 30 us at 4096 x 4096).
  * Without the flag only Sigma's diagonal and the grid are checked. */
 #define QE_DEBUG_CHECKS 0x40u
+/* qe_cd_sweep only: obj[0] holds, on entry, the objective f of the incoming
+ * What and R (e.g. the last value of the previous call), so that chained
+ * calls report f without a pass over R.  Needs obj; not with QE_INIT_FROM_W
+ * (QE_ERR_ARG). */
+#define QE_OBJ_IN 0x80u
 
 /* Human-readable name of a status code (static string). */
 const char* qe_status_string(qe_status s);
@@ -145,11 +150,16 @@ qe_status qe_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, i
  * R:      q x p, device, in/out: (What - W) Sigma on exit.
  * sweeps: >= 0 full passes over the columns.
  * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_PERIOD(k)
- *         | QE_CD_FP32 | QE_DEBUG_CHECKS.
+ *         | QE_CD_FP32 | QE_DEBUG_CHECKS | QE_OBJ_IN.
  *         Without QE_INIT_FROM_W and without QE_R_VALID, R is first
  *         computed as (What - W) Sigma (warm start from any What, Sec. 3.1).
  * obj:    NULL, or device array of `sweeps` doubles receiving
- *         f_k = <What - W, R> = ||(W - What) X||_F^2 after sweep k.
+ *         f_k = <What - W, R> = ||(W - What) X||_F^2 after sweep k, formed
+ *         as the incoming f plus the exact change of each coordinate move
+ *         (Lemma 1's one-dimensional quadratic: delta (2 R_ij + delta
+ *         Sigma_jj)), summed in fp64 while the sweep runs, in a fixed order.
+ *         The incoming f is 0 with QE_INIT_FROM_W, obj[0] with QE_OBJ_IN,
+ *         else one pass <What - W, R> at the start of the call.
  * ------------------------------------------------------------------------ */
 size_t qe_cd_workspace_size(int64_t q, int64_t p, int block);
 qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
@@ -205,7 +215,9 @@ qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int
  *           Without QE_INIT_FROM_W / QE_R_VALID, E = (What + H - W) Sigma.
  *           QE_CD_FP32 and QE_DEBUG_CHECKS as for qe_cd_sweep.
  * obj:      NULL or device array of 2*sweeps doubles: obj[2k] = g after the
- *           CD sweep of iteration k, obj[2k+1] = g after its IHT step.
+ *           CD sweep of iteration k (g after the previous IHT step, or at
+ *           the start, plus the exact change of the sweep's moves, as for
+ *           qe_cd_sweep), obj[2k+1] = g after its IHT step (<What + H - W, E>).
  * scale/zero: the outlier-aware grid (qe_grid_minmax with H excluded).
  * ------------------------------------------------------------------------ */
 size_t qe_outlier_workspace_size(int64_t q, int64_t p, int block, int64_t s);

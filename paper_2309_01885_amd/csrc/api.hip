@@ -39,9 +39,16 @@ qe_status cd_arg_error(const float* W, const float* Sigma, const float* scale, c
     if (!W || !Sigma || !scale || !zero || !W_hat || !codes || !R) return QE_ERR_ARG;
     if (bad_dims(q, p) || bad_bits(bits) || bad_block(block) || sweeps < 0) return QE_ERR_ARG;
     if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_MASK | QE_CD_FP32 |
-                  QE_DEBUG_CHECKS))
+                  QE_DEBUG_CHECKS | QE_OBJ_IN))
         return QE_ERR_ARG;
     return QE_OK;
+}
+
+// QE_OBJ_IN reads obj[0]: it needs obj, and means nothing after QE_INIT_FROM_W
+// (the objective of What = W is 0).
+bool bad_obj_in(uint32_t flags, const double* obj)
+{
+    return (flags & QE_OBJ_IN) && (!obj || (flags & QE_INIT_FROM_W));
 }
 
 // ---- scratch of qe_cd_sweep_noalloc
@@ -161,11 +168,12 @@ qe_status qe_cd_sweep(const float* W, const float* Sigma, int64_t q, int64_t p, 
     const qe_status bad = cd_arg_error(W, Sigma, scale, zero, W_hat, codes, R, q, p, bits, sweeps,
                                        block, flags);
     if (bad != QE_OK) return bad;
+    if (bad_obj_in(flags, obj)) return QE_ERR_ARG;
     if (!ws || ws_bytes < cd_ws_bytes(q, p, block)) return QE_ERR_WORKSPACE;
     hipStream_t s = as_stream(stream);
     if (clear_status(ws, s) != QE_OK) return QE_ERR_HIP;
     return launch_cd(W, Sigma, q, p, bits, scale, zero, W_hat, codes, R, nullptr, sweeps, block,
-                     flags, obj, 1, ws, s);
+                     flags, obj, 1, (flags & QE_OBJ_IN) ? obj : nullptr, ws, s);
 }
 
 qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
@@ -176,6 +184,7 @@ qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int
     const qe_status bad = cd_arg_error(W, Sigma, scale, zero, W_hat, codes, R, q, p, bits, sweeps,
                                        block, flags);
     if (bad != QE_OK) return bad;
+    if (bad_obj_in(flags, obj)) return QE_ERR_ARG;
     if (cd_ws_bytes(q, p, block) > QE_NOALLOC_SCRATCH_BYTES) return QE_ERR_TOO_LARGE;
     hipStream_t s = as_stream(stream);
     void* ws = nullptr;
@@ -184,7 +193,7 @@ qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int
     // the previous call's status word is still there
     if (clear_status(ws, s) != QE_OK) return QE_ERR_HIP;
     st = launch_cd(W, Sigma, q, p, bits, scale, zero, W_hat, codes, R, nullptr, sweeps, block,
-                   flags, obj, 1, ws, s);
+                   flags, obj, 1, (flags & QE_OBJ_IN) ? obj : nullptr, ws, s);
     if (st != QE_OK) return st;
     if (status) {
         hipLaunchKernelGGL(status_copy_kernel, dim3(1), dim3(64), 0, s,

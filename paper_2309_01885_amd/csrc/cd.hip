@@ -149,55 +149,18 @@ __global__ __launch_bounds__(256) void obj_partial_kernel(const float* __restric
     if (threadIdx.x == 0) partial[blockIdx.x] = s;
 }
 
-// The same f after a quantized sweep, with What_ij = s_i (k_ij - z_i) formed
-// from the codes by the very expression the panel stores (so the value is
-// identical) and no fused multiply-add: 9 bytes per entry instead of 12.
-// Whole rows per workgroup.
-__global__ __launch_bounds__(256) void obj_codes_partial_kernel(
-    const float* __restrict__ W, const uint8_t* __restrict__ codes, const float* __restrict__ scale,
-    const float* __restrict__ zero, const float* __restrict__ R, int64_t q, int64_t p, int vec4,
-    double* partial, const int* status)
-{
-    if (failed(status)) return;
-    __shared__ double sh[256];
-    double acc = 0.0;
-    for (int64_t i = blockIdx.x; i < q; i += gridDim.x) {
-        const float s = scale[i], z = zero[i];
-        const int64_t o = i * p;
-        int64_t c0 = 0;
-        if (vec4) {
-            const f32x4* W4 = reinterpret_cast<const f32x4*>(W + o);
-            const f32x4* R4 = reinterpret_cast<const f32x4*>(R + o);
-            const uint32_t* K4 = reinterpret_cast<const uint32_t*>(codes + o);
-            for (int64_t c = threadIdx.x; c < p / 4; c += blockDim.x) {
-                const f32x4 w = W4[c], r = R4[c];
-                const uint32_t k = K4[c];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    const float wh = __fmul_rn(s, (float)((k >> (8 * u)) & 0xffu) - z);
-                    acc += (double)(wh - w[u]) * (double)r[u];
-                }
-            }
-            c0 = p / 4 * 4;
-        }
-        for (int64_t c = c0 + threadIdx.x; c < p; c += blockDim.x) {
-            const float wh = __fmul_rn(s, (float)codes[o + c] - z);
-            acc += (double)(wh - W[o + c]) * (double)R[o + c];
-        }
-    }
-    const double tot = block_sum_f64(acc, sh);
-    if (threadIdx.x == 0) partial[blockIdx.x] = tot;
-}
-
+// *out = (*prev, or 0 without prev) + the n partials, in a fixed order (out may
+// equal prev).
 __global__ __launch_bounds__(256) void sum_partials_kernel(const double* partial, int n,
-                                                           double* out, const int* status)
+                                                           const double* prev, double* out,
+                                                           const int* status)
 {
     if (failed(status)) return;
     __shared__ double sh[256];
     double acc = 0.0;
     for (int e = threadIdx.x; e < n; e += blockDim.x) acc += partial[e];
     const double s = block_sum_f64(acc, sh);
-    if (threadIdx.x == 0) *out = s;
+    if (threadIdx.x == 0) *out = (prev ? *prev : 0.0) + s;
 }
 
 // ---------------------------------------------------------------- the step kernel
@@ -226,6 +189,9 @@ struct StepArgs {
     int64_t tiles_n;      // GEMM column tiles
     int sig_vec4;
     int r_vec4;           // R allows aligned 16-byte row access
+    double* fpart;        // per panel wave: the objective change of this sweep's moves so far
+    int fobj;             // accumulate fpart (the per-sweep objective is wanted)
+    int ffirst;           // first launch of a sweep: fpart is written, not added to
     const int* status;
 };
 
@@ -240,6 +206,8 @@ struct PanelState {
     float v[SLOTS];     // quantized: What_ij / s_i + z_i (the code itself with code
                         // differences); relaxed: delta of owned columns
     float k[SLOTS];     // quantized: code of the column (NaN while none is valid)
+    float Ls;           // L of the current 16-column group's slot at the group's start
+    float fl;           // the row's objective change over the block (this lane's share)
     float srow[3][SLOTS];   // Sigma rows J, J+1, J+2 (lane's columns), fetched ahead
 };
 
@@ -274,6 +242,27 @@ __device__ __forceinline__ void load_srow(float (&dst)[SLOTS], const float* sS, 
     }
 }
 
+// Objective change of the moves delta_G of one 16-column group G, from the
+// residual R0 at the group's start: summed over the group's coordinate steps,
+// delta (2 R_ij + delta Sigma_jj) = 2 <delta_G, R0_G> + delta_G^T Sigma_GG
+// delta_G = <delta_G, R0_G + R1_G>, where R1 = R0 + Sigma_GG delta_G is the
+// slot's residual once the group is done (every lane's slot M column receives
+// all 16 moves of group M).  With code differences the lane's share is in
+// units of s_i.
+template <int SLOTS, int M, bool RELAX, bool INTD>
+__device__ __forceinline__ void group_objective(PanelState<SLOTS>& st, int g, int width, float s,
+                                                float z)
+{
+    float d;
+    if constexpr (RELAX)
+        d = st.v[M];
+    else if constexpr (INTD)
+        d = st.k[M] - st.v[M];
+    else
+        d = fmaf(s, st.k[M] - z, -st.w[M]);
+    if (16 * M + g < width) st.fl = fmaf(d, st.Ls + st.L[M], st.fl);
+}
+
 // One column update (column J of the block) for all 16 rows of the workgroup.
 // FULL blocks (width == B) carry no per-column test.  The Sigma row of column
 // J + 2 is fetched from LDS while column J's dependent chain runs.
@@ -283,7 +272,11 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
 {
     constexpr int B = 16 * SLOTS;
     constexpr int M = J / 16, O = J % 16;
-    if (!FULL && J >= width) return;                 // uniform across the workgroup
+    if constexpr (O == 0) st.Ls = st.L[M];
+    if (!FULL && J >= width) {                       // uniform across the workgroup
+        if constexpr (O == 15) group_objective<SLOTS, M, RELAX, INTD>(st, g, width, s, z);
+        return;
+    }
     if constexpr (J + 2 < B) load_srow<SLOTS, (J + 2) / 16>(st.srow[(J + 2) % 3], sS, J + 2, g);
     // keep the fetch here: the scheduler would otherwise sink it next to its use
     __builtin_amdgcn_sched_barrier(0);
@@ -316,6 +309,7 @@ __device__ __forceinline__ void panel_step(PanelState<SLOTS>& st, const float* s
     // Slot mm holds columns 16 mm + g; slots below M are finished this block.
 #pragma unroll
     for (int mm = M; mm < SLOTS; ++mm) st.L[mm] = fmaf(db, st.srow[J % 3][mm], st.L[mm]);
+    if constexpr (O == 15) group_objective<SLOTS, M, RELAX, INTD>(st, g, width, s, z);
 }
 
 template <int SLOTS, bool FULL, bool RELAX, bool INTD, int... Js>
@@ -617,6 +611,7 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
     const float inv_s = rowok ? a.inv_s[i] : 1.f;
     const int nsub = (int)cdiv(a.sbw, B);
     const float dscale = a.intd ? s : 1.f;
+    float fl = 0.f;        // this lane's share of its row's objective change (launch)
     // (1) look-ahead: the previous super-block's deltas on this one's columns
     //     (written to R: this launch's GEMM leaves these columns out)
     if (a.psb >= 0) lookahead(a, lds, i0, lrow, g, rowok, dscale);
@@ -625,6 +620,7 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
         const int64_t j0 = a.sb + (int64_t)sub * B;
         const int width = (int)min((int64_t)B, a.sb + a.sbw - j0);
         PanelState<SLOTS> st;
+        st.fl = 0.f;
         const bool cvalid = a.codes_valid != 0;
 #pragma unroll
         for (int m = 0; m < SLOTS; ++m) {
@@ -689,10 +685,22 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
             }
             if (rowok) a.dcur[i * a.S + (int64_t)sub * B + c] = d;
         }
+        fl += st.fl;
         // This block's deltas are read back only by this workgroup (its next
         // blocks), after the __syncthreads() that opens add_block_update: a
         // workgroup-scope release/acquire.  A device-scope fence here would
         // write back and invalidate L2 under the concurrent GEMM tiles.
+    }
+    if (a.fobj) {
+        // one fp64 partial per wave (4 rows), added to across the sweep's
+        // launches in stream order: a fixed summation order, no atomics
+        double fsum = rowok ? (double)(fl * dscale) : 0.0;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) fsum += __shfl_xor(fsum, o, 64);
+        if (lane == 0) {
+            double* slot = a.fpart + (((int64_t)blockIdx.x * 256 + threadIdx.x) >> 6);
+            *slot = a.ffirst ? fsum : *slot + fsum;
+        }
     }
 }
 
@@ -777,6 +785,8 @@ size_t cd_ws_bytes(int64_t q, int64_t p, int block)
     b += align256(sizeof(float) * q);               // inv_s
     b += 2 * align256(sizeof(float) * q * S);       // delta double buffer
     b += align256(sizeof(double) * kObjBlocks);     // objective partials
+    b += align256(sizeof(double) * 4 * cdiv(q, 16)); // per panel wave: objective change
+    b += align256(sizeof(double));                  // objective of the incoming state
     return b;
 }
 
@@ -788,8 +798,8 @@ qe_status launch_residual_dot(const float* W, const float* Wh, const float* H, c
     const int vec4 = aligned16(W) && aligned16(Wh) && aligned16(R) && (!H || aligned16(H));
     hipLaunchKernelGGL(obj_partial_kernel, dim3(kObjBlocks), dim3(256), 0, s, W, Wh, H, R, count,
                        vec4, part, status);
-    hipLaunchKernelGGL(sum_partials_kernel, dim3(1), dim3(256), 0, s, part, kObjBlocks, out,
-                       status);
+    hipLaunchKernelGGL(sum_partials_kernel, dim3(1), dim3(256), 0, s, part, kObjBlocks,
+                       (const double*)nullptr, out, status);
     return hipGetLastError() == hipSuccess ? QE_OK : QE_ERR_HIP;
 }
 
@@ -807,6 +817,7 @@ static qe_status launch_steps(StepArgs base, float* d0, float* d1, int64_t q, in
         a.sbw = t < nsb ? (int)std::min<int64_t>(S, p - t * S) : 0;
         a.psb = t > 0 ? (t - 1) * S : -1;
         a.psbw = t > 0 ? (int)std::min<int64_t>(S, p - (t - 1) * S) : 0;
+        a.ffirst = t == 0;
         a.dcur = (t & 1) ? d1 : d0;
         a.dprev = (t & 1) ? d0 : d1;
         a.n_panel = t < nsb ? (int)panel_wgs : 0;
@@ -822,7 +833,7 @@ static qe_status launch_steps(StepArgs base, float* d0, float* d1, int64_t q, in
 qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
                     const float* scale, const float* zero, float* Wh, uint8_t* codes, float* R,
                     const float* H, int sweeps, int block, uint32_t flags, double* obj,
-                    int obj_stride, void* ws, hipStream_t s)
+                    int obj_stride, const double* f_in, void* ws, hipStream_t s)
 {
     const int B = block_width(block);
     const int S = super_width(B);
@@ -833,6 +844,9 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     float* d0 = w.take<float>((size_t)q * S);
     float* d1 = w.take<float>((size_t)q * S);
     double* part = w.take<double>(kObjBlocks);
+    const int n_fpart = (int)(4 * cdiv(q, 16));
+    double* fpart = w.take<double>(n_fpart);
+    double* fstart = w.take<double>(1);
 
     if (flags & QE_DEBUG_CHECKS) {
         // every input of the call (the footnote to Lemma 1: checks before the sweeps)
@@ -859,6 +873,16 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
                            Sigma, q, p, R, vec4 ? 1 : 0, (flags & QE_CD_FP32) ? 1 : 0, status);
     }
     if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+    // The per-sweep objective is the incoming one plus the exact change of
+    // the sweep's coordinate moves, which the panel sums as it goes.  The
+    // incoming value: given (f_in), 0 after QE_INIT_FROM_W (What [+ H] = W),
+    // else one pass over R.
+    const double* f_prev = f_in;
+    if (obj && !f_in && !(flags & QE_INIT_FROM_W)) {
+        const qe_status st = launch_residual_dot(W, Wh, H, R, q * p, fstart, part, status, s);
+        if (st != QE_OK) return st;
+        f_prev = fstart;
+    }
 
     StepArgs base{};
     base.R = R;
@@ -876,6 +900,8 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     base.sig_vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
     base.r_vec4 = (aligned16(R) && p % 4 == 0) ? 1 : 0;
     base.fp32 = (flags & QE_CD_FP32) ? 1 : 0;
+    base.fpart = fpart;
+    base.fobj = obj ? 1 : 0;
     base.status = status;
     const bool codes_valid0 = (flags & QE_CODES_VALID) && !(flags & QE_INIT_FROM_W);
     const int period = (int)((flags & QE_RELAX_MASK) >> 8);
@@ -900,18 +926,12 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
             default: st = launch_steps<8>(base, d0, d1, q, p, s); break;
         }
         if (st != QE_OK) return st;
-        if (obj && !H && !base.relax) {
-            // a quantized sweep leaves What on the grid: read the codes instead
-            const int v4 = (p % 4 == 0 && aligned16(W) && aligned16(R) && aligned16(codes)) ? 1 : 0;
-            hipLaunchKernelGGL(obj_codes_partial_kernel, dim3(kObjBlocks), dim3(256), 0, s, W,
-                               codes, scale, zero, R, q, p, v4, part, status);
-            hipLaunchKernelGGL(sum_partials_kernel, dim3(1), dim3(256), 0, s, part, kObjBlocks,
-                               obj + (size_t)sw * obj_stride, status);
+        if (obj) {
+            double* out = obj + (size_t)sw * obj_stride;
+            hipLaunchKernelGGL(sum_partials_kernel, dim3(1), dim3(256), 0, s, fpart, n_fpart,
+                               f_prev, out, status);
             if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
-        } else if (obj) {
-            st = launch_residual_dot(W, Wh, H, R, q * p, obj + (size_t)sw * obj_stride, part,
-                                     status, s);
-            if (st != QE_OK) return st;
+            f_prev = out;
         }
     }
     return QE_OK;

@@ -823,8 +823,10 @@ qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t 
     for (int it = 0; it < sweeps; ++it) {
         const uint32_t f = it == 0 ? (flags & ~QE_OUTLIER_COLUMNS)
                                    : (QE_R_VALID | QE_CODES_VALID | (flags & QE_CD_FP32));
+        // the CD sweep's objective builds on g after the previous IHT step
         qe_status st = launch_cd(W, Sigma, q, p, bits, scale, zero, Wh, codes, E, H, 1, block, f,
-                                 obj ? obj + 2 * it : nullptr, 2, ws, hs);
+                                 obj ? obj + 2 * it : nullptr, 2,
+                                 obj && it > 0 ? obj + 2 * it - 1 : nullptr, ws, hs);
         if (st != QE_OK) return st;
         if (s > 0) {
             const int nxt = cur ^ 1;

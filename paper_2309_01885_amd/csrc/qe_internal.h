@@ -458,7 +458,7 @@ size_t cd_ws_bytes(int64_t q, int64_t p, int block);
 qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, int bits,
                     const float* scale, const float* zero, float* Wh, uint8_t* codes, float* R,
                     const float* H, int sweeps, int block, uint32_t flags, double* obj,
-                    int obj_stride, void* ws, hipStream_t s);
+                    int obj_stride, const double* f_in, void* ws, hipStream_t s);
 qe_status launch_residual_dot(const float* W, const float* Wh, const float* H, const float* R,
                               int64_t count, double* out, double* part, const int* status,
                               hipStream_t s);

@@ -38,6 +38,7 @@ QE_RELAX_MASK = 0xff00
 QE_OUTLIER_COLUMNS = 0x10
 QE_CD_FP32 = 0x20
 QE_DEBUG_CHECKS = 0x40
+QE_OBJ_IN = 0x80
 
 
 def QE_RELAX_PERIOD(k: int) -> int:

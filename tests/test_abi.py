@@ -118,6 +118,24 @@ def test_binding_names_follow_the_abi():
         assert callable(getattr(Q, n[len("qe_"):], None)), n
 
 
+def test_binding_constants_match_the_header():
+    """Every object-like QE_ macro of qe.h (status codes, layouts, flags,
+    sizes) has the same value in the binding and is re-exported by the
+    package."""
+    import paper_2309_01885_amd as P
+    import paper_2309_01885_amd.qe as Q
+    text = re.sub(r"/\*.*?\*/", " ", open(HEADER).read(), flags=re.S)
+    macros = re.findall(r"^#define[ \t]+(QE_[A-Z0-9_]+)[ \t]+(.+?)[ \t]*$", text, flags=re.M)
+    assert {"QE_OK", "QE_OBJ_IN", "QE_NOALLOC_SCRATCH_BYTES"} <= {n for n, _ in macros}
+    for name, raw in macros:
+        # integer literals (u suffix dropped) and shifts of them
+        expr = re.sub(r"\b(0x[0-9a-fA-F]+|[0-9]+)u\b", r"\1", raw)
+        assert re.fullmatch(r"[0-9a-fA-Fx()<< ]+", expr), (name, raw)
+        value = eval(expr)
+        assert getattr(Q, name) == value, name
+        assert getattr(P, name) == value, name
+
+
 # ------------------------------------------------------------------ argument errors
 # Host-detectable argument errors return before any HIP call (qe.h: errors),
 # so they are checked here without a GPU.  Pointers are dummies: none is
@@ -148,14 +166,15 @@ def test_gram_argument_errors(lib):
     assert _gram(L, ws_bytes=16) == QE_ERR_WORKSPACE
 
 
-def _cd(L, q=64, p=64, bits=4, sweeps=1, block=0, flags=0, ws=DUMMY, ws_bytes=1 << 40, W=DUMMY):
+def _cd(L, q=64, p=64, bits=4, sweeps=1, block=0, flags=0, ws=DUMMY, ws_bytes=1 << 40, W=DUMMY,
+        obj=NULL):
     f = L.qe_cd_sweep
     f.restype = ctypes.c_int
     f.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int,
                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                   ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p,
                   ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
-    return f(W, DUMMY, q, p, bits, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, sweeps, block, flags, NULL,
+    return f(W, DUMMY, q, p, bits, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, sweeps, block, flags, obj,
              ws, ws_bytes, NULL)
 
 
@@ -169,8 +188,12 @@ def test_cd_sweep_argument_errors(lib):
     assert _cd(L, block=48) == QE_ERR_ARG         # block widths 16, 32, 64, 128 (0 = default)
     assert _cd(L, sweeps=-1) == QE_ERR_ARG
     assert _cd(L, flags=0x10) == QE_ERR_ARG       # QE_OUTLIER_COLUMNS belongs to the outlier call
-    assert _cd(L, flags=0x80) == QE_ERR_ARG       # no such flag
+    assert _cd(L, flags=0x10000) == QE_ERR_ARG    # no such flag
     assert _cd(L, flags=0x40, ws=NULL) == QE_ERR_WORKSPACE   # QE_DEBUG_CHECKS is accepted
+    # QE_OBJ_IN reads obj[0]: it needs obj, and not with QE_INIT_FROM_W
+    assert _cd(L, flags=0x80) == QE_ERR_ARG
+    assert _cd(L, flags=0x80 | 0x1, obj=DUMMY) == QE_ERR_ARG
+    assert _cd(L, flags=0x80 | 0x2, obj=DUMMY, ws=NULL) == QE_ERR_WORKSPACE
     assert _cd(L, ws=NULL) == QE_ERR_WORKSPACE
     assert _cd(L, ws_bytes=1024) == QE_ERR_WORKSPACE
 
@@ -187,10 +210,12 @@ def test_cd_sweep_noalloc_argument_errors(lib):
                   ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_uint32, ctypes.c_void_p,
                   ctypes.c_void_p, ctypes.c_void_p]
 
-    def call(W=DUMMY, q=64, p=64, bits=4, block=0):
-        return f(W, DUMMY, q, p, bits, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 1, block, 0, NULL, NULL,
-                 NULL)
+    def call(W=DUMMY, q=64, p=64, bits=4, block=0, flags=0, obj=NULL):
+        return f(W, DUMMY, q, p, bits, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, 1, block, flags, obj,
+                 NULL, NULL)
     assert call(W=NULL) == QE_ERR_ARG
+    assert call(flags=0x80) == QE_ERR_ARG              # QE_OBJ_IN without obj
+    assert call(flags=0x81, obj=DUMMY) == QE_ERR_ARG   # QE_OBJ_IN with QE_INIT_FROM_W
     assert call(bits=9) == QE_ERR_ARG
     assert call(block=48) == QE_ERR_ARG
     L.qe_cd_workspace_size.restype = ctypes.c_size_t

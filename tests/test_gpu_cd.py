@@ -46,10 +46,11 @@ def gpu_cd(qe, W, S32, bits, scale, zero, sweeps, block=0, per_sweep=True, W0=No
     flags |= extra
     hist, objs, whats, Rs = [], [], [], []
     if per_sweep:
+        # one call per sweep, the objective carried from call to call (QE_OBJ_IN)
+        obj = torch.zeros(1, dtype=torch.float64, device="cuda")
         for k in range(sweeps):
-            obj = torch.zeros(1, dtype=torch.float64, device="cuda")
             qe.cd_sweep(Wd, Sd, bits, sc, ze, Wh, codes, R, 1, block=block, flags=flags, obj=obj)
-            flags = qe.QE_R_VALID | qe.QE_CODES_VALID | extra
+            flags = qe.QE_R_VALID | qe.QE_CODES_VALID | qe.QE_OBJ_IN | extra
             hist.append(host(codes).astype(np.int32))
             objs.append(float(host(obj)[0]))
             whats.append(host(Wh))
@@ -167,6 +168,39 @@ def test_multi_sweep_call_equals_resumed_calls(qe, oracle):
     assert np.array_equal(a["codes"], b["codes"])
     assert np.array_equal(a["R"], b["R"])
     assert a["obj"] == b["obj"]
+
+
+def test_objective_paths_agree(qe, oracle):
+    """The per-sweep objective is the incoming one plus the exact change of
+    the sweep's coordinate moves (Lemma 1's one-dimensional quadratic).  The
+    incoming value comes three ways: 0 from What = W (one multi-sweep call),
+    carried in obj[0] (QE_OBJ_IN, per-sweep calls: bitwise the same as the
+    multi-sweep call), or one pass <What - W, R> at the start of each resumed
+    call.  All three follow the fp64 objective of the GPU's own What after
+    every sweep, on a ragged shape (partial panel block and GEMM tiles)."""
+    W, X = layer(150, 333, 1024, 31, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    sweeps = 5
+    multi = gpu_cd(qe, W, S32, 4, scale, zero, sweeps, per_sweep=False)
+    carried = gpu_cd(qe, W, S32, 4, scale, zero, sweeps, per_sweep=True)
+    assert multi["obj"] == carried["obj"]
+    Wd, Sd, sc, ze = dev(W), dev(S32), dev(scale), dev(zero)
+    Wh, R = torch.empty_like(Wd), torch.empty_like(Wd)
+    codes = torch.zeros(W.shape, dtype=torch.uint8, device="cuda")
+    flags = qe.QE_INIT_FROM_W
+    for k in range(sweeps):
+        obj = torch.zeros(1, dtype=torch.float64, device="cuda")
+        qe.cd_sweep(Wd, Sd, 4, sc, ze, Wh, codes, R, 1, flags=flags, obj=obj)
+        flags = qe.QE_R_VALID | qe.QE_CODES_VALID
+        f_ref = oracle.objective(W, carried["whats"][k], S32)
+        assert np.array_equal(host(Wh), carried["whats"][k])
+        f_pass = float(host(obj)[0])
+        print(f"sweep {k + 1}: f {f_ref:.9e}, carried rel err "
+              f"{abs(carried['obj'][k] - f_ref) / f_ref:.2e}, start-pass rel err "
+              f"{abs(f_pass - f_ref) / f_ref:.2e}")
+        assert carried["obj"][k] == pytest.approx(f_ref, rel=1e-5)
+        assert f_pass == pytest.approx(f_ref, rel=1e-5)
 
 
 def test_deterministic(qe, oracle):
