@@ -301,16 +301,26 @@ def main():
 
     # ---- dominant kernels, measured live on this stream
     # block-update step kernel: sweeps resumed from a valid R, no objective,
-    # so the region holds only the step launches (+2 tiny setup kernels)
+    # so the region holds only the step launches (+2 tiny setup kernels);
+    # every block update on the matrix cores (QE_CD_DENSE), so that the
+    # roofline does not count the exact zeros the default path skips
     super_w = max(256, block)                     # columns per step launch (super-block)
     nb = (p + super_w - 1) // super_w
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    P.cd_sweep(W, Sigma, bits, scale, zero, Wh, codes, R, sweeps, block=block,
-               flags=P.QE_R_VALID | P.QE_CODES_VALID, obj=None, ws=ws_cd, check=False)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    t_steps = e0.elapsed_time(e1) * 1e-3
+
+    def resumed_sweeps(extra):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        P.cd_sweep(W, Sigma, bits, scale, zero, Wh, codes, R, sweeps, block=block,
+                   flags=P.QE_R_VALID | P.QE_CODES_VALID | extra, obj=None, ws=ws_cd,
+                   check=False)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e-3
+
+    t_steps = resumed_sweeps(P.QE_CD_DENSE)
+    # the same sweeps on the default path: past convergence almost no code
+    # moves, and the block update applies only the few nonzero differences
+    t_converged = resumed_sweeps(0) / sweeps
     # one sweep per call from W = What: events around each of sweeps 2..K
     # (with its objective, carried from call to call as inside the step's
     # multi-sweep call), median
@@ -327,7 +337,8 @@ def main():
         a1.record(stream)
         per_sweep.append((a0, a1))
     torch.cuda.synchronize()
-    sweep_median_2_k = float(np.median([a.elapsed_time(b) * 1e-3 for a, b in per_sweep[1:]]))
+    sweep_times_single = [a.elapsed_time(b) * 1e-3 for a, b in per_sweep]
+    sweep_median_2_k = float(np.median(sweep_times_single[1:]))
     launches = sweeps * (nb + 1)
     cd_avg = t_steps / launches
     gram_t = float(np.median(phase["gram"]))
@@ -425,6 +436,8 @@ def main():
                         "exact_objective": float(np.median(phase["exact"]))},
         "sweep_time_s": sweep_t,
         "sweep_time_median_2_to_k_s": sweep_median_2_k,
+        "sweep_times_single_calls_s": sweep_times_single,
+        "sweep_time_converged_s": t_converged,
         "cd_column_updates_per_s": value,
         "cd_coordinate_updates_per_s": q * value,
         "layer_time_s": ms_per_step / 1e3,

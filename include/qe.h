@@ -82,6 +82,14 @@ typedef int qe_status;
  * nothing).  One extra read of those arrays (about 30 us at 4096 x 4096).
  * Without the flag only Sigma's diagonal and the grid are checked. */
 #define QE_DEBUG_CHECKS 0x40u
+/* Every block update on the matrix cores.  By default, from the second sweep
+ * on (codes valid), a 128 x 128 tile of the block update whose rows changed
+ * few codes in the super-block just finished (at most 64 rows, each at most 32
+ * codes) applies only those nonzero code differences, as fp32 FMAs; its
+ * other rows' update is exactly 0 and is skipped.  Both forms give R up to
+ * fp32 rounding; with this flag R's rounding does not depend on how many
+ * codes moved. */
+#define QE_CD_DENSE 0x10000u
 /* qe_cd_sweep only: obj[0] holds, on entry, the objective f of the incoming
  * What and R (e.g. the last value of the previous call), so that chained
  * calls report f without a pass over R.  Needs obj; not with QE_INIT_FROM_W
@@ -150,7 +158,7 @@ qe_status qe_grid_minmax(const float* W, const float* H, int64_t q, int64_t p, i
  * R:      q x p, device, in/out: (What - W) Sigma on exit.
  * sweeps: >= 0 full passes over the columns.
  * flags:  QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_PERIOD(k)
- *         | QE_CD_FP32 | QE_DEBUG_CHECKS | QE_OBJ_IN.
+ *         | QE_CD_FP32 | QE_CD_DENSE | QE_DEBUG_CHECKS | QE_OBJ_IN.
  *         Without QE_INIT_FROM_W and without QE_R_VALID, R is first
  *         computed as (What - W) Sigma (warm start from any What, Sec. 3.1).
  * obj:    NULL, or device array of `sweeps` doubles receiving
@@ -213,7 +221,7 @@ qe_status qe_cd_sweep_noalloc(const float* W, const float* Sigma, int64_t q, int
  *           QE_OUTLIER_COLUMNS: structured outliers (whole columns); start
  *           from qe_topk_columns on W.
  *           Without QE_INIT_FROM_W / QE_R_VALID, E = (What + H - W) Sigma.
- *           QE_CD_FP32 and QE_DEBUG_CHECKS as for qe_cd_sweep.
+ *           QE_CD_FP32, QE_CD_DENSE and QE_DEBUG_CHECKS as for qe_cd_sweep.
  * obj:      NULL or device array of 2*sweeps doubles: obj[2k] = g after the
  *           CD sweep of iteration k (g after the previous IHT step, or at
  *           the start, plus the exact change of the sweep's moves, as for

@@ -39,7 +39,7 @@ qe_status cd_arg_error(const float* W, const float* Sigma, const float* scale, c
     if (!W || !Sigma || !scale || !zero || !W_hat || !codes || !R) return QE_ERR_ARG;
     if (bad_dims(q, p) || bad_bits(bits) || bad_block(block) || sweeps < 0) return QE_ERR_ARG;
     if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_RELAX_MASK | QE_CD_FP32 |
-                  QE_DEBUG_CHECKS | QE_OBJ_IN))
+                  QE_CD_DENSE | QE_DEBUG_CHECKS | QE_OBJ_IN))
         return QE_ERR_ARG;
     return QE_OK;
 }
@@ -223,7 +223,7 @@ qe_status qe_cd_outlier_sweep(const float* W, const float* Sigma, int64_t q, int
     if (s < 0 || s > q * p || (s > 0 && !support)) return QE_ERR_ARG;
     if (!(lambda_max > 0.f) || !std::isfinite(lambda_max)) return QE_ERR_ARG;
     if (flags & ~(QE_INIT_FROM_W | QE_R_VALID | QE_CODES_VALID | QE_OUTLIER_COLUMNS | QE_CD_FP32 |
-                  QE_DEBUG_CHECKS))
+                  QE_CD_DENSE | QE_DEBUG_CHECKS))
         return QE_ERR_ARG;
     if (!ws || ws_bytes < outlier_ws_bytes(q, p, block, s)) return QE_ERR_WORKSPACE;
     hipStream_t st = as_stream(stream);

@@ -185,10 +185,13 @@ struct StepArgs {
     int relax;            // write beta unquantized (relaxed sweep, Sec. 3.2)
     int intd;             // deltas as code differences k_new - k_old (see launch_cd)
     int fp32;             // GEMM role on the fp32 matrix cores (else the split bf16 ones)
+    int dense;            // no sparse block update (every tile on the matrix cores)
     int n_panel;          // workgroups [0, n_panel) run the panel
     int64_t tiles_n;      // GEMM column tiles
     int sig_vec4;
     int r_vec4;           // R allows aligned 16-byte row access
+    int* nzcur;           // q: nonzero code differences of each row in the current super-block
+    const int* nzprev;    // q: the same for the previous super-block (code differences only)
     double* fpart;        // per panel wave: the objective change of this sweep's moves so far
     int fobj;             // accumulate fpart (the per-sweep objective is wanted)
     int ffirst;           // first launch of a sweep: fpart is written, not added to
@@ -612,6 +615,7 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
     const int nsub = (int)cdiv(a.sbw, B);
     const float dscale = a.intd ? s : 1.f;
     float fl = 0.f;        // this lane's share of its row's objective change (launch)
+    int nz = 0;            // this lane's nonzero code differences (launch)
     // (1) look-ahead: the previous super-block's deltas on this one's columns
     //     (written to R: this launch's GEMM leaves these columns out)
     if (a.psb >= 0) lookahead(a, lds, i0, lrow, g, rowok, dscale);
@@ -684,8 +688,15 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
                 }
             }
             if (rowok) a.dcur[i * a.S + (int64_t)sub * B + c] = d;
+            nz += d != 0.f;
         }
         fl += st.fl;
+        if (a.intd && sub == nsub - 1) {
+            // the row's count over its 16 lanes, for the next launch's block update
+#pragma unroll
+            for (int o = 8; o > 0; o >>= 1) nz += __shfl_xor(nz, o, 16);
+            if (g == 0 && rowok) a.nzcur[i] = nz;
+        }
         // This block's deltas are read back only by this workgroup (its next
         // blocks), after the __syncthreads() that opens add_block_update: a
         // workgroup-scope release/acquire.  A device-scope fence here would
@@ -707,12 +718,162 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
 // R's tile is read only after the K loop (through an LDS-staged, float4-wide
 // read-modify-write): holding it across the loop would cost 64 registers and
 // the second workgroup per CU, which matters more than hiding its latency.
+// A tile takes the sparse path when at most kSparseRows of its rows changed a
+// code in the previous super-block, none of them more than kSparseRowNz
+// codes.  A wave takes its rows kSpPass at a time, with the loads of each
+// phase of those rows in flight together: two memory round trips per pass,
+// plus one per further kSpGroup nonzeros of its busiest row (a dense tile
+// costs a whole K loop).
+constexpr int kSparseRows = 64;
+constexpr int kSparseRowNz = 32;
+constexpr int kSpPass = 8;
+constexpr int kSpGroup = 4;
+
+// Block update of a tile whose rows hold few nonzero code differences (late
+// sweeps, where most codes are kept and their differences are exact zeros):
+// R_ic += s_i sum_k D_ik Sigma_kc over the nonzero D_ik only, in increasing
+// k, as fp32 FMAs.  Rows without a nonzero difference are left as they are
+// (their update is 0).  The active rows are listed in LDS with their counts;
+// wave w takes list entries w, w + 4, ..., lane l holding columns 2l and
+// 2l + 1.  Per pass of kSpPass rows: the D rows (lane l: k = l + 64 e) and R
+// segments are loaded; each row's nonzeros are written, in k order, to the
+// wave's LDS area (positions from the ballots); then all their Sigma
+// segments are loaded, then R is updated.  nz: this thread's row count
+// (threads < 128).
+__device__ void gemm_sparse(const StepArgs& a, int* li, int nz, int active, int64_t row0,
+                            int64_t col0, int64_t ex0, int64_t ex1)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int* cnt = li;                                   // 2: active rows among tile rows 0-63, 64-127
+    int* list = li + 2;                              // kSparseRows tile row offsets, ascending
+    int* lcount = list + kSparseRows;                // their counts
+    int2* ent = reinterpret_cast<int2*>(lcount + kSparseRows) +
+                wave * kSpPass * kSparseRowNz;       // this wave's (k, d) entries
+    uint64_t b = 0;
+    if (wave < 2) {
+        b = __ballot(nz > 0);
+        if (lane == 0) cnt[wave] = __popcll(b);
+    }
+    __syncthreads();
+    if (wave < 2 && nz > 0) {
+        const int j = (wave == 1 ? cnt[0] : 0) + (int)__popcll(b & ((1ull << lane) - 1ull));
+        list[j] = (int)threadIdx.x;
+        lcount[j] = nz;
+    }
+    __syncthreads();
+
+    const uint64_t below = (1ull << lane) - 1ull;
+    const int64_t c0 = col0 + 2 * lane;
+    const bool ok0 = c0 < a.p && !(c0 >= ex0 && c0 < ex1);
+    const bool ok1 = c0 + 1 < a.p && !(c0 + 1 >= ex0 && c0 + 1 < ex1);
+    const bool pair = a.sig_vec4 && a.r_vec4 && c0 + 1 < a.p;   // 8-byte aligned pairs
+    for (int j0 = wave; j0 < active; j0 += 4 * kSpPass) {
+        int64_t ir[kSpPass];
+        int cn[kSpPass];
+        float dv[kSpPass][4], r0v[kSpPass], r1v[kSpPass];
+#pragma unroll
+        for (int u = 0; u < kSpPass; ++u) {
+            const int j = j0 + 4 * u;
+            ir[u] = j < active ? row0 + list[j] : -1;    // uniform
+            cn[u] = j < active ? lcount[j] : 0;
+            r0v[u] = r1v[u] = 0.f;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) dv[u][e] = 0.f;
+            if (ir[u] < 0) continue;
+            const float* drow = a.dprev + ir[u] * a.S;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int k = lane + 64 * e;
+                if (k < a.psbw) dv[u][e] = drow[k];
+            }
+            const float* rrow = a.R + ir[u] * a.p;
+            if (pair) {
+                const f32x2 v = *reinterpret_cast<const f32x2*>(rrow + c0);
+                r0v[u] = v[0];
+                r1v[u] = v[1];
+            } else {
+                if (c0 < a.p) r0v[u] = rrow[c0];
+                if (c0 + 1 < a.p) r1v[u] = rrow[c0 + 1];
+            }
+        }
+        // each row's nonzeros, in increasing k, to the wave's LDS area
+#pragma unroll
+        for (int u = 0; u < kSpPass; ++u) {
+            if (ir[u] < 0) continue;
+            int base = 0;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const bool on = dv[u][e] != 0.f;
+                const uint64_t m = __ballot(on);
+                if (on)
+                    ent[u * kSparseRowNz + base + (int)__popcll(m & below)] =
+                        make_int2(lane + 64 * e, __float_as_int(dv[u][e]));
+                base += (int)__popcll(m);
+            }
+        }
+        // Sigma segments of kSpGroup nonzeros per row at a time, all rows at once
+        int cmax = 0;
+#pragma unroll
+        for (int u = 0; u < kSpPass; ++u) cmax = max(cmax, cn[u]);
+        float acc0[kSpPass], acc1[kSpPass];
+#pragma unroll
+        for (int u = 0; u < kSpPass; ++u) acc0[u] = acc1[u] = 0.f;
+        for (int n0 = 0; n0 < cmax; n0 += kSpGroup) {
+            float dn[kSpPass][kSpGroup], s0[kSpPass][kSpGroup], s1[kSpPass][kSpGroup];
+#pragma unroll
+            for (int u = 0; u < kSpPass; ++u)
+#pragma unroll
+                for (int n = 0; n < kSpGroup; ++n) {
+                    dn[u][n] = s0[u][n] = s1[u][n] = 0.f;
+                    if (n0 + n >= cn[u]) continue;       // uniform
+                    const int2 en = ent[u * kSparseRowNz + n0 + n];
+                    dn[u][n] = __int_as_float(en.y);
+                    const float* srow = a.Sigma + (a.psb + en.x) * a.p;
+                    if (pair) {
+                        const f32x2 sv = *reinterpret_cast<const f32x2*>(srow + c0);
+                        s0[u][n] = sv[0];
+                        s1[u][n] = sv[1];
+                    } else {
+                        if (c0 < a.p) s0[u][n] = srow[c0];
+                        if (c0 + 1 < a.p) s1[u][n] = srow[c0 + 1];
+                    }
+                }
+#pragma unroll
+            for (int u = 0; u < kSpPass; ++u)
+#pragma unroll
+                for (int n = 0; n < kSpGroup; ++n) {
+                    acc0[u] = fmaf(dn[u][n], s0[u][n], acc0[u]);
+                    acc1[u] = fmaf(dn[u][n], s1[u][n], acc1[u]);
+                }
+        }
+#pragma unroll
+        for (int u = 0; u < kSpPass; ++u) {
+            if (ir[u] < 0) continue;
+            const float si = a.scale[ir[u]];
+            float* rrow = a.R + ir[u] * a.p;
+            if (ok0) rrow[c0] = fmaf(si, acc0[u], r0v[u]);
+            if (ok1) rrow[c0 + 1] = fmaf(si, acc1[u], r1v[u]);
+        }
+    }
+}
+
 __device__ __forceinline__ void gemm_role(const StepArgs& a, float* lds, int64_t t)
 {
     const int64_t tm = t / a.tiles_n, tn = t % a.tiles_n;
     const int64_t row0 = tm * kTile, col0 = tn * kTile;
     const int64_t ex0 = a.sb >= 0 ? a.sb : 0, ex1 = a.sb >= 0 ? a.sb + a.sbw : 0;
     if (a.sb >= 0 && col0 >= ex0 && min(col0 + kTile, a.p) <= ex1) return;   // all excluded
+    if (a.intd && !a.dense) {
+        // rows of the tile that changed a code in the previous super-block
+        int nz = 0;
+        if (threadIdx.x < kTile && row0 + threadIdx.x < a.q) nz = a.nzprev[row0 + threadIdx.x];
+        const int active = __syncthreads_count(nz > 0);
+        const int heavy = __syncthreads_count(nz > kSparseRowNz);
+        if (active <= kSparseRows && heavy == 0) {
+            gemm_sparse(a, reinterpret_cast<int*>(lds), nz, active, row0, col0, ex0, ex1);
+            return;
+        }
+    }
     f32x16 acc[2][2];
     zero_acc(acc);
     if (a.fp32) {
@@ -784,6 +945,7 @@ size_t cd_ws_bytes(int64_t q, int64_t p, int block)
     b += align256(sizeof(float) * p);               // inv_d
     b += align256(sizeof(float) * q);               // inv_s
     b += 2 * align256(sizeof(float) * q * S);       // delta double buffer
+    b += 2 * align256(sizeof(int) * q);             // nonzero-difference counts, double buffer
     b += align256(sizeof(double) * kObjBlocks);     // objective partials
     b += align256(sizeof(double) * 4 * cdiv(q, 16)); // per panel wave: objective change
     b += align256(sizeof(double));                  // objective of the incoming state
@@ -804,8 +966,8 @@ qe_status launch_residual_dot(const float* W, const float* Wh, const float* H, c
 }
 
 template <int SLOTS>
-static qe_status launch_steps(StepArgs base, float* d0, float* d1, int64_t q, int64_t p,
-                              hipStream_t s)
+static qe_status launch_steps(StepArgs base, float* d0, float* d1, int* nz0, int* nz1,
+                              int64_t q, int64_t p, hipStream_t s)
 {
     const int S = base.S;
     const int64_t nsb = cdiv(p, S);
@@ -820,6 +982,8 @@ static qe_status launch_steps(StepArgs base, float* d0, float* d1, int64_t q, in
         a.ffirst = t == 0;
         a.dcur = (t & 1) ? d1 : d0;
         a.dprev = (t & 1) ? d0 : d1;
+        a.nzcur = (t & 1) ? nz1 : nz0;
+        a.nzprev = (t & 1) ? nz0 : nz1;
         a.n_panel = t < nsb ? (int)panel_wgs : 0;
         a.tiles_n = tiles_n;
         const int64_t gemm_wgs = t > 0 ? tiles_m * tiles_n : 0;
@@ -843,6 +1007,8 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     float* inv_s = w.take<float>(q);
     float* d0 = w.take<float>((size_t)q * S);
     float* d1 = w.take<float>((size_t)q * S);
+    int* nz0 = w.take<int>(q);
+    int* nz1 = w.take<int>(q);
     double* part = w.take<double>(kObjBlocks);
     const int n_fpart = (int)(4 * cdiv(q, 16));
     double* fpart = w.take<double>(n_fpart);
@@ -900,6 +1066,7 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
     base.sig_vec4 = (aligned16(Sigma) && p % 4 == 0) ? 1 : 0;
     base.r_vec4 = (aligned16(R) && p % 4 == 0) ? 1 : 0;
     base.fp32 = (flags & QE_CD_FP32) ? 1 : 0;
+    base.dense = (flags & QE_CD_DENSE) ? 1 : 0;
     base.fpart = fpart;
     base.fobj = obj ? 1 : 0;
     base.status = status;
@@ -920,10 +1087,10 @@ qe_status launch_cd(const float* W, const float* Sigma, int64_t q, int64_t p, in
         prev_relaxed = base.relax != 0;
         qe_status st;
         switch (B) {
-            case 16: st = launch_steps<1>(base, d0, d1, q, p, s); break;
-            case 32: st = launch_steps<2>(base, d0, d1, q, p, s); break;
-            case 64: st = launch_steps<4>(base, d0, d1, q, p, s); break;
-            default: st = launch_steps<8>(base, d0, d1, q, p, s); break;
+            case 16: st = launch_steps<1>(base, d0, d1, nz0, nz1, q, p, s); break;
+            case 32: st = launch_steps<2>(base, d0, d1, nz0, nz1, q, p, s); break;
+            case 64: st = launch_steps<4>(base, d0, d1, nz0, nz1, q, p, s); break;
+            default: st = launch_steps<8>(base, d0, d1, nz0, nz1, q, p, s); break;
         }
         if (st != QE_OK) return st;
         if (obj) {

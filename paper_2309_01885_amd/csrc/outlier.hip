@@ -822,7 +822,8 @@ qe_status launch_outlier(const float* W, const float* Sigma, int64_t q, int64_t 
     int cur = 0;
     for (int it = 0; it < sweeps; ++it) {
         const uint32_t f = it == 0 ? (flags & ~QE_OUTLIER_COLUMNS)
-                                   : (QE_R_VALID | QE_CODES_VALID | (flags & QE_CD_FP32));
+                                   : (QE_R_VALID | QE_CODES_VALID |
+                                      (flags & (QE_CD_FP32 | QE_CD_DENSE)));
         // the CD sweep's objective builds on g after the previous IHT step
         qe_status st = launch_cd(W, Sigma, q, p, bits, scale, zero, Wh, codes, E, H, 1, block, f,
                                  obj ? obj + 2 * it : nullptr, 2,

@@ -37,6 +37,7 @@ QE_CODES_VALID = 0x4
 QE_RELAX_MASK = 0xff00
 QE_OUTLIER_COLUMNS = 0x10
 QE_CD_FP32 = 0x20
+QE_CD_DENSE = 0x10000
 QE_DEBUG_CHECKS = 0x40
 QE_OBJ_IN = 0x80
 

@@ -188,7 +188,8 @@ def test_cd_sweep_argument_errors(lib):
     assert _cd(L, block=48) == QE_ERR_ARG         # block widths 16, 32, 64, 128 (0 = default)
     assert _cd(L, sweeps=-1) == QE_ERR_ARG
     assert _cd(L, flags=0x10) == QE_ERR_ARG       # QE_OUTLIER_COLUMNS belongs to the outlier call
-    assert _cd(L, flags=0x10000) == QE_ERR_ARG    # no such flag
+    assert _cd(L, flags=0x20000) == QE_ERR_ARG    # no such flag
+    assert _cd(L, flags=0x10000, ws=NULL) == QE_ERR_WORKSPACE   # QE_CD_DENSE is accepted
     assert _cd(L, flags=0x40, ws=NULL) == QE_ERR_WORKSPACE   # QE_DEBUG_CHECKS is accepted
     # QE_OBJ_IN reads obj[0]: it needs obj, and not with QE_INIT_FROM_W
     assert _cd(L, flags=0x80) == QE_ERR_ARG

@@ -224,6 +224,55 @@ def test_residual_is_exact_after_sweeps(qe, oracle, q, p, fp32):
     assert np.all(np.abs(g["R"] - R_ref) <= 1e-5 * scale_R + 1e-30)
 
 
+def block_update_regimes(hist, q, p, tile=128, super_w=256, rows_max=64, row_nz_max=32):
+    """For every sweep that starts from valid codes, the number of (row tile,
+    super-block) block updates that take the sparse path and the dense one,
+    worked out from the codes alone: a tile's rows may each have changed at
+    most row_nz_max codes of the super-block, and at most rows_max rows any."""
+    out = []
+    for k in range(1, len(hist)):
+        moved = hist[k] != hist[k - 1]
+        sparse = dense = 0
+        for c0 in range(0, p, super_w):
+            per_row = moved[:, c0:c0 + super_w].sum(axis=1)
+            for r0 in range(0, q, tile):
+                rows = per_row[r0:r0 + tile]
+                if (rows > 0).sum() <= rows_max and rows.max() <= row_nz_max:
+                    sparse += 1
+                else:
+                    dense += 1
+        out.append((sparse, dense))
+    return out
+
+
+@pytest.mark.parametrize("q,p", [(512, 1024), (300, 777)])
+def test_sparse_block_update(qe, oracle, q, p):
+    """From the second sweep on, a block-update tile whose rows changed few
+    codes applies only the nonzero code differences (QE_CD_DENSE turns this
+    off).  Over 12 sweeps the run passes from dense to sparse tiles (checked
+    from the codes); every sweep meets the parity bar against the oracle and
+    leaves R = (What - W) Sigma to fp32 rounding, and the matrix-core-only
+    run reaches the same objective."""
+    W, X = layer(q, p, 2048, 43, corr=0.9)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, 4)
+    sweeps = 12
+    g = gpu_cd(qe, W, S32, 4, scale, zero, sweeps)
+    regimes = block_update_regimes(g["hist"], q, p)
+    print(f"{q}x{p}: (sparse, dense) block updates per sweep 2..{sweeps}: {regimes}")
+    assert regimes[0][1] > 0                              # sweep 2: dense tiles
+    assert sum(sp for sp, _ in regimes) > 0               # later: sparse tiles
+    check_parity(oracle, W, S32, 4, scale, zero, g, f"sparse {q}x{p}")
+    S64 = S32.astype(np.float64)
+    for k in range(sweeps):
+        D = g["whats"][k].astype(np.float64) - W
+        bound = 1e-5 * (np.abs(D) @ np.abs(S64)) + 1e-30
+        assert np.all(np.abs(g["Rs"][k] - D @ S64) <= bound), f"sweep {k + 1}"
+    d = gpu_cd(qe, W, S32, 4, scale, zero, sweeps, extra=qe.QE_CD_DENSE)
+    check_parity(oracle, W, S32, 4, scale, zero, d, f"dense {q}x{p}")
+    assert d["obj"][-1] == pytest.approx(g["obj"][-1], rel=1e-6)
+
+
 def test_on_grid_weights_bitwise(qe, oracle):
     q, p = 100, 230
     k = synth.integers((q, p), seed=20, lo=0, hi=16)
