@@ -597,6 +597,81 @@ __device__ __forceinline__ void lookahead(const StepArgs& a, float* lds, int64_t
     }
 }
 
+// The look-ahead when the workgroup's rows changed few codes in the previous
+// super-block (code differences; each row at most kLaNz): the row's nonzero
+// D_ik, listed in LDS through ballots over its 16 lanes, are applied to the
+// lane's own columns of this super-block (c = 16 m + g, the layout of the
+// dense look-ahead and of the panels' later R loads) as fp32 FMAs, kLaGroup
+// of them per round of Sigma loads; rows without one are left as they are.
+// cnt: the row's count.  Uses the first 16 * kLaNz int2 of LDS, wave-locally.
+constexpr int kLaNz = 8;
+constexpr int kLaGroup = 4;
+
+__device__ __forceinline__ void lookahead_sparse(const StepArgs& a, float* lds, int64_t i0,
+                                                 int lrow, int g, bool rowok, float dscale,
+                                                 int cnt)
+{
+    const int lane = threadIdx.x & 63;
+    int2* ent = reinterpret_cast<int2*>(lds) + lrow * kLaNz;
+    const int64_t i = i0 + lrow;
+    // the row's D over the previous super-block: lane g holds k = 64 w + 4 g + c
+    float dv[4][4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const int k = 64 * w + 4 * g + c;
+            dv[w][c] = (cnt > 0 && k < a.psbw) ? a.dprev[i * a.S + k] : 0.f;
+        }
+    const int shift = 16 * (lane >> 4);
+    const uint32_t below = (1u << g) - 1u;
+    int base = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+            const bool on = dv[w][c] != 0.f;
+            const uint32_t rb = (uint32_t)(__ballot(on) >> shift) & 0xffffu;
+            if (on) {
+                const int pos = base + __popc(rb & below);
+                if (pos < kLaNz) ent[pos] = make_int2(64 * w + 4 * g + c, __float_as_int(dv[w][c]));
+            }
+            base += __popc(rb);
+        }
+    if (!rowok || cnt == 0) return;
+    float acc[kLaCols / 16];
+#pragma unroll
+    for (int m = 0; m < kLaCols / 16; ++m) acc[m] = 0.f;
+    for (int n0 = 0; n0 < cnt; n0 += kLaGroup) {
+        float dn[kLaGroup], sv[kLaGroup][kLaCols / 16];
+#pragma unroll
+        for (int n = 0; n < kLaGroup; ++n) {
+            dn[n] = 0.f;
+#pragma unroll
+            for (int m = 0; m < kLaCols / 16; ++m) sv[n][m] = 0.f;
+            if (n0 + n >= cnt) continue;
+            const int2 en = ent[n0 + n];
+            dn[n] = __int_as_float(en.y);
+            const float* srow = a.Sigma + (a.psb + en.x) * a.p + a.sb;
+#pragma unroll
+            for (int m = 0; m < kLaCols / 16; ++m)
+                if (16 * m + g < a.sbw) sv[n][m] = srow[16 * m + g];
+        }
+#pragma unroll
+        for (int n = 0; n < kLaGroup; ++n)
+#pragma unroll
+            for (int m = 0; m < kLaCols / 16; ++m) acc[m] = fmaf(dn[n], sv[n][m], acc[m]);
+    }
+#pragma unroll
+    for (int m = 0; m < kLaCols / 16; ++m) {
+        const int c = 16 * m + g;
+        if (c < a.sbw) {
+            float* rp = a.R + i * a.p + a.sb + c;
+            *rp = fmaf(dscale, acc[m], *rp);
+        }
+    }
+}
+
 template <int SLOTS>
 __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
 {
@@ -618,7 +693,17 @@ __device__ __forceinline__ void panel_role(const StepArgs& a, float* lds)
     int nz = 0;            // this lane's nonzero code differences (launch)
     // (1) look-ahead: the previous super-block's deltas on this one's columns
     //     (written to R: this launch's GEMM leaves these columns out)
-    if (a.psb >= 0) lookahead(a, lds, i0, lrow, g, rowok, dscale);
+    if (a.psb >= 0) {
+        if (a.intd && !a.dense) {
+            const int cnt = rowok ? a.nzprev[i] : 0;
+            if (__syncthreads_and(cnt <= kLaNz))
+                lookahead_sparse(a, lds, i0, lrow, g, rowok, dscale, cnt);
+            else
+                lookahead(a, lds, i0, lrow, g, rowok, dscale);
+        } else {
+            lookahead(a, lds, i0, lrow, g, rowok, dscale);
+        }
+    }
 
     for (int sub = 0; sub < nsub; ++sub) {
         const int64_t j0 = a.sb + (int64_t)sub * B;
@@ -740,8 +825,8 @@ constexpr int kSpGroup = 4;
 // wave's LDS area (positions from the ballots); then all their Sigma
 // segments are loaded, then R is updated.  nz: this thread's row count
 // (threads < 128).
-__device__ void gemm_sparse(const StepArgs& a, int* li, int nz, int active, int64_t row0,
-                            int64_t col0, int64_t ex0, int64_t ex1)
+__device__ __forceinline__ void gemm_sparse(const StepArgs& a, int* li, int nz, int active,
+                                            int64_t row0, int64_t col0, int64_t ex0, int64_t ex1)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int* cnt = li;                                   // 2: active rows among tile rows 0-63, 64-127
