@@ -240,7 +240,7 @@ __global__ __launch_bounds__(256, TWO_LEVEL ? 1 : 2) void gram_x3_kernel(
 // LDS stage buffers (nt_tile_x3_wide).  Used when every 256-row panel lies
 // inside X (p a multiple of 256, aligned rows, token ranges multiples of 32),
 // in either layout (channel-major rows through X3Row, token-major through
-// X3ColW).  Each wave's 64 x 128 block lies in one 128 x 128 tile of the
+// X3Col).  Each wave's 64 x 128 block lies in one 128 x 128 tile of the
 // upper triangle, so the partials use the same slots as gram_x3_kernel and
 // the same finalize.
 constexpr int kWide = 256;
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
     if constexpr (TRANS) {
         // X is n x p: element (channel r, token k) at X[k * p + r]
-        const X3ColW op{X + k0 * p, p, 0, K};
+        const X3Col op{X + k0 * p, p, 0, K};
         nt_tile_x3_wide(op, ti * kWide, op, tj * kWide, K, lds, acc);
     } else {
         const X3Row op{X + k0, n, 0, K};

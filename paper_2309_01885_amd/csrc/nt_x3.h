@@ -211,85 +211,35 @@ struct X3Comp {
     __device__ inline void store(uint32_t* op, const X3Stage& st) const { x3_store_row8(op, st); }
 };
 
-// Transposed operand, element (r, k) at base[k * ld + r] (token-major X).
-// Thread t stages rows 2 (t % 64) and 2 (t % 64) + 1, k = 4 (t / 64) .. +3:
-// the 64 threads of a wave read 512 contiguous bytes per k.
+// Transposed operand, element (r, k) at base[k * ld + r] (token-major X),
+// for any thread count NT (NT / 2 rows per stage): thread t stages row t / 2
+// at k = 8 (t % 2) .. +7, one value per token, so that each 4-byte load
+// instruction of a wave covers 32 consecutive rows at two tokens (two whole
+// 128-byte lines), and the stage goes to LDS exactly as a row-major one
+// (x3_store_row8: 16-byte pieces, consecutive lanes on consecutive pieces of
+// a row pair, no bank conflicts).
 struct X3Col {
     const float* base;
     int64_t ld, rows, kvalid;
-    // whole stage inside the matrix, 8-byte aligned row pairs
+    // whole stage inside the matrix
     __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
     {
         const int t = threadIdx.x;
-        const float* src = base + (k0 + 4 * (t >> 6)) * ld + row0 + 2 * (t & 63);
+        const float* src = base + (k0 + 8 * (t & 1)) * ld + row0 + (t >> 1);
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const f32x2 v = *reinterpret_cast<const f32x2*>(src + u * ld);
-            st.v[0][u] = v[0];
-            st.v[1][u] = v[1];
-        }
+        for (int u = 0; u < 8; ++u) st.v[u >> 2][u & 3] = src[u * ld];
     }
+    // any stage: elements outside rows x kvalid read as 0
     __device__ inline void load(int64_t row0, int64_t k0, X3Stage& st) const
     {
         const int t = threadIdx.x;
-        const int64_t r = row0 + 2 * (t & 63);
-        const int64_t k = k0 + 4 * (t >> 6);
+        const int64_t r = row0 + (t >> 1);
+        const int64_t k = k0 + 8 * (t & 1);
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-            for (int e = 0; e < 2; ++e)
-                st.v[e][u] = (r + e < rows && k + u < kvalid) ? base[(k + u) * ld + r + e] : 0.f;
+        for (int u = 0; u < 8; ++u)
+            st.v[u >> 2][u & 3] = (r < rows && k + u < kvalid) ? base[(k + u) * ld + r] : 0.f;
     }
-    __device__ inline void store(uint32_t* op, const X3Stage& st) const
-    {
-        const int t = threadIdx.x;
-        const int kq = t >> 6;                   // k = 4 kq .. 4 kq + 3: half kq / 2
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const int row = 2 * (t & 63) + e;
-            const X3Pair q0 = split3(st.v[e][0], st.v[e][1]);
-            const X3Pair q1 = split3(st.v[e][2], st.v[e][3]);
-            const int o = x3_addr(row, kq >> 1, 0) + 2 * (kq & 1);
-            *reinterpret_cast<u32x2*>(op + o) = u32x2{q0.h, q1.h};
-            *reinterpret_cast<u32x2*>(op + o + 8) = u32x2{q0.m, q1.m};
-            *reinterpret_cast<u32x2*>(op + o + 16) = u32x2{q0.l, q1.l};
-        }
-    }
-};
-
-// Transposed operand for the 512-thread 256 x 256 tile: thread t stages rows
-// 2 (t % 128) and 2 (t % 128) + 1, k = 4 (t / 128) .. +3, so that the 128
-// threads of a k group read 1024 contiguous bytes per k.
-struct X3ColW {
-    const float* base;
-    int64_t ld, rows, kvalid;
-    // whole stage inside the matrix, 8-byte aligned row pairs
-    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
-    {
-        const int t = threadIdx.x;
-        const float* src = base + (k0 + 4 * (t >> 7)) * ld + row0 + 2 * (t & 127);
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            const f32x2 v = *reinterpret_cast<const f32x2*>(src + u * ld);
-            st.v[0][u] = v[0];
-            st.v[1][u] = v[1];
-        }
-    }
-    __device__ inline void store(uint32_t* op, const X3Stage& st) const
-    {
-        const int t = threadIdx.x;
-        const int kq = t >> 7;                   // k = 4 kq .. 4 kq + 3: half kq / 2
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-            const int row = 2 * (t & 127) + e;
-            const X3Pair q0 = split3(st.v[e][0], st.v[e][1]);
-            const X3Pair q1 = split3(st.v[e][2], st.v[e][3]);
-            const int o = x3_addr(row, kq >> 1, 0) + 2 * (kq & 1);
-            *reinterpret_cast<u32x2*>(op + o) = u32x2{q0.h, q1.h};
-            *reinterpret_cast<u32x2*>(op + o + 8) = u32x2{q0.m, q1.m};
-            *reinterpret_cast<u32x2*>(op + o + 16) = u32x2{q0.l, q1.l};
-        }
-    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const { x3_store_row8(op, st); }
 };
 
 // acc[mi][ni] += A(wave rows mi) B(wave cols ni)^T over one staged K = 16 of
