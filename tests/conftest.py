@@ -27,3 +27,21 @@ def qe():
     import paper_2309_01885_amd as P
     P.load()
     return P
+
+
+@pytest.fixture(scope="session")
+def c2_x():
+    """The attention-projection workload's activations (4096 x 262144
+    heavy-tailed tokens); the MLP up-projection and the outlier-aware
+    workload draw the very same X."""
+    import synth
+    spec = synth.CONFIGS["c2"]
+    print(f"[c2] drawing X {spec.p}x{spec.n}", flush=True)
+    return synth.activations(spec)
+
+
+@pytest.fixture(scope="session")
+def c2_sigma64(c2_x, oracle):
+    """The oracle's undamped fp64 Gram of all 262144 tokens of c2_x."""
+    print("[c2] oracle Gram of all tokens (fp64)", flush=True)
+    return oracle.gram_blas(c2_x)

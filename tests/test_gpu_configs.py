@@ -1,18 +1,21 @@
 """Parity of every workload configuration at its full size (the 4096-channel
-layers on their own Sigma are in test_gpu_large.py).
+layers c2 and c3-up are in test_gpu_large.py).
 
 * c1 (512 x 512, 4-bit, 5 sweeps): the whole chain (Gram, grid, sweeps,
   exact objective) against the oracle on every entry, teacher-forced.
-* c3-down (4096 x 11008, 3-bit, 10 sweeps): the Gram over the full
-  11008 x 262144 X on every diagonal entry and a seeded 256 x 256 block
-  (outlier channels included); CD on all rows against a seeded 64-row
-  sample, teacher-forced and free-running.
-* c4 (4096 x 4096, 3-bit, s = 1% outliers, 10 iterations): the whole CD + IHT
-  run against the oracle's whole run.  g must agree within 1e-4 after every
-  CD and IHT step.  P_s itself is an exact decision on the same fp32 V, so
-  at full size it is checked on a seeded V (identical support).  End to end,
-  V is fp32 on the GPU and fp64 in the oracle; supports may then differ only
-  at entries whose |V| lies within 1e-5 of the threshold.
+* c3-down (4096 x 11008, 3-bit, 10 sweeps): the whole 11008 x 11008 Gram
+  over all 262144 tokens against the oracle's fp64 Gram of the same X; CD on
+  all rows on that Sigma (the layer's own, damped, in fp32) against a seeded
+  64-row sample, teacher-forced and free-running; and the same on the more
+  strongly coupled Gram of a 2048-token prefix.
+* c4 (4096 x 4096, 3-bit, s = 1% outliers, 10 iterations; c2's activations):
+  the whole CD + IHT run on the layer's own Sigma (the oracle's Gram of all
+  262144 tokens) against the oracle's whole run.  g must agree within 1e-4
+  after every CD and IHT step.  P_s itself is an exact decision on the same
+  fp32 V, so at full size it is checked on a seeded V (identical support).
+  End to end, V is fp32 on the GPU and fp64 in the oracle; supports may then
+  differ only at entries whose |V| lies within 1e-5 of the threshold.  The
+  structured variant runs on a 2048-token prefix Gram.
 * c5 (14848 x 59392, 4-bit, 5 sweeps): the Gram over 262144 device-drawn
   tokens streamed in 8192-token chunks, on every diagonal entry and a seeded
   256 x 256 block, against the oracle's fp64 sums of the same numbers; CD
@@ -20,12 +23,12 @@ layers on their own Sigma are in test_gpu_large.py).
   free-running, on a Sigma with the workload's coupling; and a stress case on
   a rank-deficient Sigma (see the two tests).
 
-The CD inputs at c3-down, c4 and c5 use a Sigma the oracle forms from a
-token prefix (2048 tokens; 256 at c5, whose fp64 Gram of all tokens would
-take the host about half an hour), so no GPU output feeds the oracle.  With
-fewer tokens than channels these Sigmas are more strongly coupled than the
-workloads' own (off-diagonal entries about n^-1/2 of the diagonal), which
-makes them the harder parity inputs."""
+Every CD input is a Sigma the oracle forms itself (no GPU output feeds the
+oracle).  At c5 the fp64 Gram of all tokens would take the host about half
+an hour, so its Sigma comes from a 256-token prefix (see the test); a prefix
+Gram with fewer tokens than channels is more strongly coupled than a
+workload's own (whose off-diagonal entries are about n^-1/2 of the
+diagonal), which makes it the harder parity input."""
 import numpy as np
 import pytest
 import torch
@@ -113,35 +116,61 @@ def test_c1_whole_chain(qe, oracle):
     assert exact[1] == pytest.approx(float(np.sum((W.astype(np.float64) @ S32) * W)), rel=1e-5)
 
 
-@pytest.mark.timeout(900)
-def test_c3_down_projection_gram_full_size_sampled(qe, oracle):
+@pytest.fixture(scope="module")
+def c3down_x():
     spec = synth.CONFIGS["c3down"]
-    print("[c3-down] drawing X", flush=True)
-    X = synth.activations(spec)
-    S = qe.gram(dev(X))
-    idx = synth.entry_sample(spec.p, 256, spec.cfg, must=synth.outlier_channels(spec)[:32])
-    assert len(idx) >= 256
-    idx_d = torch.as_tensor(idx, device="cuda")
-    block = host(S[idx_d][:, idx_d])
-    diag = host(torch.diagonal(S))
-    assert torch.equal(S, S.T)
-    del S
-    torch.cuda.empty_cache()
-    print("[c3-down] oracle entries", flush=True)
-    ref_block = oracle.gram_blas(X[idx])
-    ref_diag = oracle.gram_entries(X, np.arange(spec.p), np.arange(spec.p))
-    assert rel_fro(block, ref_block) <= 1e-5
-    assert rel_fro(diag, ref_diag) <= 1e-5
-    assert np.max(np.abs(diag - ref_diag) / ref_diag) <= 1e-5
+    print(f"[c3-down] drawing X {spec.p}x{spec.n}", flush=True)
+    return synth.activations(spec)
+
+
+@pytest.fixture(scope="module")
+def c3down_sigma64(c3down_x, oracle):
+    """The oracle's undamped fp64 Gram of all 262144 tokens (Lemma 1)."""
+    p, n = c3down_x.shape
+    S = np.zeros((p, p), np.float64)
+    step = 32768
+    for t0 in range(0, n, step):
+        print(f"[c3-down] oracle Gram, tokens {t0}..{min(n, t0 + step)} of {n}", flush=True)
+        oracle.gram_blas(c3down_x[:, t0:t0 + step], out=S)
+    return S
 
 
 @pytest.mark.timeout(900)
-def test_c3_down_projection_row_sampled(qe, oracle):
+def test_c3_down_projection_gram_full_size(qe, c3down_x, c3down_sigma64):
+    """The whole 11008 x 11008 Sigma against the oracle's fp64 Gram of all
+    262144 tokens (relative Frobenius <= 1e-5), the diagonal entry by entry
+    (outlier channels included), exactly symmetric."""
+    Xd = dev(c3down_x)
+    S = host(qe.gram(Xd))
+    del Xd
+    torch.cuda.empty_cache()
+    assert np.array_equal(S, S.T)
+    err = rel_fro(S, c3down_sigma64)
+    print(f"[c3-down] Gram relative Frobenius error {err:.3e}", flush=True)
+    assert err <= 1e-5
+    d, dref = np.diag(S).astype(np.float64), np.diag(c3down_sigma64)
+    assert np.max(np.abs(d - dref) / dref) <= 1e-5
+
+
+@pytest.mark.timeout(900)
+def test_c3_down_projection_own_sigma(qe, oracle, c3down_sigma64):
+    spec = synth.CONFIGS["c3down"]
+    W = synth.weights(spec)
+    S32 = oracle.damp(c3down_sigma64, spec.damp).astype(np.float32)
+    cd_row_sampled(qe, oracle, W, S32, spec.bits, spec.sweeps,
+                   synth.row_sample(spec.q, 64, spec.cfg), "c3-down own Sigma")
+
+
+@pytest.mark.timeout(900)
+def test_c3_down_projection_prefix_sigma(qe, oracle):
+    """The same layer on the Gram of a 2048-token prefix (damped 0.01):
+    fewer tokens than channels, so its off-diagonal entries are about 11
+    times the workload's relative to the diagonal."""
     spec = synth.CONFIGS["c3down"]
     W = synth.weights(spec)
     S32 = host_sigma(oracle, spec, 2048).astype(np.float32)
     cd_row_sampled(qe, oracle, W, S32, spec.bits, spec.sweeps,
-                   synth.row_sample(spec.q, 64, spec.cfg), "c3-down")
+                   synth.row_sample(spec.q, 64, spec.cfg), "c3-down 2048-token Sigma")
 
 
 def test_c4_topk_full_size_identical(qe, oracle):
@@ -160,11 +189,14 @@ def test_c4_topk_full_size_identical(qe, oracle):
 
 
 @pytest.mark.timeout(900)
-def test_c4_outlier_full_run(qe, oracle):
+def test_c4_outlier_full_run(qe, oracle, c2_sigma64):
     spec = synth.CONFIGS["c4"]
+    c2 = synth.CONFIGS["c2"]
+    x_seed = lambda sp: sp.cfg if sp.x_cfg is None else sp.x_cfg       # noqa: E731
+    assert x_seed(spec) == x_seed(c2) and spec.p == c2.p and spec.n == c2.n   # c2's activations
     q, p, bits, iters, s = spec.q, spec.p, spec.bits, spec.sweeps, spec.s_budget
     W = synth.weights(spec)
-    S32 = host_sigma(oracle, spec, 2048).astype(np.float32)
+    S32 = oracle.damp(c2_sigma64, spec.damp).astype(np.float32)     # the layer's own Sigma
     lam = float(np.float32(oracle.lambda_max(S32)))
     H0, sup0, n0 = qe.topk_abs(dev(W), s)
     ref_sup0, ref_H0 = oracle.topk_abs(W, s)

@@ -27,19 +27,6 @@ pytestmark = pytest.mark.gpu
 SPEC = synth.CONFIGS["c2"]
 
 
-@pytest.fixture(scope="module")
-def c2_x():
-    print(f"[c2] drawing X {SPEC.p}x{SPEC.n}", flush=True)
-    return synth.activations(SPEC)
-
-
-@pytest.fixture(scope="module")
-def c2_sigma64(c2_x, oracle):
-    """The oracle's undamped fp64 Gram of all tokens."""
-    print("[c2] oracle Gram of all tokens (fp64)", flush=True)
-    return oracle.gram_blas(c2_x)
-
-
 @pytest.mark.timeout(900)
 def test_gram_full_size_full_matrix(qe, c2_x, c2_sigma64):
     Xd = dev(c2_x)
