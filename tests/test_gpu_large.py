@@ -77,21 +77,22 @@ def test_gram_token_major_streamed_full_size(qe, c2_x, c2_sigma64):
     assert np.max(np.abs(d - dref) / dref) <= 1e-5
 
 
-def cd_rows_on_gpu(qe, W, S32, bits, sweeps, rows, block=128):
-    """All rows on the GPU, one sweep per call from What = W; the sampled
-    rows' codes, What and R after every sweep."""
+def cd_rows_on_gpu(qe, W, S32, bits, sweeps, rows, block=128, extra=0):
+    """All rows on the GPU, one sweep per call from What = W (extra: further
+    flags, e.g. QE_CD_DENSE); the sampled rows' codes, What and R after every
+    sweep."""
     q, p = W.shape
     scale, zero = qe.grid_minmax(dev(W), bits)
     Wd, Sd = dev(W), dev(S32)
     Wh = torch.empty_like(Wd)
     codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
     R = torch.empty_like(Wd)
-    flags = qe.QE_INIT_FROM_W
+    flags = qe.QE_INIT_FROM_W | extra
     hist, whats, Rs = [], [], []
     rows_d = torch.as_tensor(rows, device="cuda")
     for _ in range(sweeps):
         qe.cd_sweep(Wd, Sd, bits, scale, zero, Wh, codes, R, 1, block=block, flags=flags)
-        flags = qe.QE_R_VALID | qe.QE_CODES_VALID
+        flags = qe.QE_R_VALID | qe.QE_CODES_VALID | extra
         hist.append(host(codes[rows_d]).astype(np.int32))
         whats.append(host(Wh[rows_d]))
         Rs.append(host(R[rows_d]))
@@ -101,9 +102,10 @@ def cd_rows_on_gpu(qe, W, S32, bits, sweeps, rows, block=128):
     return sc, ze, hist, whats, Rs
 
 
-def row_sampled_parity(qe, oracle, spec, W, S64, rows, label):
+def row_sampled_parity(qe, oracle, spec, W, S64, rows, label, extra=0):
     S32 = oracle.damp(S64, spec.damp).astype(np.float32)
-    sc, ze, hist, whats, Rs = cd_rows_on_gpu(qe, W, S32, spec.bits, spec.sweeps, rows)
+    sc, ze, hist, whats, Rs = cd_rows_on_gpu(qe, W, S32, spec.bits, spec.sweeps, rows,
+                                             extra=extra)
     # the grid is an exact fp32 decision on both sides
     scale, zero = oracle.grid_minmax(W, spec.bits)
     assert np.array_equal(sc, scale) and np.array_equal(ze, zero)
@@ -135,3 +137,58 @@ def test_c3_up_projection_own_sigma(qe, oracle, c2_sigma64):
     W = synth.weights(spec)
     rows = synth.row_sample(spec.q, 128, spec.cfg)
     row_sampled_parity(qe, oracle, spec, W, c2_sigma64, rows, "c3-up own Sigma")
+
+
+@pytest.mark.timeout(900)
+def test_cd_full_size_dense_block_updates(qe, oracle, c2_sigma64):
+    """The configuration the benchmark's roofline times: every block update
+    on the matrix cores (QE_CD_DENSE), on c2's own Sigma, 512 seeded rows
+    against the oracle, teacher-forced and free-running."""
+    W = synth.weights(SPEC)
+    rows = synth.row_sample(SPEC.q, 512, SPEC.cfg)
+    row_sampled_parity(qe, oracle, SPEC, W, c2_sigma64, rows, "c2 own Sigma, dense",
+                       extra=qe.QE_CD_DENSE)
+
+
+@pytest.mark.timeout(900)
+def test_cd_full_size_benchmark_call(qe, oracle, c2_sigma64):
+    """The benchmark's call (all 10 sweeps in one qe_cd_sweep from What = W,
+    the objective after each) against 10 single-sweep calls that carry the
+    objective in obj[0] (QE_OBJ_IN): What, codes, R and every objective
+    bitwise the same; every reported objective within 1e-6 of the fp64
+    objective of the GPU's own What over the whole layer (problem (1) with
+    the damped Sigma, <What - W, (What - W) Sigma>)."""
+    W = synth.weights(SPEC)
+    S32 = oracle.damp(c2_sigma64, SPEC.damp).astype(np.float32)
+    S64 = S32.astype(np.float64)
+    q, p, bits, sweeps = SPEC.q, SPEC.p, SPEC.bits, SPEC.sweeps
+    Wd, Sd = dev(W), dev(S32)
+    scale, zero = qe.grid_minmax(Wd, bits)
+    Wh, R = torch.empty_like(Wd), torch.empty_like(Wd)
+    codes = torch.zeros((q, p), dtype=torch.uint8, device="cuda")
+    obj = torch.zeros(sweeps, dtype=torch.float64, device="cuda")
+    qe.cd_sweep(Wd, Sd, bits, scale, zero, Wh, codes, R, sweeps, block=128,
+                flags=qe.QE_INIT_FROM_W, obj=obj)
+    multi = (host(Wh), host(codes), host(R), host(obj))
+    whats = []
+    for k in range(sweeps):
+        if k > 0:
+            obj[k].copy_(obj[k - 1])
+        qe.cd_sweep(Wd, Sd, bits, scale, zero, Wh, codes, R, 1, block=128,
+                    flags=(qe.QE_INIT_FROM_W if k == 0
+                           else qe.QE_R_VALID | qe.QE_CODES_VALID | qe.QE_OBJ_IN),
+                    obj=obj[k:])
+        whats.append(host(Wh))
+    single = (whats[-1], host(codes), host(R), host(obj))
+    del Wd, Sd, Wh, R, codes
+    torch.cuda.empty_cache()
+    for a, b, name in zip(multi, single, ("What", "codes", "R", "objective")):
+        assert np.array_equal(a, b), name
+    W64 = W.astype(np.float64)
+    for k in range(sweeps):
+        D = whats[k].astype(np.float64) - W64
+        f = float(np.sum(D * (D @ S64)))
+        err = abs(multi[3][k] - f) / f
+        print(f"[c2 call] sweep {k + 1}: objective {multi[3][k]:.9e}, fp64 of What "
+              f"{f:.9e}, rel. error {err:.2e}", flush=True)
+        assert err <= 1e-6
