@@ -2,7 +2,11 @@
 qe_cd_sweep, through the C ABI: two calls in a row, the second on a smaller
 layer, each bit-identical to qe_cd_sweep on the same inputs (the same
 kernels run on the library's fixed scratch instead of a workspace); the
-status output reports a data error and is cleared by the next call."""
+status output reports a data error and is cleared by the next call.  The
+call allocates nothing and enqueues only kernels, so it can be recorded in a
+HIP graph (torch.cuda.CUDAGraph on the capturing stream): every replay, with
+eager work and synchronisations between the replays, gives bitwise what the
+eager call gives."""
 import numpy as np
 import pytest
 import torch
@@ -96,3 +100,45 @@ def test_noalloc_rejects_sizes_beyond_its_scratch(qe):
     assert e.value.code == qe.QE_ERR_TOO_LARGE
     torch.cuda.synchronize()
     assert bool(torch.all(Wh == 7.0))
+
+
+def test_noalloc_call_replayed_from_a_graph(qe, oracle):
+    q, p, bits, sweeps = 256, 384, 4, 3
+    W = synth.gaussian((q, p), seed=41, std=0.02)
+    X = synth.correlated_activations(p, 1024, 0.9, 41, out_channels=8, out_mult=20.0)
+    S32 = oracle.damp(oracle.gram(X), 0.01).astype(np.float32)
+    scale, zero = oracle.grid_minmax(W, bits)
+    Wd, Sd, sc, ze = dev(W), dev(S32), dev(scale), dev(zero)
+
+    def buffers():
+        return (torch.empty_like(Wd), torch.zeros((q, p), dtype=torch.uint8, device="cuda"),
+                torch.empty_like(Wd), torch.zeros(sweeps, dtype=torch.float64, device="cuda"),
+                torch.full((1,), -1, dtype=torch.int32, device="cuda"))
+
+    # eager call first (also where the scratch's address is looked up on this GPU)
+    Wh, codes, R, obj, st = buffers()
+    qe.cd_sweep_noalloc(Wd, Sd, bits, sc, ze, Wh, codes, R, sweeps, obj=obj, status=st)
+    torch.cuda.synchronize()
+    ref = [host(x) for x in (Wh, codes, R, obj, st)]
+    assert ref[4][0] == 0
+
+    # one call recorded (QE_INIT_FROM_W: every replay starts again from What = W)
+    Wh2, codes2, R2, obj2, st2 = buffers()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        qe.cd_sweep_noalloc(Wd, Sd, bits, sc, ze, Wh2, codes2, R2, sweeps, obj=obj2, status=st2)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        # the program's own eager work between replays: overwrite every output
+        Wh2.fill_(1.0)
+        codes2.fill_(7)
+        R2.fill_(-1.0)
+        obj2.fill_(0.0)
+        st2.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = [host(x) for x in (Wh2, codes2, R2, obj2, st2)]
+        for name, a, b in zip(("What", "codes", "R", "objective", "status"), ref, got):
+            assert np.array_equal(a, b), f"replay {rep}: {name}"
