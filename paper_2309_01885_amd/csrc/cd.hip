@@ -327,8 +327,8 @@ __device__ __forceinline__ void panel_run(std::integer_sequence<int, Js...>,
 
 // Stages Sigma[r0 + k][c0 + c] (k < kw, c < cw; else 0) into LDS with the
 // column permutation used by the panel: column c = 16 m + g sits at g * SLOTS + m.
-// Full blocks issue all their 16-byte loads before the first LDS store, so the
-// global latency is paid once per block.
+// Full blocks issue all their loads before the first LDS store, so the global
+// latency is paid once per block.
 template <int SLOTS>
 __device__ __forceinline__ void stage_sigma_block(const float* __restrict__ Sigma, int64_t p,
                                                   int64_t r0, int kw, int64_t c0, int cw,
@@ -337,6 +337,35 @@ __device__ __forceinline__ void stage_sigma_block(const float* __restrict__ Sigm
     constexpr int B = 16 * SLOTS;
     constexpr int Q = B / 4;                     // float4 per row
     constexpr int PER = (B * Q + 255) / 256;     // float4 per thread
+    if constexpr (SLOTS % 4 == 0) {
+        if (kw == B && cw == B) {
+            // thread t takes (row k, lane g) pairs: the lane's SLOTS columns
+            // g, g + 16, ... of row k, read as single floats (16 lanes of a
+            // wave cover 64 contiguous bytes of a row), written as float4
+            // runs of the panel layout (a quarter of the LDS store
+            // instructions of element-wise stores)
+            constexpr int PPT = B * 16 / 256;    // pairs per thread
+            float v[PPT][SLOTS];
+#pragma unroll
+            for (int u = 0; u < PPT; ++u) {
+                const int pi = threadIdx.x + 256 * u;
+                const int k = pi >> 4, g = pi & 15;
+                const float* src = Sigma + (r0 + k) * p + c0 + g;
+#pragma unroll
+                for (int m = 0; m < SLOTS; ++m) v[u][m] = src[16 * m];
+            }
+#pragma unroll
+            for (int u = 0; u < PPT; ++u) {
+                const int pi = threadIdx.x + 256 * u;
+                const int k = pi >> 4, g = pi & 15;
+#pragma unroll
+                for (int m4 = 0; m4 < SLOTS / 4; ++m4)
+                    *reinterpret_cast<f32x4*>(sS + k * B + g * SLOTS + 4 * m4) =
+                        f32x4{v[u][4 * m4], v[u][4 * m4 + 1], v[u][4 * m4 + 2], v[u][4 * m4 + 3]};
+            }
+            return;
+        }
+    }
     if (vec4 && kw == B && cw == B) {
         f32x4 v[PER];
 #pragma unroll
