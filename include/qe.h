@@ -48,10 +48,12 @@ typedef int qe_status;
 #define QE_ERR_TOO_LARGE   7  /* qe_cd_sweep_noalloc: the sizes need more than its fixed scratch */
 #define QE_ERR_NONFINITE   8  /* QE_DEBUG_CHECKS found a NaN or infinity in an input */
 
-/* Layouts of X for qe_gram, optionally or-ed with QE_GRAM_FP32. */
+/* Layouts of X for qe_gram, optionally or-ed with one of QE_GRAM_FP32 and
+ * QE_GRAM_BF16X3 (both at once is QE_ERR_ARG). */
 #define QE_LAYOUT_PN 0        /* X is p x n: each channel's n tokens contiguous */
 #define QE_LAYOUT_NP 1        /* X is n x p: each token's p channels contiguous */
-#define QE_GRAM_FP32 0x100    /* products on the fp32 matrix cores instead of the split bf16 ones */
+#define QE_GRAM_FP32 0x100    /* products on the fp32 matrix cores instead of split ones */
+#define QE_GRAM_BF16X3 0x200  /* the three-way bf16 split everywhere (no fp16 split) */
 
 /* Flags for qe_cd_sweep / qe_cd_outlier_sweep. */
 #define QE_INIT_FROM_W 0x1u   /* start from What = W (Sec. 3.1) or What = W - H (Sec. 4.3);
@@ -114,13 +116,21 @@ qe_status qe_sync_status(void* ws, void* stream);
  * Sigma: p x p fp32, device; overwritten (accumulate = 0) or added to
  * (accumulate = 1, for token chunks streamed through several calls; pass
  * damp = 0 on all but the last).  The result is exactly symmetric.
- * Products: by default each fp32 value x is split exactly into three bf16
- * values (h = bf16(x), m = bf16(x - h), l = x - h - m) and x_i x_j is formed
- * from the six products h h, h m, m h, h l, m m, l h on the bf16 matrix
- * cores, every product exact in fp32; the dropped terms are below 2^-23
- * |x_i x_j| (one fp32 rounding).  With QE_GRAM_FP32 the products run on the
- * fp32 matrix cores.  Accumulation: fp32 over short token chunks, chunk sums
- * added in fp32, split partial sums reduced in fp64.
+ * Products, by default: when p is a multiple of 256, X's rows 16-byte aligned
+ * and (channel-major X) n a multiple of 32, each channel i is first scaled by
+ * 2^e_i (exact; its largest |x| lands in [2^14, 2^15), a pass over X) and
+ * each scaled value y split into two fp16 values (h = fp16(y),
+ * m = fp16(y - h)); y_i y_j is formed from the three products h h, h m, m h
+ * on the fp16 matrix cores, every product exact in fp32, and the sums are
+ * scaled back by 2^-(e_i + e_j).  The dropped terms are below
+ * 3 * 2^-22 |y_i y_j| (plus 2^-39 of the channels' largest values for the
+ * smallest ones).  Otherwise, or with QE_GRAM_BF16X3, each fp32 value x is
+ * split exactly into three bf16 values (h = bf16(x), m = bf16(x - h),
+ * l = x - h - m) and x_i x_j is formed from the six products h h, h m, m h,
+ * h l, m m, l h on the bf16 matrix cores; the dropped terms are below
+ * 2^-23 |x_i x_j| (one fp32 rounding).  With QE_GRAM_FP32 the products run
+ * on the fp32 matrix cores.  Accumulation: fp32 over short token chunks,
+ * chunk sums added in fp32, split partial sums reduced in fp64.
  * ------------------------------------------------------------------------ */
 size_t qe_gram_workspace_size(int64_t p, int64_t n);
 qe_status qe_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma,

@@ -136,8 +136,9 @@ qe_status qe_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma
                   float damp, void* ws, size_t ws_bytes, void* stream)
 {
     if (!X || !Sigma || p <= 0 || n <= 0 || p > (int64_t(1) << 31)) return QE_ERR_ARG;
-    const int base_layout = layout & ~QE_GRAM_FP32;
+    const int base_layout = layout & ~(QE_GRAM_FP32 | QE_GRAM_BF16X3);
     if (base_layout != QE_LAYOUT_PN && base_layout != QE_LAYOUT_NP) return QE_ERR_ARG;
+    if ((layout & QE_GRAM_FP32) && (layout & QE_GRAM_BF16X3)) return QE_ERR_ARG;
     if (!(damp >= 0.f) || !std::isfinite(damp)) return QE_ERR_ARG;
     if (!ws || ws_bytes < gram_ws_bytes(p, n)) return QE_ERR_WORKSPACE;
     hipStream_t s = as_stream(stream);

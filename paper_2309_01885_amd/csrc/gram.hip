@@ -1,9 +1,13 @@
 // Gram matrix Sigma = X X^T on the matrix cores of gfx950.
 //
-// Products: by default on the bf16 matrix cores, every fp32 operand split
-// exactly into three bf16 values and six bf16 products kept per fp32 product
-// (gram_x3_kernel, see nt_x3.h); with QE_GRAM_FP32 on the fp32 matrix cores
-// (gram_kernel).  Both share the work split and the reductions below.
+// Products: by default, on the 256 x 256 tiles, on the fp16 matrix cores with
+// every channel scaled by a power of two and split into two fp16 values, three
+// products kept per fp32 product (gram_x3w_kernel with F2, see nt_f2.h); on
+// the other tiles, or with QE_GRAM_BF16X3, on the bf16 matrix cores with every
+// fp32 operand split exactly into three bf16 values and six products kept
+// (gram_x3_kernel and gram_x3w_kernel, see nt_x3.h); with QE_GRAM_FP32 on the
+// fp32 matrix cores (gram_kernel).  All share the work split and the
+// reductions below.
 //
 // Lemma 1 (Sec. 3.2) needs X only through Sigma, a p x p statistic whose size
 // does not grow with the token count n.  Work split: 128 x 128 tiles of the
@@ -17,6 +21,7 @@
 // sums of 512 tokens added into a second fp32 accumulator) and writes Sigma
 // directly.  The lower triangle is
 // written as an exact mirror through an LDS transpose.
+#include "nt_f2.h"
 #include "nt_x3.h"
 #include "qe_internal.h"
 
@@ -272,14 +277,20 @@ __device__ inline void band_index_wide(int64_t t, int64_t nt, int64_t& ti, int64
 // LDS-transposed symmetric writes as the two-level mode, 128 x 128 quadrant
 // by quadrant; the large-p replacement of the two-level mode for streamed
 // token chunks.
-template <bool DIRECT, bool TRANS>
+//
+// F2: the two-way fp16 split of nt_f2.h, channel i scaled by 2^chexp[i] on the
+// way in and every sum scaled back by 2^-(chexp[i] + chexp[j]) on the way out
+// (exact); otherwise the three-way bf16 split of nt_x3.h (chexp unused).
+template <bool DIRECT, bool TRANS, bool F2>
 __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
     const float* __restrict__ X, int64_t p, int64_t n, int64_t ntw, int64_t tiles_w, int64_t nt,
     int64_t tiles, int64_t splits, int64_t split_len, float* __restrict__ out, int accumulate,
-    const int* status)
+    const int* __restrict__ chexp, const int* status)
 {
     if (failed(status)) return;
-    __shared__ __attribute__((aligned(16))) uint32_t lds[kX3wLdsDw];
+    // the direct mode also stages a finished 128 x kTStride quadrant here
+    static_assert(kTile * kTStride <= kF2LdsDw && kTile * kTStride <= kX3wLdsDw, "quadrant fits");
+    __shared__ __attribute__((aligned(16))) uint32_t lds[F2 ? kF2LdsDw : kX3wLdsDw];
     const int64_t items = tiles_w * splits;
     const int64_t per = cdiv(items, 8);
     const int64_t item = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
@@ -296,7 +307,18 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
         for (int ni = 0; ni < 4; ++ni)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
-    if constexpr (TRANS) {
+    if constexpr (F2) {
+        // this thread stages row t / 2 of both panels
+        const int ea = chexp[ti * kWide + (threadIdx.x >> 1)];
+        const int eb = chexp[tj * kWide + (threadIdx.x >> 1)];
+        if constexpr (TRANS) {
+            const F2Op<X3Col> A{{X + k0 * p, p, 0, K}, ea}, B{{X + k0 * p, p, 0, K}, eb};
+            nt_tile_f2_wide(A, ti * kWide, B, tj * kWide, K, lds, acc);
+        } else {
+            const F2Op<X3Row> A{{X + k0, n, 0, K}, ea}, B{{X + k0, n, 0, K}, eb};
+            nt_tile_f2_wide(A, ti * kWide, B, tj * kWide, K, lds, acc);
+        }
+    } else if constexpr (TRANS) {
         // X is n x p: element (channel r, token k) at X[k * p + r]
         const X3Col op{X + k0 * p, p, 0, K};
         nt_tile_x3_wide(op, ti * kWide, op, tj * kWide, K, lds, acc);
@@ -310,6 +332,19 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
     const int64_t qi = 2 * ti + wm / 2, qj = 2 * tj + wn;
     const int lane = threadIdx.x & 63;
     const int r0 = (wm & 1) * 64;
+    if constexpr (F2) {
+        int ec[4];
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) ec[ni] = chexp[tj * kWide + wn * 128 + 32 * ni + (lane & 31)];
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int er = chexp[ti * kWide + wm * 64 + 32 * mi + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)];
+#pragma unroll
+                for (int ni = 0; ni < 4; ++ni) acc[mi][ni][v] = ldexpf(acc[mi][ni][v], -(er + ec[ni]));
+            }
+    }
     if constexpr (DIRECT) {
         // the K loop ended with a barrier: its LDS holds a 128 x kTStride tile
         float* tl = reinterpret_cast<float*>(lds);
@@ -400,6 +435,107 @@ __global__ __launch_bounds__(256) void damp_kernel(float* Sigma, int64_t p, floa
     for (int64_t j = threadIdx.x; j < p; j += blockDim.x) Sigma[j * p + j] += add;
 }
 
+// Channel exponents of the fp16 split: e with the channel's largest |x| times
+// 2^e in [2^14, 2^15) (frexp: amax = f 2^ex, f in [1/2, 1)); 0 for an all-zero
+// or non-finite channel (a non-finite value reaches Sigma as in fp32).
+__device__ inline int chan_exp(float amax)
+{
+    if (!(amax > 0.f) || !isfinite(amax)) return 0;
+    int ex;
+    (void)frexpf(amax, &ex);
+    return 15 - ex;
+}
+
+__device__ inline float absmax4(float m, f32x4 v)
+{
+    return fmaxf(m, fmaxf(fmaxf(fabsf(v[0]), fabsf(v[1])), fmaxf(fabsf(v[2]), fabsf(v[3]))));
+}
+
+// Channel-major X (p x n): one workgroup per channel.
+__global__ __launch_bounds__(256) void chan_exp_pn_kernel(const float* __restrict__ X, int64_t n,
+                                                          int x_vec4, int* __restrict__ chexp,
+                                                          const int* status)
+{
+    if (failed(status)) return;
+    __shared__ float sh[4];
+    const float* row = X + (int64_t)blockIdx.x * n;
+    float m = 0.f;
+    if (x_vec4) {
+        // n % 4 == 0 and 16-byte aligned rows
+        const f32x4* r4 = reinterpret_cast<const f32x4*>(row);
+#pragma unroll 4
+        for (int64_t i = threadIdx.x; i < n / 4; i += 256) m = absmax4(m, r4[i]);
+    } else {
+        for (int64_t i = threadIdx.x; i < n; i += 256) m = fmaxf(m, fabsf(row[i]));
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
+    if ((threadIdx.x & 63) == 0) sh[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) chexp[blockIdx.x] = chan_exp(fmaxf(fmaxf(sh[0], sh[1]), fmaxf(sh[2], sh[3])));
+}
+
+// Token-major X (n x p): workgroup (column block of 1024, token slice y) takes
+// the tokens y, y + slices, ... of its columns (4 per thread) and writes
+// their largest |x| to part[y * p + column]; chan_exp_np_kernel reduces.
+__global__ __launch_bounds__(256) void chan_absmax_np_kernel(const float* __restrict__ X, int64_t p,
+                                                             int64_t n, int x_vec4,
+                                                             float* __restrict__ part,
+                                                             const int* status)
+{
+    if (failed(status)) return;
+    const int64_t c = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+    if (c >= p) return;
+    const int64_t slices = gridDim.y;
+    f32x4 m = {0.f, 0.f, 0.f, 0.f};
+    if (x_vec4) {
+        // p % 4 == 0 and 16-byte aligned token rows: the 4 columns are inside X
+        float a = 0.f, b = 0.f, cc = 0.f, d = 0.f;
+#pragma unroll 4
+        for (int64_t t = blockIdx.y; t < n; t += slices) {
+            const f32x4 v = *reinterpret_cast<const f32x4*>(X + t * p + c);
+            a = fmaxf(a, fabsf(v[0]));
+            b = fmaxf(b, fabsf(v[1]));
+            cc = fmaxf(cc, fabsf(v[2]));
+            d = fmaxf(d, fabsf(v[3]));
+        }
+        m = f32x4{a, b, cc, d};
+    } else {
+        for (int64_t t = blockIdx.y; t < n; t += slices)
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+                if (c + u < p) m[u] = fmaxf(m[u], fabsf(X[t * p + c + u]));
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        if (c + u < p) part[blockIdx.y * p + c + u] = m[u];
+}
+
+__global__ __launch_bounds__(256) void chan_exp_np_kernel(const float* __restrict__ part, int64_t p,
+                                                          int slices, int* __restrict__ chexp,
+                                                          const int* status)
+{
+    if (failed(status)) return;
+    const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (j >= p) return;
+    float m = 0.f;
+    for (int y = 0; y < slices; ++y) m = fmaxf(m, part[y * p + j]);
+    chexp[j] = chan_exp(m);
+}
+
+// Token slices of chan_absmax_np_kernel: about 1024 workgroups, at most 256
+// slices (the partials then hold at most 4 MB).
+static int64_t chan_slices(int64_t p)
+{
+    return std::max<int64_t>(1, std::min<int64_t>(256, 1024 / cdiv(p, 1024)));
+}
+
+// Workspace of the channel exponents: p ints and the token-major partials.
+static size_t chan_ws_bytes(int64_t p)
+{
+    return align256((size_t)p * sizeof(int)) + align256((size_t)chan_slices(p) * p * sizeof(float));
+}
+
 // Number of token splits, or 0 for the two-level direct mode.
 //
 // The tile kernels hold one workgroup per slot (256 slots for the 256 x 256
@@ -445,7 +581,8 @@ static size_t gram_ws_one(int64_t p, int64_t n)
     const int64_t nt = cdiv(p, kTile);
     const int64_t tiles = nt * (nt + 1) / 2;
     const int64_t splits = gram_splits(p, n);
-    return kStatusBytes + align256((size_t)splits * tiles * kTileFloats * sizeof(float));
+    return kStatusBytes + align256((size_t)splits * tiles * kTileFloats * sizeof(float)) +
+           chan_ws_bytes(p);
 }
 
 // Token-major X with a token count that is not a multiple of 32 is taken as
@@ -466,7 +603,7 @@ static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layou
 qe_status launch_gram(const float* X, int64_t p, int64_t n, int layout, float* Sigma,
                       int accumulate, float damp, void* ws, hipStream_t s)
 {
-    const bool trans = (layout & ~QE_GRAM_FP32) == QE_LAYOUT_NP;
+    const bool trans = (layout & ~(QE_GRAM_FP32 | QE_GRAM_BF16X3)) == QE_LAYOUT_NP;
     if (trans && !(layout & QE_GRAM_FP32) && p % kWide == 0 && n > kTokAlign &&
         n % kTokAlign != 0) {
         // token rows are contiguous: the tail is X's last n % 32 token rows
@@ -486,7 +623,8 @@ static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layou
     const int64_t tiles = nt * (nt + 1) / 2;
     const int64_t splits = gram_splits(p, n);
     const bool fp32 = (layout & QE_GRAM_FP32) != 0;
-    const bool trans = (layout & ~QE_GRAM_FP32) == QE_LAYOUT_NP;
+    const bool f2 = (layout & QE_GRAM_BF16X3) == 0;
+    const bool trans = (layout & ~(QE_GRAM_FP32 | QE_GRAM_BF16X3)) == QE_LAYOUT_NP;
     // 16-byte loads need an aligned base and a row stride that keeps them aligned
     const int x_vec4 = aligned16(X) && ((trans ? p : n) % 4 == 0);
     // split length: a multiple of the K chunk, at most kSplitTokensMax
@@ -494,6 +632,11 @@ static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layou
     const int64_t used = splits == 0 ? 1 : cdiv(n, split_len);
     float* parts = reinterpret_cast<float*>(static_cast<char*>(ws) + kStatusBytes);
     float* dst = splits == 0 ? Sigma : parts;
+    // channel exponents (fp16 split) after the split partials
+    char* const chws = static_cast<char*>(ws) + kStatusBytes +
+                       align256((size_t)splits * tiles * kTileFloats * sizeof(float));
+    int* const chexp = reinterpret_cast<int*>(chws);
+    float* const chpart = reinterpret_cast<float*>(chws + align256((size_t)p * sizeof(int)));
     if (fp32) {
         dim3 grid((unsigned)tiles, (unsigned)used);
         if (splits == 0) {
@@ -523,13 +666,34 @@ static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layou
             const int64_t ntw = p / kWide;
             const int64_t tiles_w = ntw * (ntw + 1) / 2;
             const dim3 grid((unsigned)(8 * cdiv(tiles_w * used, 8)));
-#define QE_GRAM_X3W(D, T, SPLITS, LEN, OUT)                                                    \
-    hipLaunchKernelGGL((gram_x3w_kernel<D, T>), grid, dim3(512), 0, s, X, p, n, ntw, tiles_w, nt, \
-                       tiles, SPLITS, LEN, OUT, accumulate, status)
-            if (two && trans) QE_GRAM_X3W(true, true, (int64_t)1, n, Sigma);
-            else if (two) QE_GRAM_X3W(true, false, (int64_t)1, n, Sigma);
-            else if (trans) QE_GRAM_X3W(false, true, used, split_len, parts);
-            else QE_GRAM_X3W(false, false, used, split_len, parts);
+            if (f2) {
+                if (trans) {
+                    const int64_t sl = chan_slices(p);
+                    hipLaunchKernelGGL(chan_absmax_np_kernel,
+                                       dim3((unsigned)cdiv(p, 1024), (unsigned)sl), dim3(256), 0, s,
+                                       X, p, n, x_vec4, chpart, status);
+                    hipLaunchKernelGGL(chan_exp_np_kernel, dim3((unsigned)cdiv(p, 256)), dim3(256),
+                                       0, s, chpart, p, (int)sl, chexp, status);
+                } else {
+                    hipLaunchKernelGGL(chan_exp_pn_kernel, dim3((unsigned)p), dim3(256), 0, s, X, n,
+                                       x_vec4, chexp, status);
+                }
+                if (hipGetLastError() != hipSuccess) return QE_ERR_HIP;
+            }
+#define QE_GRAM_X3W(D, T, F, SPLITS, LEN, OUT)                                                  \
+    hipLaunchKernelGGL((gram_x3w_kernel<D, T, F>), grid, dim3(512), 0, s, X, p, n, ntw, tiles_w,   \
+                       nt, tiles, SPLITS, LEN, OUT, accumulate, chexp, status)
+            if (f2) {
+                if (two && trans) QE_GRAM_X3W(true, true, true, (int64_t)1, n, Sigma);
+                else if (two) QE_GRAM_X3W(true, false, true, (int64_t)1, n, Sigma);
+                else if (trans) QE_GRAM_X3W(false, true, true, used, split_len, parts);
+                else QE_GRAM_X3W(false, false, true, used, split_len, parts);
+            } else {
+                if (two && trans) QE_GRAM_X3W(true, true, false, (int64_t)1, n, Sigma);
+                else if (two) QE_GRAM_X3W(true, false, false, (int64_t)1, n, Sigma);
+                else if (trans) QE_GRAM_X3W(false, true, false, used, split_len, parts);
+                else QE_GRAM_X3W(false, false, false, used, split_len, parts);
+            }
 #undef QE_GRAM_X3W
         } else if (trans) {
             if (two) { if (full) QE_GRAM_X3(true, true, true); else QE_GRAM_X3(true, true, false); }

@@ -1,0 +1,238 @@
+// fp32 Gram products on the fp16 matrix cores of gfx950 (two-way split of
+// power-of-two-scaled channels), on the 256 x 256 tile of eight waves.
+//
+// Channel i of X is scaled by 2^e_i, exactly, with e_i chosen so that the
+// channel's largest |x| lands in [2^14, 2^15) (a pre-pass over X).  Every
+// scaled value y then splits into two fp16 values,
+//     h = fp16(y),  m = fp16(y - h),
+// with round-to-nearest-even conversions: y - h is exact in fp32 and at most
+// 2^-11 |y|, and the remainder y - h - m is at most 2^-22 |y| (at most 2^-25,
+// i.e. 2^-39 of the channel's largest value, where y - h is below fp16's
+// normal range).  The product of two fp16 values is exact in fp32, and
+//     y_i y_j = h_i h_j + (h_i m_j + m_i h_j) + E,
+// where the dropped part E (m_i m_j and the products with the remainders) is
+// below 3 * 2^-22 |y_i y_j| with random signs.  The three kept products run
+// as v_mfma_f32_32x32x16_f16 with fp32 accumulation, half the matrix-core
+// work of the six-product bf16 split (nt_x3.h); the tile's sums are scaled
+// back by 2^-(e_i + e_j), exactly, before they leave the kernel.
+//
+// Pipeline as nt_tile_x3_wide: wave (wm, wn) owns rows wm * 64 + 32 mi and
+// columns wn * 128 + 32 ni of the tile, K in stages of 16 through three LDS
+// stage buffers, global loads three stages ahead, one barrier per stage.
+// Per operand and stage the LDS holds 256 rows of 16 dwords: four 16-byte
+// slots (plane 2 p + half, each 8 k values of one plane) whose order is
+// permuted by row bits 2 and 3, so that the operand reads (16 consecutive
+// rows of one slot) and the staging writes (8 consecutive rows, both halves
+// of one plane) each cover the 64 banks once.
+#pragma once
+
+#include "nt_x3.h"
+
+namespace qe {
+
+constexpr int kF2RowDw = 16;                      // h, m: 8 dwords each
+constexpr int kF2OpDw = 256 * kF2RowDw;           // one operand of one stage
+constexpr int kF2BufDw = 2 * kF2OpDw;             // A and B of one stage
+constexpr int kF2LdsDw = 3 * kF2BufDw;            // three stages: 98,304 bytes
+
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+
+// Slot permutation of a row: bit 1 from row bit 2, bit 0 from row bit 3.
+__device__ inline int f2_perm(int row) { return (((row >> 2) & 1) << 1) | ((row >> 3) & 1); }
+
+// Dword offset of (row, half, plane) inside one operand's stage area.
+__device__ inline int f2_addr(int row, int half, int plane)
+{
+    return row * kF2RowDw + 4 * ((2 * plane + half) ^ f2_perm(row));
+}
+
+// Scales a stage held as thread t (row t / 2, k = 8 (t % 2) .. +7) by 2^e,
+// splits it and stores one 16-byte half of each plane.
+__device__ inline void f2_store_row8(uint32_t* op, const X3Stage& st, int e)
+{
+    const int t = threadIdx.x;
+    u32x4 h, m;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+        const float a = ldexpf(st.v[u >> 1][2 * (u & 1)], e);
+        const float b = ldexpf(st.v[u >> 1][2 * (u & 1) + 1], e);
+        const f16x2 hh = __builtin_convertvector((f32x2){a, b}, f16x2);
+        const f32x2 hf = __builtin_convertvector(hh, f32x2);
+        const f16x2 mm = __builtin_convertvector((f32x2){a - hf[0], b - hf[1]}, f16x2);
+        h[u] = __builtin_bit_cast(uint32_t, hh);
+        m[u] = __builtin_bit_cast(uint32_t, mm);
+    }
+    *reinterpret_cast<u32x4*>(op + f2_addr(t >> 1, t & 1, 0)) = h;
+    *reinterpret_cast<u32x4*>(op + f2_addr(t >> 1, t & 1, 1)) = m;
+}
+
+// A row-per-two-lanes loader (X3Row: channel-major, X3Col: token-major) whose
+// stages are split as above; e is the exponent of this thread's row.
+template <class Base>
+struct F2Op : Base {
+    int e;
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const { f2_store_row8(op, st, e); }
+};
+
+__device__ __forceinline__ f16x8 f2_frag(const uint32_t* p)
+{
+    return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(p));
+}
+
+// One 32-column block ni of one stage: products mh, hm, hh (A planes m, h, h),
+// two MFMAs (mi = 0, 1) each.
+__device__ __forceinline__ void f2w_block(const f16x8 (&a)[2][2], const f16x8 (&b)[2],
+                                          f32x16 (&acc)[2][4], int ni)
+{
+    constexpr int PA[3] = {1, 0, 0};
+    constexpr int PB[3] = {0, 1, 0};
+#pragma unroll
+    for (int q = 0; q < 3; ++q)
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi)
+            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a[mi][PA[q]], b[PB[q]],
+                                                                 acc[mi][ni], 0, 0, 0);
+}
+
+// Stage c: multiplies the fragments of `cur` (fa and fb[0] arrive holding A
+// and B block 0), splits and writes stage c + 2 from (ga, gb) to `wr`, loads
+// stage kload into (la, lb), and leaves fa and fb[0] holding the fragments of
+// `nxt` (stage c + 1).  offa[pl] / offb[pl]: this lane's plane-pl fragment of
+// row block 0 (further blocks of 32 rows keep the slot permutation).
+template <class OA, class OB>
+__device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                          int64_t kload, const uint32_t* cur, const uint32_t* nxt,
+                                          uint32_t* wr, X3Stage& ga, X3Stage& gb, X3Stage& la,
+                                          X3Stage& lb, const int (&offa)[2], const int (&offb)[2],
+                                          f16x8 (&fa)[2][2], f16x8 (&fb)[2][2], f32x16 (&acc)[2][4])
+{
+    constexpr int BLK = 32 * kF2RowDw;
+    // group 0: global loads, B block 1 reads, split of A (stage c + 2)
+    A.load_full(row0a, kload, la);
+    B.load_full(row0b, kload, lb);
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl) fb[1][pl] = f2_frag(cur + offb[pl] + 1 * BLK);
+    f2w_block(fa, fb[0], acc, 0);
+    A.store(wr, ga);
+    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);     // VMEM reads
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // DS reads
+#pragma unroll
+    for (int i = 0; i < 6; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);     // VALU
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);     // DS writes
+    __builtin_amdgcn_sched_barrier(0);
+    // group 1: B block 2 reads, split of B
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl) fb[0][pl] = f2_frag(cur + offb[pl] + 2 * BLK);
+    f2w_block(fa, fb[1], acc, 1);
+    B.store(wr + kF2OpDw, gb);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+#pragma unroll
+    for (int i = 0; i < 6; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    // group 2: B block 3 reads; the barrier makes stage c + 2 visible and ends
+    // this stage's reads of `cur`
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl) fb[1][pl] = f2_frag(cur + offb[pl] + 3 * BLK);
+    f2w_block(fa, fb[0], acc, 2);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    // group 3: next stage's B block 0 and A fragments, each after its last use
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl) fb[0][pl] = f2_frag(nxt + offb[pl]);
+    {
+        constexpr int PA[3] = {1, 0, 0};
+        constexpr int PB[3] = {0, 1, 0};
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+#pragma unroll
+            for (int mi = 0; mi < 2; ++mi)
+                acc[mi][3] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[mi][PA[q]], fb[1][PB[q]],
+                                                                    acc[mi][3], 0, 0, 0);
+            if (q == 0 || q == 2) {
+                const int pl = PA[q];
+#pragma unroll
+                for (int mi = 0; mi < 2; ++mi) fa[mi][pl] = f2_frag(nxt + offa[pl] + mi * BLK);
+            }
+        }
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Stage c with c % 3 == R: stage s lives in LDS buffer s % 3 and in register
+// set s % 3; the set that held stage c + 1 takes stage c + 4 (a load past the
+// last stage re-reads the last stage: in bounds, and it lands in a buffer no
+// stage reads).
+template <int R, class OA, class OB>
+__device__ __forceinline__ void f2w_stage3(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                           int64_t c, int64_t nst, uint32_t* lds, X3Stage (&ga)[3],
+                                           X3Stage (&gb)[3], const int (&offa)[2],
+                                           const int (&offb)[2], f16x8 (&fa)[2][2],
+                                           f16x8 (&fb)[2][2], f32x16 (&acc)[2][4])
+{
+    f2w_stage(A, row0a, B, row0b, min(c + 4, nst - 1) * kX3KC, lds + R * kF2BufDw,
+              lds + ((R + 1) % 3) * kF2BufDw, lds + ((R + 2) % 3) * kF2BufDw, ga[(R + 2) % 3],
+              gb[(R + 2) % 3], ga[(R + 1) % 3], gb[(R + 1) % 3], offa, offb, fa, fb, acc);
+}
+
+// acc += A[row0a.., 0..K) B[row0b.., 0..K)^T (scaled values) on the 256 x 256
+// tile of 512 threads; K a positive multiple of 32, every 256-row panel
+// inside the matrix, aligned rows.  `lds` holds kF2LdsDw dwords.  Ends with
+// a barrier.
+template <class OA, class OB>
+__device__ __forceinline__ void nt_tile_f2_wide(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                                int64_t K, uint32_t* lds, f32x16 (&acc)[2][4])
+{
+    const int64_t nst = K / kX3KC;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int ra = wm * 64 + (lane & 31), rb = wn * 128 + (lane & 31);
+    const int offa[2] = {f2_addr(ra, lane >> 5, 0), f2_addr(ra, lane >> 5, 1)};
+    const int offb[2] = {kF2OpDw + f2_addr(rb, lane >> 5, 0), kF2OpDw + f2_addr(rb, lane >> 5, 1)};
+    X3Stage ga[3], gb[3];
+    A.load_full(row0a, 0, ga[0]);
+    B.load_full(row0b, 0, gb[0]);
+    A.load_full(row0a, kX3KC, ga[1]);
+    B.load_full(row0b, kX3KC, gb[1]);
+    A.store(lds, ga[0]);
+    B.store(lds + kF2OpDw, gb[0]);
+    A.load_full(row0a, min<int64_t>(2, nst - 1) * kX3KC, ga[2]);
+    B.load_full(row0b, min<int64_t>(2, nst - 1) * kX3KC, gb[2]);
+    A.load_full(row0a, min<int64_t>(3, nst - 1) * kX3KC, ga[0]);
+    B.load_full(row0b, min<int64_t>(3, nst - 1) * kX3KC, gb[0]);
+    A.store(lds + kF2BufDw, ga[1]);
+    B.store(lds + kF2BufDw + kF2OpDw, gb[1]);
+    __syncthreads();
+    f16x8 fa[2][2], fb[2][2];
+#pragma unroll
+    for (int mi = 0; mi < 2; ++mi)
+#pragma unroll
+        for (int pl = 0; pl < 2; ++pl) fa[mi][pl] = f2_frag(lds + offa[pl] + mi * 32 * kF2RowDw);
+#pragma unroll
+    for (int pl = 0; pl < 2; ++pl) fb[0][pl] = f2_frag(lds + offb[pl]);
+    int64_t c = 0;
+    for (; c + 3 <= nst; c += 3) {
+        f2w_stage3<0>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+        f2w_stage3<1>(A, row0a, B, row0b, c + 1, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+        f2w_stage3<2>(A, row0a, B, row0b, c + 2, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+    }
+    if (c < nst) f2w_stage3<0>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+    if (c + 1 < nst) f2w_stage3<1>(A, row0a, B, row0b, c + 1, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+    __syncthreads();
+}
+
+}  // namespace qe

@@ -30,6 +30,7 @@ QE_NOALLOC_SCRATCH_BYTES = 64 << 20
 QE_LAYOUT_PN = 0
 QE_LAYOUT_NP = 1
 QE_GRAM_FP32 = 0x100
+QE_GRAM_BF16X3 = 0x200
 
 QE_INIT_FROM_W = 0x1
 QE_R_VALID = 0x2
@@ -154,15 +155,19 @@ def _finish(ws, check, where, stream=None):
 # ---------------------------------------------------------------------------- Gram
 def gram(X: torch.Tensor, layout: int = QE_LAYOUT_PN, Sigma: Optional[torch.Tensor] = None,
          accumulate: bool = False, damp: float = 0.0, ws: Optional[torch.Tensor] = None,
-         check: bool = True, stream=None, fp32: bool = False) -> torch.Tensor:
+         check: bool = True, stream=None, fp32: bool = False,
+         bf16x3: bool = False) -> torch.Tensor:
     """Sigma (+)= X X^T (qe_gram).  fp32=True selects the fp32 matrix-core
-    products (QE_GRAM_FP32) instead of the exact three-way bf16 split."""
+    products (QE_GRAM_FP32), bf16x3=True the three-way bf16 split on every
+    tile (QE_GRAM_BF16X3), instead of the default split products."""
     lib = load()
     if X.dim() != 2:
         raise ValueError("X must be 2-D")
     p, n = (X.shape if layout == QE_LAYOUT_PN else X.shape[::-1])
     if fp32:
         layout |= QE_GRAM_FP32
+    if bf16x3:
+        layout |= QE_GRAM_BF16X3
     if Sigma is None:
         Sigma = torch.empty((p, p), dtype=torch.float32, device=X.device)
     need = lib.qe_gram_workspace_size(p, n)

@@ -72,15 +72,18 @@ def test_workspace_sizes(lib):
     """Host arithmetic only.  The Gram's size pins its token-split choice:
     4096 channels x 262144 tokens -> 15 splits of the 528 upper-triangle
     128 x 128 tiles (64 KiB each) after the 256-byte status word; at 59392
-    channels the partials would not fit, so Sigma is written directly."""
+    channels the partials would not fit, so Sigma is written directly.  Then
+    the channel exponents of the fp16 split (p ints) and the token-major
+    pre-pass partials (slices x p floats, about 1024 workgroups of 1024
+    channels: 256 slices at p = 4096, 17 at p = 59392)."""
     L, _ = lib
     for f in ("qe_gram_workspace_size", "qe_cd_workspace_size", "qe_objective_workspace_size",
               "qe_lambda_workspace_size", "qe_outlier_workspace_size", "qe_topk_workspace_size",
               "qe_topk_columns_workspace_size"):
         getattr(L, f).restype = ctypes.c_size_t
     L.qe_gram_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64]
-    assert L.qe_gram_workspace_size(4096, 262144) == 256 + 15 * 528 * 65536
-    assert L.qe_gram_workspace_size(59392, 32768) == 256
+    assert L.qe_gram_workspace_size(4096, 262144) == 256 + 15 * 528 * 65536 + 4096 * 4 + 256 * 4096 * 4
+    assert L.qe_gram_workspace_size(59392, 32768) == 256 + 59392 * 4 + 17 * 59392 * 4
     assert L.qe_gram_workspace_size(0, 10) == 256
     L.qe_cd_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
     c2 = L.qe_cd_workspace_size(4096, 4096, 0)
@@ -160,6 +163,9 @@ def test_gram_argument_errors(lib):
     assert _gram(L, p=0) == QE_ERR_ARG            # empty input
     assert _gram(L, n=0) == QE_ERR_ARG
     assert _gram(L, layout=2) == QE_ERR_ARG
+    assert _gram(L, layout=0x100 | 0x200) == QE_ERR_ARG   # QE_GRAM_FP32 with QE_GRAM_BF16X3
+    assert _gram(L, layout=0x400) == QE_ERR_ARG           # no such flag
+    assert _gram(L, layout=0x200 | 1, ws=NULL) == QE_ERR_WORKSPACE   # QE_GRAM_BF16X3 is accepted
     assert _gram(L, damp=-1.0) == QE_ERR_ARG
     assert _gram(L, damp=float("nan")) == QE_ERR_ARG
     assert _gram(L, ws=NULL) == QE_ERR_WORKSPACE

@@ -1,8 +1,10 @@
 """GPU parity of qe_gram (Sigma = X X^T, Lemma 1) against the fp64 oracle.
 
-Bar: relative Frobenius error <= 1e-5; Sigma exactly symmetric.  Both product
-paths are covered: the default three-way bf16 split and QE_GRAM_FP32.  Split
-products: p a multiple of 256 with n a multiple of 32 takes the 256 x 256
+Bar: relative Frobenius error <= 1e-5; Sigma exactly symmetric.  Every
+product path is covered: the default split (on the 256 x 256 tiles the
+two-way fp16 split of power-of-two-scaled channels, elsewhere the three-way
+bf16 split), QE_GRAM_BF16X3 (the bf16 split on every tile) and QE_GRAM_FP32.
+Tiles: p a multiple of 256 with n a multiple of 32 takes the 256 x 256
 tiles, p a multiple of 128 the unguarded 128 x 128 loop, other shapes the
 guarded one."""
 import numpy as np
@@ -15,64 +17,112 @@ from parity import dev, host, rel_fro
 pytestmark = pytest.mark.gpu
 
 
-def _gram(qe, X, layout=0, **kw):
-    return host(qe.gram(dev(X), layout=layout, **kw))
+def _gram(qe, X, layout=0, mode="default", **kw):
+    return host(qe.gram(dev(X), layout=layout, fp32=mode == "fp32", bf16x3=mode == "bf16x3", **kw))
 
 
-@pytest.mark.parametrize("fp32", [False, True])
+MODES = ["default", "bf16x3", "fp32"]
+
+
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("p,n", [(512, 2048), (200, 1000), (1, 7), (129, 33), (300, 5000),
                                  (384, 4096 + 32), (256, 16), (768, 4096 + 64),
                                  (256, 4096), (512, 8192 + 32)])
-def test_gram_matches_oracle(qe, oracle, p, n, fp32):
+def test_gram_matches_oracle(qe, oracle, p, n, mode):
     """(256, 4096) takes 128 token splits of 32: the shortest K loop of the
     256 x 256 tile (two stages); (512, 8224) a split count that leaves a
     shorter last split."""
     spec = synth.CONFIGS["c1"]
     X = synth.activations(spec, n=n, p=p)
-    S = _gram(qe, X, fp32=fp32)
+    S = _gram(qe, X, mode=mode)
     ref = oracle.gram(X)
     assert rel_fro(S, ref) <= 1e-5
     assert np.array_equal(S, S.T)
 
 
-@pytest.mark.parametrize("fp32", [False, True])
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("p,n", [(256, 1024), (130, 77), (384, 96), (512, 2048 + 17), (256, 31)])
-def test_gram_token_major_layout(qe, oracle, p, n, fp32):
+def test_gram_token_major_layout(qe, oracle, p, n, mode):
     """(256, 1024) takes the 256 x 256 tiles; (512, 2065) an aligned part on
     them plus a 17-token tail; the others the 128 x 128 tiles."""
     X = synth.gaussian((p, n), seed=3)
-    S_pn = _gram(qe, X, 0, fp32=fp32)
-    S_np = _gram(qe, np.ascontiguousarray(X.T), 1, fp32=fp32)
+    S_pn = _gram(qe, X, 0, mode=mode)
+    S_np = _gram(qe, np.ascontiguousarray(X.T), 1, mode=mode)
     ref = oracle.gram(X)
     assert rel_fro(S_np, ref) <= 1e-5
     assert rel_fro(S_np, S_pn) <= 1e-6
     assert np.array_equal(S_np, S_np.T)
 
 
-def test_gram_split_products_exact_on_short_values(qe):
-    """Values with at most 8 significant bits are their own bf16 h part
-    (m = l = 0); with integer products and partial sums below 2^24 every
-    step is exact, so both product paths return the exact integer Gram."""
+@pytest.mark.parametrize("layout", [0, 1])
+def test_gram_split_products_exact_on_short_values(qe, layout):
+    """Integers |x| <= 15 are their own bf16 h part (m = l = 0) and, scaled by
+    the channel's power of two, their own fp16 h part (m = 0); with integer
+    products and partial sums below 2^24 every step is exact (the scaling
+    moves only exponents), so every product path returns the exact integer
+    Gram."""
     rng = np.random.default_rng(11)
     X = rng.integers(-15, 16, size=(256, 2048)).astype(np.float32)
     exact = (X.astype(np.int64) @ X.T.astype(np.int64)).astype(np.float32)
-    assert np.array_equal(_gram(qe, X), exact)
-    assert np.array_equal(_gram(qe, X, fp32=True), exact)
+    Xl = X if layout == 0 else np.ascontiguousarray(X.T)
+    for mode in MODES:
+        assert np.array_equal(_gram(qe, Xl, layout, mode=mode), exact), mode
 
 
-def test_gram_split_reconstructs_low_bits(qe, oracle):
-    """x = +-(1 + k 2^-20), k < 16: bf16(x) = +-1, so all of the k part lives in
-    the m plane.  The off-diagonal error must stay far below what the h plane
-    alone would give (the Gram of the signs)."""
+@pytest.mark.parametrize("mode", ["default", "bf16x3"])
+def test_gram_split_reconstructs_low_bits(qe, oracle, mode):
+    """x = +-(1 + k 2^-20), k < 16: bf16(x) = +-1 and, with the channel
+    scaled to 2^14 (1 + k 2^-20), fp16 of it is +-2^14, so all of the k part
+    lives in the m plane of either split.  The off-diagonal error must stay
+    far below what the h plane alone would give (the Gram of the signs)."""
     rng = np.random.default_rng(12)
-    k = rng.integers(0, 16, size=(128, 512)).astype(np.float64)
-    sgn = rng.choice([-1.0, 1.0], size=(128, 512))
+    k = rng.integers(0, 16, size=(256, 512)).astype(np.float64)
+    sgn = rng.choice([-1.0, 1.0], size=(256, 512))
     X = (sgn * (1.0 + k * 2.0 ** -20)).astype(np.float32)
     ref = oracle.gram(X)
-    off = ~np.eye(128, dtype=bool)
-    err = np.max(np.abs(_gram(qe, X) - ref)[off])
+    off = ~np.eye(256, dtype=bool)
+    err = np.max(np.abs(_gram(qe, X, mode=mode) - ref)[off])
     gap = np.max(np.abs(oracle.gram(sgn.astype(np.float32)) - ref)[off])
     assert err <= 0.05 * gap
+
+
+def _ranged_channels(p, n, seed):
+    """Channels whose magnitudes span 2^-40 .. 2^40 (fp16 alone covers 2^-24
+    .. 2^16), with special channels: all zero, a single nonzero, a largest
+    |x| that is exactly a power of two, one just below a power of two (its
+    scaled value rounds up to 2^15 in fp16), and values spread log-uniformly
+    over 2^-30 .. 1 of the channel's largest."""
+    rng = np.random.default_rng(seed)
+    X = rng.standard_t(4, size=(p, n))
+    X *= 2.0 ** rng.uniform(-40, 40, size=(p, 1))
+    X[3] = 0.0
+    X[5] = 0.0
+    X[5, n // 3] = -3.0e-7
+    X[7] = np.clip(X[7], -1.0, 1.0) * 2.0 ** 9
+    X[7, 11] = 2.0 ** 10
+    X[9] = np.clip(X[9], -1.0, 1.0)
+    X[9, 17] = -np.float32(1 - 2.0 ** -24) * 2.0 ** 6
+    X[11] = rng.choice([-1.0, 1.0], size=n) * 2.0 ** rng.uniform(-30, 0, size=n)
+    return X.astype(np.float32)
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("layout", [0, 1])
+def test_gram_channel_scales(qe, oracle, mode, layout):
+    """Every entry against the oracle relative to its Cauchy-Schwarz scale,
+    |S_ij - ref_ij| <= 1e-5 sqrt(ref_ii ref_jj), on channels 2^80 apart (no
+    single fp16 scale holds them, so this pins the per-channel power-of-two
+    scaling and its exact removal); the all-zero channel's row and column
+    exactly 0."""
+    p, n = 256, 1024
+    X = _ranged_channels(p, n, seed=21)
+    Xl = X if layout == 0 else np.ascontiguousarray(X.T)
+    S = _gram(qe, Xl, layout, mode=mode).astype(np.float64)
+    ref = oracle.gram(X)
+    d = np.sqrt(np.diag(ref))
+    assert np.all(np.abs(S - ref) <= 1e-5 * np.outer(d, d))
+    assert not np.any(S[3]) and not np.any(S[:, 3])
+    assert np.array_equal(S, S.T)
 
 
 @pytest.mark.parametrize("p,cuts", [(320, (1000, 2100)), (512, (1024, 2048 + 512))])
