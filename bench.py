@@ -35,7 +35,8 @@ METRIC = "CD sweep time per layer (s) and column-updates/s at 4096×4096 4-bit"
 HBM_PEAK_GBS = 8000.0
 FP32_MFMA_PEAK_TFLOPS = 157.3
 BF16_MFMA_PEAK_TFLOPS = 2500.0
-SPLIT_PRODUCTS = 6             # bf16 products per fp32 product (exact three-way split)
+FP16_MFMA_PEAK_TFLOPS = 2500.0
+GRAM_PRODUCTS = 3              # fp16 products per fp32 product (two-way split of scaled channels)
 INT_DELTA_PRODUCTS = 3         # integer code difference x three bf16 planes of Sigma
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_c2_4096x4096.md")
 LAUNCH_PROFILE = os.path.join(ROOT, "profiles", "kernel_trace_gram_cd_step_c2_4096x4096.md")
@@ -46,7 +47,7 @@ CALIB_COPY_BYTES = 256 << 20
 
 # HIP sources each measured kernel is compiled from
 KERNEL_SOURCES = {
-    "gram_x3w_kernel": ["gram.hip", "nt_x3.h", "qe_internal.h"],
+    "gram_x3w_kernel": ["gram.hip", "nt_f2.h", "nt_x3.h", "qe_internal.h"],
     "cd_step_kernel": ["cd.hip", "nt_x3.h", "qe_internal.h"],
 }
 
@@ -345,37 +346,42 @@ def main():
     sweep_t = cd_phase_t / sweeps
     traffic = measured_traffic()
 
-    def roofline(kernel, flops, seconds, products, issued, extra):
+    def roofline(kernel, flops, seconds, cores, products, issued, extra):
         """The method's own flops (fp32 multiply-adds x 2) per launch over the
-        launch time, against the peak of the matrix-core type issued (bf16);
-        the issue rate (`products` exact bf16 products per fp32 product) and
-        the fp32-equivalent fraction are separate fields."""
+        launch time, against the peak of the matrix-core type issued (`cores`:
+        bf16 or fp16, both 2.5 PFLOP/s dense); the issue rate (`products`
+        exact products of that type per fp32 product) and the fp32-equivalent
+        fraction are separate fields."""
+        peak = BF16_MFMA_PEAK_TFLOPS if cores == "bf16" else FP16_MFMA_PEAK_TFLOPS
         achieved = flops / seconds / 1e12
         r = {"kernel": kernel, "bound": "mfma", "achieved": achieved,
-             "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-             "frac": achieved / BF16_MFMA_PEAK_TFLOPS,
+             "peak": peak, "unit": "TFLOP/s",
+             "frac": achieved / peak,
              "traffic": traffic.get(kernel.split("<")[0]),
              "flops_per_launch": flops,
              "flops_counted": "the method's: fp32 products of the algorithm, 2 flops each",
              "issued": issued,
-             "bf16_products_per_fp32_product": products,
-             "issued_bf16_tflops": products * achieved,
-             "issued_frac_of_bf16_peak": products * achieved / BF16_MFMA_PEAK_TFLOPS,
+             "matrix_cores": cores,
+             "products_per_fp32_product": products,
+             "issued_tflops": products * achieved,
+             "issued_frac_of_peak": products * achieved / peak,
              "fp32_equivalent_frac": achieved / FP32_MFMA_PEAK_TFLOPS,
-             "frac_of_split_ceiling": achieved / (BF16_MFMA_PEAK_TFLOPS / products)}
+             "frac_of_split_ceiling": achieved / (peak / products)}
         r.update(extra)
         return r
 
     # 2qp^2 per sweep over its nb + 1 launches; p(p+1)n for the Gram (symmetric half).
     # The resumed sweeps start from valid codes, so the block update multiplies
     # integer code differences (one exact bf16 plane) by Sigma's three planes.
-    roof_cd = roofline("cd_step_kernel<8>", 2.0 * q * p * p / (nb + 1), cd_avg,
+    roof_cd = roofline("cd_step_kernel<8>", 2.0 * q * p * p / (nb + 1), cd_avg, "bf16",
                        INT_DELTA_PRODUCTS,
                        "bf16 matrix cores: integer code differences (exact in bf16) times "
                        "the three bf16 planes of Sigma, 3 products per fp32 product",
                        {"avg_launch_s": cd_avg, "launches_per_sweep": nb + 1})
-    roof_gram = roofline("gram_x3w_kernel", float(p) * (p + 1) * n, gram_t, SPLIT_PRODUCTS,
-                         "bf16 matrix cores, 6 exact bf16 products per fp32 product",
+    roof_gram = roofline("gram_x3w_kernel", float(p) * (p + 1) * n, gram_t, "fp16", GRAM_PRODUCTS,
+                         "fp16 matrix cores: each channel scaled by a power of two and split "
+                         "into two fp16 values, 3 exact fp16 products per fp32 product "
+                         "(the call includes the pass that finds the scales)",
                          {"call_s": gram_t})
 
     # the Gram from token-major activations (n x p, as a model produces them),
@@ -424,7 +430,8 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32 (matrix products: bf16x3 split, f32 accumulate)",
+        "dtype": "f32 (matrix products: Gram fp16x2 split of power-of-two-scaled channels, "
+                 "CD bf16x3 split; f32 accumulate)",
         "data": "synthetic",
         "config": {"workload": spec.name, "q": q, "p": p, "n": n, "bits": bits,
                    "sweeps": sweeps, "block": block, "damp": spec.damp},
@@ -458,7 +465,8 @@ def main():
         mp = peaks.measure(torch)
         result["measured_peaks"] = mp
         for r in result["rooflines"]:
-            r["issued_frac_of_measured_bf16_peak"] = r["issued_bf16_tflops"] / mp["mfma_bf16_tflops"]
+            r["issued_frac_of_measured_peak"] = (r["issued_tflops"] /
+                                                 mp[f"mfma_{r['matrix_cores']}_tflops"])
 
     if not args.no_cpu:
         log("CPU oracle baseline")

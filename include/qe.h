@@ -118,11 +118,11 @@ qe_status qe_sync_status(void* ws, void* stream);
  * damp = 0 on all but the last).  The result is exactly symmetric.
  * Products, by default: when p is a multiple of 256, X's rows 16-byte aligned
  * and (channel-major X) n a multiple of 32, each channel i is first scaled by
- * 2^e_i (exact; its largest |x| lands in [2^14, 2^15), a pass over X) and
- * each scaled value y split into two fp16 values (h = fp16(y),
- * m = fp16(y - h)); y_i y_j is formed from the three products h h, h m, m h
- * on the fp16 matrix cores, every product exact in fp32, and the sums are
- * scaled back by 2^-(e_i + e_j).  The dropped terms are below
+ * 2^e_i (exact; its largest |x| lands in [2^14, 2^15), a pass over X; e_i at
+ * most 127) and each scaled value y split into two fp16 values
+ * (h = fp16(y), m = fp16(y - h)); y_i y_j is formed from the three products
+ * h h, h m, m h on the fp16 matrix cores, every product exact in fp32, and
+ * the sums are scaled back by 2^-(e_i + e_j).  The dropped terms are below
  * 3 * 2^-22 |y_i y_j| (plus 2^-39 of the channels' largest values for the
  * smallest ones).  Otherwise, or with QE_GRAM_BF16X3, each fp32 value x is
  * split exactly into three bf16 values (h = bf16(x), m = bf16(x - h),

@@ -309,14 +309,14 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
     if constexpr (F2) {
         // this thread stages row t / 2 of both panels
-        const int ea = chexp[ti * kWide + (threadIdx.x >> 1)];
-        const int eb = chexp[tj * kWide + (threadIdx.x >> 1)];
+        const float ea = ldexpf(1.f, chexp[ti * kWide + (threadIdx.x >> 1)]);
+        const float eb = ldexpf(1.f, chexp[tj * kWide + (threadIdx.x >> 1)]);
         if constexpr (TRANS) {
             const F2Op<X3Col> A{{X + k0 * p, p, 0, K}, ea}, B{{X + k0 * p, p, 0, K}, eb};
-            nt_tile_f2_wide(A, ti * kWide, B, tj * kWide, K, lds, acc);
+            nt_tile_f2_wide<4>(A, ti * kWide, B, tj * kWide, K, lds, acc);
         } else {
             const F2Op<X3Row> A{{X + k0, n, 0, K}, ea}, B{{X + k0, n, 0, K}, eb};
-            nt_tile_f2_wide(A, ti * kWide, B, tj * kWide, K, lds, acc);
+            nt_tile_f2_wide<4>(A, ti * kWide, B, tj * kWide, K, lds, acc);
         }
     } else if constexpr (TRANS) {
         // X is n x p: element (channel r, token k) at X[k * p + r]
@@ -436,14 +436,15 @@ __global__ __launch_bounds__(256) void damp_kernel(float* Sigma, int64_t p, floa
 }
 
 // Channel exponents of the fp16 split: e with the channel's largest |x| times
-// 2^e in [2^14, 2^15) (frexp: amax = f 2^ex, f in [1/2, 1)); 0 for an all-zero
-// or non-finite channel (a non-finite value reaches Sigma as in fp32).
+// 2^e in [2^14, 2^15) (frexp: amax = f 2^ex, f in [1/2, 1)), at most 127 (2^e
+// a normal float; e >= -113 holds for any finite amax); 0 for an all-zero or
+// non-finite channel (a non-finite value reaches Sigma as in fp32).
 __device__ inline int chan_exp(float amax)
 {
     if (!(amax > 0.f) || !isfinite(amax)) return 0;
     int ex;
     (void)frexpf(amax, &ex);
-    return 15 - ex;
+    return min(15 - ex, 127);
 }
 
 __device__ inline float absmax4(float m, f32x4 v)
@@ -491,7 +492,7 @@ __global__ __launch_bounds__(256) void chan_absmax_np_kernel(const float* __rest
     if (x_vec4) {
         // p % 4 == 0 and 16-byte aligned token rows: the 4 columns are inside X
         float a = 0.f, b = 0.f, cc = 0.f, d = 0.f;
-#pragma unroll 4
+#pragma unroll 8
         for (int64_t t = blockIdx.y; t < n; t += slices) {
             const f32x4 v = *reinterpret_cast<const f32x4*>(X + t * p + c);
             a = fmaxf(a, fabsf(v[0]));
@@ -519,15 +520,16 @@ __global__ __launch_bounds__(256) void chan_exp_np_kernel(const float* __restric
     const int64_t j = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (j >= p) return;
     float m = 0.f;
+#pragma unroll 8
     for (int y = 0; y < slices; ++y) m = fmaxf(m, part[y * p + j]);
     chexp[j] = chan_exp(m);
 }
 
-// Token slices of chan_absmax_np_kernel: about 1024 workgroups, at most 256
-// slices (the partials then hold at most 4 MB).
+// Token slices of chan_absmax_np_kernel: about 2048 workgroups, at most 512
+// slices (the partials then hold at most 8 MB).
 static int64_t chan_slices(int64_t p)
 {
-    return std::max<int64_t>(1, std::min<int64_t>(256, 1024 / cdiv(p, 1024)));
+    return std::max<int64_t>(1, std::min<int64_t>(512, 2048 / cdiv(p, 1024)));
 }
 
 // Workspace of the channel exponents: p ints and the token-major partials.

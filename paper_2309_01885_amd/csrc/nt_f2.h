@@ -2,7 +2,9 @@
 // power-of-two-scaled channels), on the 256 x 256 tile of eight waves.
 //
 // Channel i of X is scaled by 2^e_i, exactly, with e_i chosen so that the
-// channel's largest |x| lands in [2^14, 2^15) (a pre-pass over X).  Every
+// channel's largest |x| lands in [2^14, 2^15) (a pre-pass over X; e_i is
+// capped at 127 so that 2^e_i is a normal float, which leaves a channel whose
+// largest |x| is below 2^-112 under 2^14 after scaling).  Every
 // scaled value y then splits into two fp16 values,
 //     h = fp16(y),  m = fp16(y - h),
 // with round-to-nearest-even conversions: y - h is exact in fp32 and at most
@@ -21,10 +23,13 @@
 // stage buffers, global loads three stages ahead, one barrier per stage.
 // Per operand and stage the LDS holds 256 rows of 16 dwords: four 16-byte
 // slots (plane 2 p + half, each 8 k values of one plane) whose order is
-// permuted by row bits 2 and 3, so that the operand reads (16 consecutive
-// rows of one slot) and the staging writes (8 consecutive rows, both halves
-// of one plane) each cover the 64 banks once.
+// permuted by row bits 1 to 3, so that any 4, 8 or 16 consecutive lanes of an
+// operand read (consecutive rows, one slot) or of a staging write (row pairs,
+// both halves of one plane) touch distinct 16-byte bank groups: conflict-free
+// whether the 16-byte accesses are served 4, 8 or 16 lanes at a time.
 #pragma once
+
+#include <utility>
 
 #include "nt_x3.h"
 
@@ -33,13 +38,17 @@ namespace qe {
 constexpr int kF2RowDw = 16;                      // h, m: 8 dwords each
 constexpr int kF2OpDw = 256 * kF2RowDw;           // one operand of one stage
 constexpr int kF2BufDw = 2 * kF2OpDw;             // A and B of one stage
-constexpr int kF2LdsDw = 3 * kF2BufDw;            // three stages: 98,304 bytes
+constexpr int kF2LdsDw = 4 * kF2BufDw;            // four stages: 131,072 bytes
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 
-// Slot permutation of a row: bit 1 from row bit 2, bit 0 from row bit 3.
-__device__ inline int f2_perm(int row) { return (((row >> 2) & 1) << 1) | ((row >> 3) & 1); }
+// Slot permutation of a row (b_k: row bit k): bit 1 = b2 ^ b1, bit 0 = b3 ^ b1.
+__device__ inline int f2_perm(int row)
+{
+    const int b1 = (row >> 1) & 1;
+    return ((((row >> 2) & 1) ^ b1) << 1) | (((row >> 3) & 1) ^ b1);
+}
 
 // Dword offset of (row, half, plane) inside one operand's stage area.
 __device__ inline int f2_addr(int row, int half, int plane)
@@ -47,19 +56,20 @@ __device__ inline int f2_addr(int row, int half, int plane)
     return row * kF2RowDw + 4 * ((2 * plane + half) ^ f2_perm(row));
 }
 
-// Scales a stage held as thread t (row t / 2, k = 8 (t % 2) .. +7) by 2^e,
-// splits it and stores one 16-byte half of each plane.
-__device__ inline void f2_store_row8(uint32_t* op, const X3Stage& st, int e)
+// Scales a stage held as thread t (row t / 2, k = 8 (t % 2) .. +7) by the
+// power of two sc, splits it and stores one 16-byte half of each plane.  The
+// remainder x sc - h is one fused multiply-add with the fp16 h as its addend
+// (v_fma_mix_f32): exact, and the same value as (x sc) - h.
+__device__ inline void f2_store_row8(uint32_t* op, const X3Stage& st, float sc)
 {
     const int t = threadIdx.x;
     u32x4 h, m;
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-        const float a = ldexpf(st.v[u >> 1][2 * (u & 1)], e);
-        const float b = ldexpf(st.v[u >> 1][2 * (u & 1) + 1], e);
-        const f16x2 hh = __builtin_convertvector((f32x2){a, b}, f16x2);
-        const f32x2 hf = __builtin_convertvector(hh, f32x2);
-        const f16x2 mm = __builtin_convertvector((f32x2){a - hf[0], b - hf[1]}, f16x2);
+        const float x0 = st.v[u >> 1][2 * (u & 1)], x1 = st.v[u >> 1][2 * (u & 1) + 1];
+        const f16x2 hh = __builtin_convertvector((f32x2){x0 * sc, x1 * sc}, f16x2);
+        const f16x2 mm = __builtin_convertvector(
+            (f32x2){fmaf(x0, sc, -(float)hh[0]), fmaf(x1, sc, -(float)hh[1])}, f16x2);
         h[u] = __builtin_bit_cast(uint32_t, hh);
         m[u] = __builtin_bit_cast(uint32_t, mm);
     }
@@ -68,11 +78,11 @@ __device__ inline void f2_store_row8(uint32_t* op, const X3Stage& st, int e)
 }
 
 // A row-per-two-lanes loader (X3Row: channel-major, X3Col: token-major) whose
-// stages are split as above; e is the exponent of this thread's row.
+// stages are split as above; sc = 2^e of this thread's row.
 template <class Base>
 struct F2Op : Base {
-    int e;
-    __device__ inline void store(uint32_t* op, const X3Stage& st) const { f2_store_row8(op, st, e); }
+    float sc;
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const { f2_store_row8(op, st, sc); }
 };
 
 __device__ __forceinline__ f16x8 f2_frag(const uint32_t* p)
@@ -100,7 +110,7 @@ __device__ __forceinline__ void f2w_block(const f16x8 (&a)[2][2], const f16x8 (&
 // stage kload into (la, lb), and leaves fa and fb[0] holding the fragments of
 // `nxt` (stage c + 1).  offa[pl] / offb[pl]: this lane's plane-pl fragment of
 // row block 0 (further blocks of 32 rows keep the slot permutation).
-template <class OA, class OB>
+template <bool SYNC, class OA, class OB>
 __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                           int64_t kload, const uint32_t* cur, const uint32_t* nxt,
                                           uint32_t* wr, X3Stage& ga, X3Stage& gb, X3Stage& la,
@@ -120,7 +130,7 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
 #pragma unroll
     for (int i = 0; i < 6; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);     // VALU
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);     // VALU
     }
     __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);     // DS writes
     __builtin_amdgcn_sched_barrier(0);
@@ -133,19 +143,19 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
 #pragma unroll
     for (int i = 0; i < 6; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
     }
     __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
     __builtin_amdgcn_sched_barrier(0);
-    // group 2: B block 3 reads; the barrier makes stage c + 2 visible and ends
-    // this stage's reads of `cur`
+    // group 2: B block 3 reads; with SYNC, the barrier makes the stages written
+    // so far visible and ends the reads of the stages multiplied so far
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) fb[1][pl] = f2_frag(cur + offb[pl] + 3 * BLK);
     f2w_block(fa, fb[0], acc, 2);
     __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
     __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
     __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();
+    if constexpr (SYNC) __syncthreads();
     // group 3: next stage's B block 0 and A fragments, each after its last use
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) fb[0][pl] = f2_frag(nxt + offb[pl]);
@@ -173,30 +183,54 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
     __builtin_amdgcn_sched_barrier(0);
 }
 
-// Stage c with c % 3 == R: stage s lives in LDS buffer s % 3 and in register
-// set s % 3; the set that held stage c + 1 takes stage c + 4 (a load past the
-// last stage re-reads the last stage: in bounds, and it lands in a buffer no
-// stage reads).
-template <int R, class OA, class OB>
-__device__ __forceinline__ void f2w_stage3(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
-                                           int64_t c, int64_t nst, uint32_t* lds, X3Stage (&ga)[3],
-                                           X3Stage (&gb)[3], const int (&offa)[2],
-                                           const int (&offb)[2], f16x8 (&fa)[2][2],
-                                           f16x8 (&fb)[2][2], f32x16 (&acc)[2][4])
+// Stage s = c + R (c a multiple of the unroll, a multiple of 2 and 3): stage
+// s lives in LDS buffer s % NBUF and in register set s % 3; the set that held
+// stage s + 1 takes stage s + 4 (a load past the last stage re-reads the last
+// stage: in bounds, and it lands in a buffer no stage reads).  Stage s writes
+// stage s + 2 into buffer (s + 2) % NBUF.  With three buffers every stage
+// ends its reads with a barrier.  With four, only the odd stages do: a stage
+// reads its own buffer and (after its third block) the next one's; the next
+// stage's buffer was written two stages earlier, before an odd stage's barrier,
+// and the buffer a stage writes was last read two stages earlier, before one.
+template <int R, int NBUF, class OA, class OB>
+__device__ __forceinline__ void f2w_stage_r(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                            int64_t c, int64_t nst, uint32_t* lds,
+                                            X3Stage (&ga)[3], X3Stage (&gb)[3],
+                                            const int (&offa)[2], const int (&offb)[2],
+                                            f16x8 (&fa)[2][2], f16x8 (&fb)[2][2],
+                                            f32x16 (&acc)[2][4])
 {
-    f2w_stage(A, row0a, B, row0b, min(c + 4, nst - 1) * kX3KC, lds + R * kF2BufDw,
-              lds + ((R + 1) % 3) * kF2BufDw, lds + ((R + 2) % 3) * kF2BufDw, ga[(R + 2) % 3],
-              gb[(R + 2) % 3], ga[(R + 1) % 3], gb[(R + 1) % 3], offa, offb, fa, fb, acc);
+    f2w_stage<NBUF == 3 || (R & 1)>(
+        A, row0a, B, row0b, min(c + R + 4, nst - 1) * kX3KC, lds + (R % NBUF) * kF2BufDw,
+        lds + ((R + 1) % NBUF) * kF2BufDw, lds + ((R + 2) % NBUF) * kF2BufDw, ga[(R + 2) % 3],
+        gb[(R + 2) % 3], ga[(R + 1) % 3], gb[(R + 1) % 3], offa, offb, fa, fb, acc);
+}
+
+template <int NBUF, class OA, class OB, int... R>
+__device__ __forceinline__ void f2w_stages(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
+                                           int64_t c, int64_t nst, uint32_t* lds,
+                                           X3Stage (&ga)[3], X3Stage (&gb)[3],
+                                           const int (&offa)[2], const int (&offb)[2],
+                                           f16x8 (&fa)[2][2], f16x8 (&fb)[2][2],
+                                           f32x16 (&acc)[2][4], bool guarded,
+                                           std::integer_sequence<int, R...>)
+{
+    ((!guarded || c + R < nst
+          ? f2w_stage_r<R, NBUF>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc)
+          : void()),
+     ...);
 }
 
 // acc += A[row0a.., 0..K) B[row0b.., 0..K)^T (scaled values) on the 256 x 256
 // tile of 512 threads; K a positive multiple of 32, every 256-row panel
-// inside the matrix, aligned rows.  `lds` holds kF2LdsDw dwords.  Ends with
-// a barrier.
-template <class OA, class OB>
+// inside the matrix, aligned rows.  `lds` holds NBUF * kF2BufDw dwords.  Ends
+// with a barrier.
+template <int NBUF, class OA, class OB>
 __device__ __forceinline__ void nt_tile_f2_wide(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                                 int64_t K, uint32_t* lds, f32x16 (&acc)[2][4])
 {
+    static_assert(NBUF == 3 || NBUF == 4, "three or four stage buffers");
+    constexpr int U = NBUF == 3 ? 3 : 12;          // stages per loop trip
     const int64_t nst = K / kX3KC;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int wm = wave >> 1, wn = wave & 1;
@@ -224,14 +258,13 @@ __device__ __forceinline__ void nt_tile_f2_wide(const OA& A, int64_t row0a, cons
         for (int pl = 0; pl < 2; ++pl) fa[mi][pl] = f2_frag(lds + offa[pl] + mi * 32 * kF2RowDw);
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) fb[0][pl] = f2_frag(lds + offb[pl]);
+    constexpr auto all = std::make_integer_sequence<int, U>{};
     int64_t c = 0;
-    for (; c + 3 <= nst; c += 3) {
-        f2w_stage3<0>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc);
-        f2w_stage3<1>(A, row0a, B, row0b, c + 1, nst, lds, ga, gb, offa, offb, fa, fb, acc);
-        f2w_stage3<2>(A, row0a, B, row0b, c + 2, nst, lds, ga, gb, offa, offb, fa, fb, acc);
-    }
-    if (c < nst) f2w_stage3<0>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc);
-    if (c + 1 < nst) f2w_stage3<1>(A, row0a, B, row0b, c + 1, nst, lds, ga, gb, offa, offb, fa, fb, acc);
+    for (; c + U <= nst; c += U)
+        f2w_stages<NBUF>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc, false, all);
+    if (c < nst)
+        f2w_stages<NBUF>(A, row0a, B, row0b, c, nst, lds, ga, gb, offa, offb, fa, fb, acc, true,
+                         std::make_integer_sequence<int, U - 1>{});
     __syncthreads();
 }
 

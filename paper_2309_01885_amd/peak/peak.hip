@@ -3,11 +3,12 @@
 // libqe_peak.so, apart from libqe.so: these are measurement probes, not part
 // of the quantizer's C ABI.
 //
-//   qpk_mfma_bf16 / qpk_mfma_f32: register-only loops of the matrix-core
-//     instruction the split products (v_mfma_f32_32x32x16_bf16) and the fp32
-//     products (v_mfma_f32_32x32x2f32) use, four independent accumulators per
-//     wave, two waves per SIMD; the caller times the launch.  Flops per launch:
-//     blocks * 4 waves * iters * 16 MFMAs * (2 * 32 * 32 * K), K = 16 or 2.
+//   qpk_mfma_bf16 / qpk_mfma_f16 / qpk_mfma_f32: register-only loops of the
+//     matrix-core instruction the split products (v_mfma_f32_32x32x16_bf16,
+//     v_mfma_f32_32x32x16_f16) and the fp32 products (v_mfma_f32_32x32x2f32)
+//     use, four independent accumulators per wave, two waves per SIMD; the
+//     caller times the launch.  Flops per launch: blocks * 4 waves * iters *
+//     16 MFMAs * (2 * 32 * 32 * K), K = 16, 16 or 2.
 //   qpk_copy: dst = src over n 16-byte elements, grid-stride or one contiguous
 //     range per workgroup (HBM stream).
 //   qpk_clock: per-wave shader-clock and constant-rate (100 MHz) counter
@@ -22,6 +23,7 @@
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
@@ -52,6 +54,17 @@ __device__ inline void bf16_loop(int iters, const u32x4& ua, const u32x4& ub, f3
     }
 }
 
+// fp16 operands in [2^-2, 1) (exponent field 13 or 14) from the same LCG.
+__device__ inline void seed_f16(unsigned x, u32x4& ua, u32x4& ub)
+{
+    for (int i = 0; i < 4; ++i) {
+        x = x * 1664525u + 1013904223u;
+        ua[i] = (x & 0x07ff07ffu) | 0x34003400u;
+        x = x * 1664525u + 1013904223u;
+        ub[i] = (x & 0x07ff07ffu) | 0x34003400u;
+    }
+}
+
 __device__ inline float acc_sum(const f32x16 (&acc)[4])
 {
     float s = 0.f;
@@ -66,6 +79,22 @@ __global__ __launch_bounds__(kThreads, 2) void mfma_bf16_kernel(float* out, int 
     seed_bf16(threadIdx.x * 2654435761u ^ blockIdx.x * 40503u ^ 7u, ua, ub);
     f32x16 acc[4] = {};
     bf16_loop(iters, ua, ub, acc);
+    out[(size_t)blockIdx.x * kThreads + threadIdx.x] = acc_sum(acc);
+}
+
+__global__ __launch_bounds__(kThreads, 2) void mfma_f16_kernel(float* out, int iters)
+{
+    u32x4 ua, ub;
+    seed_f16(threadIdx.x * 2654435761u ^ blockIdx.x * 40503u ^ 7u, ua, ub);
+    const f16x8 a = __builtin_bit_cast(f16x8, ua), b = __builtin_bit_cast(f16x8, ub);
+    f32x16 acc[4] = {};
+    for (int it = 0; it < iters; ++it) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int k = 0; k < 4; ++k)
+                acc[k] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[k], 0, 0, 0);
+    }
     out[(size_t)blockIdx.x * kThreads + threadIdx.x] = acc_sum(acc);
 }
 
@@ -139,6 +168,14 @@ int qpk_mfma_bf16(float* out, int blocks, int iters, void* stream)
 {
     if (!out || blocks <= 0 || iters <= 0) return 1;
     hipLaunchKernelGGL(mfma_bf16_kernel, dim3(blocks), dim3(kThreads), 0, (hipStream_t)stream,
+                       out, iters);
+    return launched();
+}
+
+int qpk_mfma_f16(float* out, int blocks, int iters, void* stream)
+{
+    if (!out || blocks <= 0 || iters <= 0) return 1;
+    hipLaunchKernelGGL(mfma_f16_kernel, dim3(blocks), dim3(kThreads), 0, (hipStream_t)stream,
                        out, iters);
     return launched();
 }

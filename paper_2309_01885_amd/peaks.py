@@ -1,6 +1,6 @@
 """Peak checks for the roofline denominators (libqe_peak.so, built beside
-libqe.so from peak/peak.hip): matrix-core throughput of the bf16 and fp32
-MFMA instructions the products use, in register-only loops; the engine clock
+libqe.so from peak/peak.hip): matrix-core throughput of the bf16, fp16 and
+fp32 MFMA instructions the products use, in register-only loops; the engine clock
 under that load; and an HBM copy.  The vendor peaks stay the roofline
 denominators; these say how much of them this chip sustains."""
 import ctypes
@@ -21,7 +21,8 @@ def load():
             raise RuntimeError(f"{LIB_PATH} is not built (run __graft_entry__.build())")
         lib = ctypes.CDLL(LIB_PATH)
         vp, i = ctypes.c_void_p, ctypes.c_int
-        for f, args in (("qpk_mfma_bf16", [vp, i, i, vp]), ("qpk_mfma_f32", [vp, i, i, vp]),
+        for f, args in (("qpk_mfma_bf16", [vp, i, i, vp]), ("qpk_mfma_f16", [vp, i, i, vp]),
+                        ("qpk_mfma_f32", [vp, i, i, vp]),
                         ("qpk_clock", [vp, vp, i, i, vp]),
                         ("qpk_copy", [vp, vp, ctypes.c_size_t, i, i, vp])):
             getattr(lib, f).argtypes = args
@@ -57,10 +58,13 @@ def measure(torch, bf16_iters=4000, f32_iters=2000, copy_bytes=1 << 30):
     out = torch.empty(BLOCKS * 256, dtype=torch.float32, device=dev)
     t_bf = _timed(torch, lambda: _ok(lib.qpk_mfma_bf16(out.data_ptr(), BLOCKS, bf16_iters, st),
                                      "qpk_mfma_bf16"))
+    t_f16 = _timed(torch, lambda: _ok(lib.qpk_mfma_f16(out.data_ptr(), BLOCKS, bf16_iters, st),
+                                      "qpk_mfma_f16"))
     t_f32 = _timed(torch, lambda: _ok(lib.qpk_mfma_f32(out.data_ptr(), BLOCKS, f32_iters, st),
                                       "qpk_mfma_f32"))
     waves_iters = BLOCKS * 4 * 16           # waves x MFMAs per iteration
     bf_tf = waves_iters * bf16_iters * 2 * 32 * 32 * 16 / t_bf / 1e12
+    f16_tf = waves_iters * bf16_iters * 2 * 32 * 32 * 16 / t_f16 / 1e12
     f32_tf = waves_iters * f32_iters * 2 * 32 * 32 * 2 / t_f32 / 1e12
     clk = torch.zeros(BLOCKS * 4 * 2, dtype=torch.int64, device=dev)
     _ok(lib.qpk_clock(out.data_ptr(), clk.data_ptr(), BLOCKS, bf16_iters, st), "qpk_clock")
@@ -74,10 +78,10 @@ def measure(torch, bf16_iters=4000, f32_iters=2000, copy_bytes=1 << 30):
                for b, ch in COPY_SHAPES)
     ok = bool(torch.equal(src, dst))
     del src, dst
-    return {"mfma_bf16_tflops": bf_tf, "mfma_f32_tflops": f32_tf,
+    return {"mfma_bf16_tflops": bf_tf, "mfma_f16_tflops": f16_tf, "mfma_f32_tflops": f32_tf,
             "engine_clock_ghz_under_mfma": ghz, "copy_gbps": 2 * n16 * 16 / t_cp / 1e9,
             "copy_checked": ok,
-            "method": (f"register-only v_mfma_f32_32x32x16_bf16 / v_mfma_f32_32x32x2f32 loops, "
+            "method": (f"register-only v_mfma_f32_32x32x16_bf16 / _f16 / v_mfma_f32_32x32x2f32 loops, "
                        f"{BLOCKS} workgroups of 4 waves, 4 accumulators a wave; clock from "
                        f"s_memtime over s_memrealtime; copy of {copy_bytes >> 20} MiB, best of "
                        f"(workgroups, chunked) in {COPY_SHAPES}; best of 3")}

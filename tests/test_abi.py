@@ -74,16 +74,16 @@ def test_workspace_sizes(lib):
     128 x 128 tiles (64 KiB each) after the 256-byte status word; at 59392
     channels the partials would not fit, so Sigma is written directly.  Then
     the channel exponents of the fp16 split (p ints) and the token-major
-    pre-pass partials (slices x p floats, about 1024 workgroups of 1024
-    channels: 256 slices at p = 4096, 17 at p = 59392)."""
+    pre-pass partials (slices x p floats, about 2048 workgroups of 1024
+    channels: 512 slices at p = 4096, 35 at p = 59392)."""
     L, _ = lib
     for f in ("qe_gram_workspace_size", "qe_cd_workspace_size", "qe_objective_workspace_size",
               "qe_lambda_workspace_size", "qe_outlier_workspace_size", "qe_topk_workspace_size",
               "qe_topk_columns_workspace_size"):
         getattr(L, f).restype = ctypes.c_size_t
     L.qe_gram_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64]
-    assert L.qe_gram_workspace_size(4096, 262144) == 256 + 15 * 528 * 65536 + 4096 * 4 + 256 * 4096 * 4
-    assert L.qe_gram_workspace_size(59392, 32768) == 256 + 59392 * 4 + 17 * 59392 * 4
+    assert L.qe_gram_workspace_size(4096, 262144) == 256 + 15 * 528 * 65536 + 4096 * 4 + 512 * 4096 * 4
+    assert L.qe_gram_workspace_size(59392, 32768) == 256 + 59392 * 4 + 35 * 59392 * 4
     assert L.qe_gram_workspace_size(0, 10) == 256
     L.qe_cd_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
     c2 = L.qe_cd_workspace_size(4096, 4096, 0)
@@ -257,6 +257,7 @@ def test_peak_library_exports_and_argument_errors():
     from paper_2309_01885_amd import peaks
     L = peaks.load()
     assert L.qpk_mfma_bf16(None, 512, 10, None) == 1
+    assert L.qpk_mfma_f16(DUMMY, 512, 0, None) == 1
     assert L.qpk_mfma_f32(DUMMY, 0, 10, None) == 1
     assert L.qpk_clock(DUMMY, None, 512, 10, None) == 1
     assert L.qpk_copy(DUMMY, ctypes.c_void_p(4100), 16, 64, 0, None) == 1    # misaligned

@@ -108,6 +108,33 @@ def _ranged_channels(p, n, seed):
 
 @pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("layout", [0, 1])
+def test_gram_tiny_elements_beside_a_large_one(qe, oracle, mode, layout):
+    """Channel a holds one value 1 (its scale: 2^14 after scaling) and values
+    2^-26 .. 2^-34 elsewhere, whose scaled h parts are fp16 subnormals; channel
+    b is 0 where a is 1, so Sigma_ab comes from a's tiny values alone.  Their
+    split keeps an absolute error of at most 2^-25 in scaled units (2^-39 of
+    the channel's largest), a relative 2^-15 .. 2^-7 of each value, errors
+    that average out over the tokens: Sigma_ab within 2e-3 of the oracle (a
+    CPU model of the split gives 6e-4).  fp16 subnormals taken as 0 in the
+    split would leave it off by about 18%."""
+    p, n = 256, 2048
+    rng = np.random.default_rng(31)
+    X = rng.standard_normal((p, n))
+    a, b = 1, 2
+    X[a] = rng.choice([-1.0, 1.0], size=n) * 2.0 ** rng.uniform(-34, -26, size=n)
+    X[a, 0] = 1.0
+    X[b, 0] = 0.0
+    X = X.astype(np.float32)
+    Xl = X if layout == 0 else np.ascontiguousarray(X.T)
+    S = _gram(qe, Xl, layout, mode=mode).astype(np.float64)
+    ref = oracle.gram(X)
+    assert abs(S[a, b] - ref[a, b]) <= 2e-3 * abs(ref[a, b])
+    d = np.sqrt(np.diag(ref))
+    assert np.all(np.abs(S - ref) <= 1e-5 * np.outer(d, d))
+
+
+@pytest.mark.parametrize("mode", MODES)
+@pytest.mark.parametrize("layout", [0, 1])
 def test_gram_channel_scales(qe, oracle, mode, layout):
     """Every entry against the oracle relative to its Cauchy-Schwarz scale,
     |S_ij - ref_ij| <= 1e-5 sqrt(ref_ii ref_jj), on channels 2^80 apart (no

@@ -13,6 +13,7 @@ def test_measured_peaks_are_sane():
     print(m, flush=True)
     assert m["copy_checked"]
     assert 0.3 * 2500 < m["mfma_bf16_tflops"] < 1.05 * 2500
+    assert 0.3 * 2500 < m["mfma_f16_tflops"] < 1.05 * 2500
     assert 0.3 * 157.3 < m["mfma_f32_tflops"] < 1.05 * 157.3
     assert 0.5 < m["engine_clock_ghz_under_mfma"] < 2.6
     assert 0 < m["copy_gbps"] < 8000
