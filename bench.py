@@ -465,8 +465,8 @@ def main():
         mp = peaks.measure(torch)
         result["measured_peaks"] = mp
         for r in result["rooflines"]:
-            r["issued_frac_of_measured_peak"] = (r["issued_tflops"] /
-                                                 mp[f"mfma_{r['matrix_cores']}_tflops"])
+            key = {"bf16": "mfma_bf16_tflops", "fp16": "mfma_f16_tflops"}[r["matrix_cores"]]
+            r["issued_frac_of_measured_peak"] = r["issued_tflops"] / mp[key]
 
     if not args.no_cpu:
         log("CPU oracle baseline")

@@ -525,17 +525,19 @@ __global__ __launch_bounds__(256) void chan_exp_np_kernel(const float* __restric
     chexp[j] = chan_exp(m);
 }
 
-// Token slices of chan_absmax_np_kernel: about 2048 workgroups, at most 512
-// slices (the partials then hold at most 8 MB).
-static int64_t chan_slices(int64_t p)
+// Token slices of chan_absmax_np_kernel: about 2048 workgroups, at least 256
+// tokens a slice, at most 512 slices (the partials then hold at most 8 MB).
+static int64_t chan_slices(int64_t p, int64_t n)
 {
-    return std::max<int64_t>(1, std::min<int64_t>(512, 2048 / cdiv(p, 1024)));
+    return std::max<int64_t>(
+        1, std::min<int64_t>(std::min<int64_t>(512, 2048 / cdiv(p, 1024)), cdiv(n, 256)));
 }
 
 // Workspace of the channel exponents: p ints and the token-major partials.
-static size_t chan_ws_bytes(int64_t p)
+static size_t chan_ws_bytes(int64_t p, int64_t n)
 {
-    return align256((size_t)p * sizeof(int)) + align256((size_t)chan_slices(p) * p * sizeof(float));
+    return align256((size_t)p * sizeof(int)) +
+           align256((size_t)chan_slices(p, n) * p * sizeof(float));
 }
 
 // Number of token splits, or 0 for the two-level direct mode.
@@ -584,7 +586,7 @@ static size_t gram_ws_one(int64_t p, int64_t n)
     const int64_t tiles = nt * (nt + 1) / 2;
     const int64_t splits = gram_splits(p, n);
     return kStatusBytes + align256((size_t)splits * tiles * kTileFloats * sizeof(float)) +
-           chan_ws_bytes(p);
+           chan_ws_bytes(p, n);
 }
 
 // Token-major X with a token count that is not a multiple of 32 is taken as
@@ -670,7 +672,7 @@ static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layou
             const dim3 grid((unsigned)(8 * cdiv(tiles_w * used, 8)));
             if (f2) {
                 if (trans) {
-                    const int64_t sl = chan_slices(p);
+                    const int64_t sl = chan_slices(p, n);
                     hipLaunchKernelGGL(chan_absmax_np_kernel,
                                        dim3((unsigned)cdiv(p, 1024), (unsigned)sl), dim3(256), 0, s,
                                        X, p, n, x_vec4, chpart, status);

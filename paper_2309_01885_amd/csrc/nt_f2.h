@@ -29,6 +29,7 @@
 // whether the 16-byte accesses are served 4, 8 or 16 lanes at a time.
 #pragma once
 
+#include <type_traits>
 #include <utility>
 
 #include "nt_x3.h"
@@ -110,7 +111,7 @@ __device__ __forceinline__ void f2w_block(const f16x8 (&a)[2][2], const f16x8 (&
 // stage kload into (la, lb), and leaves fa and fb[0] holding the fragments of
 // `nxt` (stage c + 1).  offa[pl] / offb[pl]: this lane's plane-pl fragment of
 // row block 0 (further blocks of 32 rows keep the slot permutation).
-template <bool SYNC, class OA, class OB>
+template <bool SYNC, bool HINTS, class OA, class OB>
 __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                           int64_t kload, const uint32_t* cur, const uint32_t* nxt,
                                           uint32_t* wr, X3Stage& ga, X3Stage& gb, X3Stage& la,
@@ -125,35 +126,41 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
     for (int pl = 0; pl < 2; ++pl) fb[1][pl] = f2_frag(cur + offb[pl] + 1 * BLK);
     f2w_block(fa, fb[0], acc, 0);
     A.store(wr, ga);
-    __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);     // VMEM reads
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // DS reads
+    if constexpr (HINTS) {
+        __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);     // VMEM reads
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // DS reads
 #pragma unroll
-    for (int i = 0; i < 6; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);     // VALU
+        for (int i = 0; i < 6; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);     // VALU
+        }
+        __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);     // DS writes
     }
-    __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);     // DS writes
     __builtin_amdgcn_sched_barrier(0);
     // group 1: B block 2 reads, split of B
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) fb[0][pl] = f2_frag(cur + offb[pl] + 2 * BLK);
     f2w_block(fa, fb[1], acc, 1);
     B.store(wr + kF2OpDw, gb);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    if constexpr (HINTS) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
 #pragma unroll
-    for (int i = 0; i < 6; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        for (int i = 0; i < 6; ++i) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
     __builtin_amdgcn_sched_barrier(0);
     // group 2: B block 3 reads; with SYNC, the barrier makes the stages written
     // so far visible and ends the reads of the stages multiplied so far
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) fb[1][pl] = f2_frag(cur + offb[pl] + 3 * BLK);
     f2w_block(fa, fb[0], acc, 2);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+    if constexpr (HINTS) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
+    }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (SYNC) __syncthreads();
     // group 3: next stage's B block 0 and A fragments, each after its last use
@@ -175,13 +182,21 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
             }
         }
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    if constexpr (HINTS) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+    }
     __builtin_amdgcn_sched_barrier(0);
 }
+
+// The instruction-order hints of f2w_stage pay off for the token-major loader
+// (its sixteen 4-byte loads per stage) and cost 2% for the channel-major one,
+// which the compiler's own order serves better.
+template <class O> struct F2Plain : std::false_type {};
+template <> struct F2Plain<F2Op<X3Row>> : std::true_type {};
 
 // Stage s = c + R (c a multiple of the unroll, a multiple of 2 and 3): stage
 // s lives in LDS buffer s % NBUF and in register set s % 3; the set that held
@@ -200,7 +215,7 @@ __device__ __forceinline__ void f2w_stage_r(const OA& A, int64_t row0a, const OB
                                             f16x8 (&fa)[2][2], f16x8 (&fb)[2][2],
                                             f32x16 (&acc)[2][4])
 {
-    f2w_stage<NBUF == 3 || (R & 1)>(
+    f2w_stage<NBUF == 3 || (R & 1), !F2Plain<OA>::value>(
         A, row0a, B, row0b, min(c + R + 4, nst - 1) * kX3KC, lds + (R % NBUF) * kF2BufDw,
         lds + ((R + 1) % NBUF) * kF2BufDw, lds + ((R + 2) % NBUF) * kF2BufDw, ga[(R + 2) % 3],
         gb[(R + 2) % 3], ga[(R + 1) % 3], gb[(R + 1) % 3], offa, offb, fa, fb, acc);

@@ -74,8 +74,9 @@ def test_workspace_sizes(lib):
     128 x 128 tiles (64 KiB each) after the 256-byte status word; at 59392
     channels the partials would not fit, so Sigma is written directly.  Then
     the channel exponents of the fp16 split (p ints) and the token-major
-    pre-pass partials (slices x p floats, about 2048 workgroups of 1024
-    channels: 512 slices at p = 4096, 35 at p = 59392)."""
+    pre-pass partials (slices x p floats: about 2048 workgroups of 1024
+    channels, at least 256 tokens a slice; 512 slices at p = 4096 and 262144
+    tokens, 128 at 32768 tokens, 35 at p = 59392)."""
     L, _ = lib
     for f in ("qe_gram_workspace_size", "qe_cd_workspace_size", "qe_objective_workspace_size",
               "qe_lambda_workspace_size", "qe_outlier_workspace_size", "qe_topk_workspace_size",
@@ -84,6 +85,9 @@ def test_workspace_sizes(lib):
     L.qe_gram_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64]
     assert L.qe_gram_workspace_size(4096, 262144) == 256 + 15 * 528 * 65536 + 4096 * 4 + 512 * 4096 * 4
     assert L.qe_gram_workspace_size(59392, 32768) == 256 + 59392 * 4 + 35 * 59392 * 4
+    # a 32768-token chunk at 4096 channels: 13 splits of 2528 tokens fill the 256 CUs
+    assert (L.qe_gram_workspace_size(4096, 32768) ==
+            256 + 13 * 528 * 65536 + 4096 * 4 + 128 * 4096 * 4)
     assert L.qe_gram_workspace_size(0, 10) == 256
     L.qe_cd_workspace_size.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int]
     c2 = L.qe_cd_workspace_size(4096, 4096, 0)
