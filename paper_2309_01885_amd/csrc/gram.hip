@@ -307,17 +307,23 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
         for (int ni = 0; ni < 4; ++ni)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
-    if constexpr (F2) {
-        // this thread stages row t / 2 of both panels
-        const float ea = ldexpf(1.f, chexp[ti * kWide + (threadIdx.x >> 1)]);
-        const float eb = ldexpf(1.f, chexp[tj * kWide + (threadIdx.x >> 1)]);
-        if constexpr (TRANS) {
-            const F2Op<X3Col> A{{X + k0 * p, p, 0, K}, ea}, B{{X + k0 * p, p, 0, K}, eb};
-            nt_tile_f2_wide<4>(A, ti * kWide, B, tj * kWide, K, lds, acc);
-        } else {
-            const F2Op<X3Row> A{{X + k0, n, 0, K}, ea}, B{{X + k0, n, 0, K}, eb};
-            nt_tile_f2_wide<4>(A, ti * kWide, B, tj * kWide, K, lds, acc);
-        }
+    if constexpr (F2 && TRANS) {
+        // X is n x p; this thread stages channel t / 2 of both panels (eight
+        // tokens); four stage buffers
+        const int r = threadIdx.x >> 1;
+        const F2Op<X3Col> A{{X + k0 * p, p, 0, K}, ldexpf(1.f, chexp[ti * kWide + r])};
+        const F2Op<X3Col> B{{X + k0 * p, p, 0, K}, ldexpf(1.f, chexp[tj * kWide + r])};
+        nt_tile_f2_wide<4>(A, ti * kWide, B, tj * kWide, K, lds, acc);
+    } else if constexpr (F2) {
+        // this thread stages channels t / 4 and t / 4 + 128 of both panels
+        // (four tokens each); three stage buffers, which keep the loop free of
+        // register spills
+        const int r = threadIdx.x >> 2;
+        const F2RowQ A{X + k0, n, {ldexpf(1.f, chexp[ti * kWide + r]),
+                                   ldexpf(1.f, chexp[ti * kWide + r + 128])}};
+        const F2RowQ B{X + k0, n, {ldexpf(1.f, chexp[tj * kWide + r]),
+                                   ldexpf(1.f, chexp[tj * kWide + r + 128])}};
+        nt_tile_f2_wide<3>(A, ti * kWide, B, tj * kWide, K, lds, acc);
     } else if constexpr (TRANS) {
         // X is n x p: element (channel r, token k) at X[k * p + r]
         const X3Col op{X + k0 * p, p, 0, K};

@@ -19,8 +19,9 @@
 // back by 2^-(e_i + e_j), exactly, before they leave the kernel.
 //
 // Pipeline as nt_tile_x3_wide: wave (wm, wn) owns rows wm * 64 + 32 mi and
-// columns wn * 128 + 32 ni of the tile, K in stages of 16 through three LDS
-// stage buffers, global loads three stages ahead, one barrier per stage.
+// columns wn * 128 + 32 ni of the tile, K in stages of 16 through three or
+// four LDS stage buffers (one barrier per stage, or per two), global loads
+// three stages ahead.
 // Per operand and stage the LDS holds 256 rows of 16 dwords: four 16-byte
 // slots (plane 2 p + half, each 8 k values of one plane) whose order is
 // permuted by row bits 1 to 3, so that any 4, 8 or 16 consecutive lanes of an
@@ -78,12 +79,52 @@ __device__ inline void f2_store_row8(uint32_t* op, const X3Stage& st, float sc)
     *reinterpret_cast<u32x4*>(op + f2_addr(t >> 1, t & 1, 1)) = m;
 }
 
-// A row-per-two-lanes loader (X3Row: channel-major, X3Col: token-major) whose
-// stages are split as above; sc = 2^e of this thread's row.
+// A row-per-two-lanes loader (X3Col: token-major X) whose stages are split as
+// above; sc = 2^e of this thread's row.
 template <class Base>
 struct F2Op : Base {
     float sc;
     __device__ inline void store(uint32_t* op, const X3Stage& st) const { f2_store_row8(op, st, sc); }
+};
+
+// Channel-major operand staged by four lanes per row (512 threads): thread t
+// holds rows t / 4 and t / 4 + 128 at k = 4 (t % 4) .. +3, so that each 16-byte
+// load instruction of a wave covers 16 rows of 64 contiguous bytes (half the
+// cache lines of two lanes per row); sc[h] = 2^e of its two rows.  The planes
+// go to LDS as 8-byte pieces (dwords 2 (k % 2) .. +1 of the slot of half
+// k / 2), which keep the slot layout's reads and writes conflict-free.
+struct F2RowQ {
+    const float* base;
+    int64_t ld;
+    float sc[2];
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const float* src = base + (row0 + (t >> 2)) * ld + k0 + 4 * (t & 3);
+        st.v[0] = *reinterpret_cast<const f32x4*>(src);
+        st.v[1] = *reinterpret_cast<const f32x4*>(src + 128 * ld);
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const int kq = t & 3;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int r = (t >> 2) + 128 * h;
+            u32x2 hp, mp;
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const float x0 = st.v[h][2 * u], x1 = st.v[h][2 * u + 1];
+                const f16x2 hh = __builtin_convertvector((f32x2){x0 * sc[h], x1 * sc[h]}, f16x2);
+                const f16x2 mm = __builtin_convertvector(
+                    (f32x2){fmaf(x0, sc[h], -(float)hh[0]), fmaf(x1, sc[h], -(float)hh[1])}, f16x2);
+                hp[u] = __builtin_bit_cast(uint32_t, hh);
+                mp[u] = __builtin_bit_cast(uint32_t, mm);
+            }
+            *reinterpret_cast<u32x2*>(op + f2_addr(r, kq >> 1, 0) + 2 * (kq & 1)) = hp;
+            *reinterpret_cast<u32x2*>(op + f2_addr(r, kq >> 1, 1) + 2 * (kq & 1)) = mp;
+        }
+    }
 };
 
 __device__ __forceinline__ f16x8 f2_frag(const uint32_t* p)
@@ -193,10 +234,10 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
 }
 
 // The instruction-order hints of f2w_stage pay off for the token-major loader
-// (its sixteen 4-byte loads per stage) and cost 2% for the channel-major one,
+// (its sixteen 4-byte loads per stage) and not for the channel-major one,
 // which the compiler's own order serves better.
 template <class O> struct F2Plain : std::false_type {};
-template <> struct F2Plain<F2Op<X3Row>> : std::true_type {};
+template <> struct F2Plain<F2RowQ> : std::true_type {};
 
 // Stage s = c + R (c a multiple of the unroll, a multiple of 2 and 3): stage
 // s lives in LDS buffer s % NBUF and in register set s % 3; the set that held
