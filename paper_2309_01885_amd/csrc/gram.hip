@@ -309,10 +309,10 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
             for (int v = 0; v < 16; ++v) acc[mi][ni][v] = 0.f;
     if constexpr (F2 && TRANS) {
         // X is n x p; this thread stages channel t / 2 of both panels (eight
-        // tokens); four stage buffers
+        // tokens, buffer loads); four stage buffers
         const int r = threadIdx.x >> 1;
-        const F2Op<X3Col> A{{X + k0 * p, p, 0, K}, ldexpf(1.f, chexp[ti * kWide + r])};
-        const F2Op<X3Col> B{{X + k0 * p, p, 0, K}, ldexpf(1.f, chexp[tj * kWide + r])};
+        const F2ColB A{X + k0 * p, p, ldexpf(1.f, chexp[ti * kWide + r])};
+        const F2ColB B{X + k0 * p, p, ldexpf(1.f, chexp[tj * kWide + r])};
         nt_tile_f2_wide<4>(A, ti * kWide, B, tj * kWide, K, lds, acc);
     } else if constexpr (F2) {
         // this thread stages channels t / 4 and t / 4 + 128 of both panels

@@ -30,7 +30,6 @@
 // whether the 16-byte accesses are served 4, 8 or 16 lanes at a time.
 #pragma once
 
-#include <type_traits>
 #include <utility>
 
 #include "nt_x3.h"
@@ -79,14 +78,6 @@ __device__ inline void f2_store_row8(uint32_t* op, const X3Stage& st, float sc)
     *reinterpret_cast<u32x4*>(op + f2_addr(t >> 1, t & 1, 1)) = m;
 }
 
-// A row-per-two-lanes loader (X3Col: token-major X) whose stages are split as
-// above; sc = 2^e of this thread's row.
-template <class Base>
-struct F2Op : Base {
-    float sc;
-    __device__ inline void store(uint32_t* op, const X3Stage& st) const { f2_store_row8(op, st, sc); }
-};
-
 // Channel-major operand staged by four lanes per row (512 threads): thread t
 // holds rows t / 4 and t / 4 + 128 at k = 4 (t % 4) .. +3, so that each 16-byte
 // load instruction of a wave covers 16 rows of 64 contiguous bytes (half the
@@ -127,6 +118,29 @@ struct F2RowQ {
     }
 };
 
+// Token-major operand with X3Col's staging (thread t: channel t / 2 at eight
+// tokens), read through a buffer descriptor per stage: one 32-bit offset per
+// thread and the token steps as scalar offsets, instead of eight 64-bit
+// addresses.  base = the launch's first token row, ld = p; the descriptor
+// covers the stage's 16 token rows (reads outside it return 0).
+struct F2ColB {
+    const float* base;
+    int64_t ld;
+    float sc;
+    __device__ inline void load_full(int64_t row0, int64_t k0, X3Stage& st) const
+    {
+        const int t = threadIdx.x;
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<float*>(base + k0 * ld), 0, (int)(16 * ld * 4), 0x00020000);
+        const int vo = (int)((8 * (t & 1) * ld + row0 + (t >> 1)) * 4);
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+            st.v[u >> 2][u & 3] = __builtin_bit_cast(
+                float, __builtin_amdgcn_raw_buffer_load_b32(rs, vo, (int)(u * ld * 4), 0));
+    }
+    __device__ inline void store(uint32_t* op, const X3Stage& st) const { f2_store_row8(op, st, sc); }
+};
+
 __device__ __forceinline__ f16x8 f2_frag(const uint32_t* p)
 {
     return __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4*>(p));
@@ -152,7 +166,7 @@ __device__ __forceinline__ void f2w_block(const f16x8 (&a)[2][2], const f16x8 (&
 // stage kload into (la, lb), and leaves fa and fb[0] holding the fragments of
 // `nxt` (stage c + 1).  offa[pl] / offb[pl]: this lane's plane-pl fragment of
 // row block 0 (further blocks of 32 rows keep the slot permutation).
-template <bool SYNC, bool HINTS, class OA, class OB>
+template <bool SYNC, class OA, class OB>
 __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& B, int64_t row0b,
                                           int64_t kload, const uint32_t* cur, const uint32_t* nxt,
                                           uint32_t* wr, X3Stage& ga, X3Stage& gb, X3Stage& la,
@@ -167,41 +181,18 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
     for (int pl = 0; pl < 2; ++pl) fb[1][pl] = f2_frag(cur + offb[pl] + 1 * BLK);
     f2w_block(fa, fb[0], acc, 0);
     A.store(wr, ga);
-    if constexpr (HINTS) {
-        __builtin_amdgcn_sched_group_barrier(0x020, 4, 0);     // VMEM reads
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);     // DS reads
-#pragma unroll
-        for (int i = 0; i < 6; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);     // VALU
-        }
-        __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);     // DS writes
-    }
     __builtin_amdgcn_sched_barrier(0);
     // group 1: B block 2 reads, split of B
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) fb[0][pl] = f2_frag(cur + offb[pl] + 2 * BLK);
     f2w_block(fa, fb[1], acc, 1);
     B.store(wr + kF2OpDw, gb);
-    if constexpr (HINTS) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-#pragma unroll
-        for (int i = 0; i < 6; ++i) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
-        }
-        __builtin_amdgcn_sched_group_barrier(0x200, 2, 0);
-    }
     __builtin_amdgcn_sched_barrier(0);
     // group 2: B block 3 reads; with SYNC, the barrier makes the stages written
     // so far visible and ends the reads of the stages multiplied so far
 #pragma unroll
     for (int pl = 0; pl < 2; ++pl) fb[1][pl] = f2_frag(cur + offb[pl] + 3 * BLK);
     f2w_block(fa, fb[0], acc, 2);
-    if constexpr (HINTS) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 6, 0);
-    }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (SYNC) __syncthreads();
     // group 3: next stage's B block 0 and A fragments, each after its last use
@@ -223,21 +214,8 @@ __device__ __forceinline__ void f2w_stage(const OA& A, int64_t row0a, const OB& 
             }
         }
     }
-    if constexpr (HINTS) {
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
-        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
-    }
     __builtin_amdgcn_sched_barrier(0);
 }
-
-// The instruction-order hints of f2w_stage pay off for the token-major loader
-// (its sixteen 4-byte loads per stage) and not for the channel-major one,
-// which the compiler's own order serves better.
-template <class O> struct F2Plain : std::false_type {};
-template <> struct F2Plain<F2RowQ> : std::true_type {};
 
 // Stage s = c + R (c a multiple of the unroll, a multiple of 2 and 3): stage
 // s lives in LDS buffer s % NBUF and in register set s % 3; the set that held
@@ -256,7 +234,7 @@ __device__ __forceinline__ void f2w_stage_r(const OA& A, int64_t row0a, const OB
                                             f16x8 (&fa)[2][2], f16x8 (&fb)[2][2],
                                             f32x16 (&acc)[2][4])
 {
-    f2w_stage<NBUF == 3 || (R & 1), !F2Plain<OA>::value>(
+    f2w_stage<NBUF == 3 || (R & 1)>(
         A, row0a, B, row0b, min(c + R + 4, nst - 1) * kX3KC, lds + (R % NBUF) * kF2BufDw,
         lds + ((R + 1) % NBUF) * kF2BufDw, lds + ((R + 2) % NBUF) * kF2BufDw, ga[(R + 2) % 3],
         gb[(R + 2) % 3], ga[(R + 1) % 3], gb[(R + 1) % 3], offa, offb, fa, fb, acc);
