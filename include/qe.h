@@ -116,13 +116,13 @@ qe_status qe_sync_status(void* ws, void* stream);
  * Sigma: p x p fp32, device; overwritten (accumulate = 0) or added to
  * (accumulate = 1, for token chunks streamed through several calls; pass
  * damp = 0 on all but the last).  The result is exactly symmetric.
- * Products, by default: when p is a multiple of 256, X's rows are 16-byte
- * aligned, n is a multiple of 32 (token-major X: all but its last n % 32
- * tokens) and either the split partials fit the workspace or n <= 32768 (at
- * very large p, stream longer token ranges in chunks of at most 32768), each
- * channel i is first scaled by 2^e_i (exact; its largest |x| lands in
- * [2^14, 2^15), a pass over X; e_i at most 127) and each scaled value y is
- * split into two fp16 values
+ * Products, by default: when p is a multiple of 256 (at most 2^24), X's rows
+ * are 16-byte aligned, n is a multiple of 32 (token-major X: all but its last
+ * n % 32 tokens) and either the split partials fit the workspace or
+ * n <= 32768 (at very large p, stream longer token ranges in chunks of at
+ * most 32768), each channel i is first scaled by 2^e_i (exact; its largest |x|
+ * lands in [2^14, 2^15), a pass over X; e_i at most 127) and each scaled value
+ * y is split into two fp16 values
  * (h = fp16(y), m = fp16(y - h)); y_i y_j is formed from the three products
  * h h, h m, m h on the fp16 matrix cores, every product exact in fp32, and
  * the sums are scaled back by 2^-(e_i + e_j).  The dropped terms are below

@@ -289,8 +289,8 @@ __global__ __launch_bounds__(512, 1) void gram_x3w_kernel(
 {
     if (failed(status)) return;
     // the direct mode also stages a finished 128 x kTStride quadrant here
-    static_assert(kTile * kTStride <= kF2LdsDw && kTile * kTStride <= kX3wLdsDw, "quadrant fits");
-    __shared__ __attribute__((aligned(16))) uint32_t lds[F2 ? kF2LdsDw : kX3wLdsDw];
+    static_assert(kTile * kTStride <= 3 * kF2BufDw && kTile * kTStride <= kX3wLdsDw, "quadrant fits");
+    __shared__ __attribute__((aligned(16))) uint32_t lds[F2 ? (TRANS ? 4 : 3) * kF2BufDw : kX3wLdsDw];
     const int64_t items = tiles_w * splits;
     const int64_t per = cdiv(items, 8);
     const int64_t item = (int64_t)(blockIdx.x % 8) * per + blockIdx.x / 8;
@@ -633,7 +633,8 @@ static qe_status launch_gram_one(const float* X, int64_t p, int64_t n, int layou
     const int64_t tiles = nt * (nt + 1) / 2;
     const int64_t splits = gram_splits(p, n);
     const bool fp32 = (layout & QE_GRAM_FP32) != 0;
-    const bool f2 = (layout & QE_GRAM_BF16X3) == 0;
+    // the fp16 split (its token-major loader's buffer offsets are 32-bit)
+    const bool f2 = (layout & QE_GRAM_BF16X3) == 0 && p <= (int64_t(1) << 24);
     const bool trans = (layout & ~(QE_GRAM_FP32 | QE_GRAM_BF16X3)) == QE_LAYOUT_NP;
     // 16-byte loads need an aligned base and a row stride that keeps them aligned
     const int x_vec4 = aligned16(X) && ((trans ? p : n) % 4 == 0);

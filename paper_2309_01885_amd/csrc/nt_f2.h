@@ -39,7 +39,6 @@ namespace qe {
 constexpr int kF2RowDw = 16;                      // h, m: 8 dwords each
 constexpr int kF2OpDw = 256 * kF2RowDw;           // one operand of one stage
 constexpr int kF2BufDw = 2 * kF2OpDw;             // A and B of one stage
-constexpr int kF2LdsDw = 4 * kF2BufDw;            // four stages: 131,072 bytes
 
 typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
