@@ -189,3 +189,33 @@ def test_gram_heavy_tailed_with_outlier_channels(qe, oracle):
     S = _gram(qe, X, damp=0.01)
     ref = oracle.damp(oracle.gram(X), 0.01)
     assert rel_fro(S, ref) <= 1e-5
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("layout,n", [(1, 2048 + 17), (0, 2048 + 32)])
+def test_gram_direct_mode_large_p(qe, oracle, layout, n):
+    """33024 channels: the split partials of 33411 128 x 128 tiles would
+    exceed the 2 GB budget, so each call writes Sigma directly (256 x 256
+    tiles, the fp16 split); token-major with a 17-token tail on the 128 x 128
+    tiles.  A seeded block of 256 channels and every diagonal entry against
+    the oracle's fp64 sums of the same numbers; the block exactly symmetric."""
+    p = 33024
+    ws = qe.load().qe_gram_workspace_size(p, n)
+    assert ws < (64 << 20)                       # no split partials: direct mode
+    rng = np.random.default_rng(41)
+    X = rng.standard_t(4, size=(p, n)).astype(np.float32)
+    X[rng.choice(p, 300, replace=False)] *= 30.0
+    idx = np.sort(rng.choice(p, 256, replace=False))
+    Xl = X if layout == 0 else np.ascontiguousarray(X.T)
+    S = qe.gram(dev(Xl), layout=layout)
+    idx_d = torch.as_tensor(idx, device="cuda")
+    block = host(S[idx_d][:, idx_d])
+    blockT = host(S[:, idx_d][idx_d])
+    diag = host(torch.diagonal(S)).astype(np.float64)
+    del S
+    torch.cuda.empty_cache()
+    ref_block = oracle.gram(X[idx])
+    ref_diag = np.einsum("ij,ij->i", X.astype(np.float64), X.astype(np.float64))
+    assert np.array_equal(block, blockT.T)
+    assert rel_fro(block, ref_block) <= 1e-5
+    assert np.max(np.abs(diag - ref_diag) / ref_diag) <= 1e-5
