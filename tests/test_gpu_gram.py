@@ -192,13 +192,15 @@ def test_gram_heavy_tailed_with_outlier_channels(qe, oracle):
 
 
 @pytest.mark.timeout(600)
+@pytest.mark.parametrize("mode", ["default", "bf16x3"])
 @pytest.mark.parametrize("layout,n", [(1, 2048 + 17), (0, 2048 + 32)])
-def test_gram_direct_mode_large_p(qe, oracle, layout, n):
+def test_gram_direct_mode_large_p(qe, oracle, layout, n, mode):
     """33024 channels: the split partials of 33411 128 x 128 tiles would
     exceed the 2 GB budget, so each call writes Sigma directly (256 x 256
-    tiles, the fp16 split); token-major with a 17-token tail on the 128 x 128
-    tiles.  A seeded block of 256 channels and every diagonal entry against
-    the oracle's fp64 sums of the same numbers; the block exactly symmetric."""
+    tiles, the fp16 split or, with QE_GRAM_BF16X3, the bf16 one); token-major
+    with a 17-token tail on the 128 x 128 tiles.  A seeded block of 256
+    channels and every diagonal entry against the oracle's fp64 sums of the
+    same numbers; the block exactly symmetric."""
     p = 33024
     ws = qe.load().qe_gram_workspace_size(p, n)
     assert ws < (64 << 20)                       # no split partials: direct mode
@@ -207,7 +209,7 @@ def test_gram_direct_mode_large_p(qe, oracle, layout, n):
     X[rng.choice(p, 300, replace=False)] *= 30.0
     idx = np.sort(rng.choice(p, 256, replace=False))
     Xl = X if layout == 0 else np.ascontiguousarray(X.T)
-    S = qe.gram(dev(Xl), layout=layout)
+    S = qe.gram(dev(Xl), layout=layout, bf16x3=mode == "bf16x3")
     idx_d = torch.as_tensor(idx, device="cuda")
     block = host(S[idx_d][:, idx_d])
     blockT = host(S[:, idx_d][idx_d])
